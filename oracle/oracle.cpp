@@ -1,0 +1,443 @@
+// PinSage CPU oracle — TEST INFRASTRUCTURE ONLY.
+//
+// A plain, slow, obviously-correct CPU statement of what the PinSage hot path
+// computes (Ying et al., "Graph Convolutional Neural Networks for Web-Scale
+// Recommender Systems", KDD 2018). Only the test-suite, the smoke check and the
+// benchmark's CPU-baseline leg may load this library; the product path never
+// does. It shares no code, header or constant table with the GPU library.
+//
+// Every function below follows one passage of the paper, cited in its comment:
+//   * Philox4x32-10 .......... Salmon et al., SC'11 ("Parallel random numbers:
+//                              as easy as 1, 2, 3"), Sec. 3.2 + Table 2.
+//   * random walks / counts .. Sec. 3.2, "Importance-based neighborhoods".
+//   * top-T + L1 weights ..... Sec. 3.2, same paragraph and "importance pooling".
+//   * CONVOLVE ............... Sec. 3.2, Algorithm 1 (lines 1-3).
+//   * stacked layers ......... Sec. 3.2, "Stacking convolutions".
+//   * layer-wise inference ... Sec. 3.4 (project every pin once, then pool).
+//   * MINIBATCH sets + loop .. Sec. 3.2, Algorithm 2 (sampling and embedding).
+//   * max-margin loss ........ Sec. 3.3, Eq. (1).
+//
+// Readings of points the paper leaves open are listed in the repository's
+// design notes; the ones that change arithmetic are restated at each function.
+// All floating point is fp64 except the importance weights, which the method
+// stores as fp32 (one fp32 division c/S per weight).
+//
+// Parity pins: every exported function is pinned by a CPU test against an
+// independent statement (published known-answer vectors, a library routine,
+// closed-form expectations, brute force or a special case); see tests/.
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <set>
+#include <thread>
+#include <utility>
+#include <vector>
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11). One round maps the 128-bit counter
+// (c0,c1,c2,c3) with 64-bit key (k0,k1) to
+//   (hi(M1*c2) ^ c1 ^ k0,  lo(M1*c2),  hi(M0*c0) ^ c3 ^ k1,  lo(M0*c0))
+// and the key is bumped by the Weyl constants between rounds.
+// ---------------------------------------------------------------------------
+const uint32_t kPhiloxM0 = 0xD2511F53u;
+const uint32_t kPhiloxM1 = 0xCD9E8D57u;
+const uint32_t kWeyl0 = 0x9E3779B9u;  // golden ratio
+const uint32_t kWeyl1 = 0xBB67AE85u;  // sqrt(3) - 1
+
+void philox4x32_10(const uint32_t in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  uint32_t c[4] = {in[0], in[1], in[2], in[3]};
+  uint32_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    uint64_t p0 = (uint64_t)kPhiloxM0 * (uint64_t)c[0];
+    uint64_t p1 = (uint64_t)kPhiloxM1 * (uint64_t)c[2];
+    uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    uint32_t n0 = hi1 ^ c[1] ^ k0;
+    uint32_t n1 = lo1;
+    uint32_t n2 = hi0 ^ c[3] ^ k1;
+    uint32_t n3 = lo0;
+    c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+    k0 += kWeyl0;
+    k1 += kWeyl1;
+  }
+  out[0] = c[0]; out[1] = c[1]; out[2] = c[2]; out[3] = c[3];
+}
+
+// The random word used at edge step s of walk w from source u.
+// Stream layout (a reading; the paper does not fix one): counter
+// (u, w, s/4, 0), key (lo32(seed), hi32(seed)); step s uses output word s%4.
+uint32_t walk_word(uint64_t seed, uint32_t u, uint32_t w, uint32_t s) {
+  uint32_t ctr[4] = {u, w, s / 4u, 0u};
+  uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+  uint32_t out[4];
+  philox4x32_10(ctr, key, out);
+  return out[s % 4u];
+}
+
+struct Graph {
+  const int64_t* off;   // [num_nodes + 1]
+  const int32_t* col;   // [off[num_nodes]]
+  int64_t num_pins;     // pins are ids [0, num_pins)
+  int64_t num_nodes;    // boards are ids [num_pins, num_nodes)
+};
+
+// Sec. 3.2, importance-based neighbourhoods: simulate random walks from u and
+// record every pin the walk lands on. Readings: each walk is unbiased (the next
+// node is a uniformly chosen CSR neighbour; the draw maps the 32-bit word r to
+// index floor(r*deg / 2^32)), a walk ends after `hops` landings on a pin, after
+// 2*hops edge steps, or at a node with no edges; the source itself is not
+// recorded. Appends visited pin ids to `visits`; returns edge steps taken.
+int64_t walk_from(const Graph& g, uint64_t seed, int64_t u, int walks, int hops,
+                  std::vector<int32_t>& visits) {
+  int64_t steps = 0;
+  for (int w = 0; w < walks; ++w) {
+    int64_t cur = u;
+    int landed = 0;
+    int s = 0;
+    while (landed < hops && s < 2 * hops) {
+      int64_t deg = g.off[cur + 1] - g.off[cur];
+      if (deg <= 0) break;
+      uint32_t r = walk_word(seed, (uint32_t)u, (uint32_t)w, (uint32_t)s);
+      int64_t j = (int64_t)(((uint64_t)r * (uint64_t)deg) >> 32);
+      cur = g.col[g.off[cur] + j];
+      ++s;
+      if (cur < g.num_pins) {
+        ++landed;
+        if (cur != u) visits.push_back((int32_t)cur);
+      }
+    }
+    steps += s;
+  }
+  return steps;
+}
+
+// Sec. 3.2: the neighbourhood is the T pins with the highest visit counts;
+// importance pooling weights them by their L1-normalised counts. Readings:
+// ties are broken by the lower node id, and the L1 normalisation runs over the
+// kept T counts, so the weights of a row sum to one (the weighted mean is the
+// same under either normalisation). Rows with fewer than T distinct pins are
+// padded with (-1, 0, 0.0f).
+void select_top_t(const std::vector<int32_t>& visits, int T, int32_t* idx, uint16_t* cnt,
+                  float* wts) {
+  std::map<int32_t, int64_t> counts;
+  for (int32_t v : visits) counts[v] += 1;
+  std::vector<std::pair<int64_t, int32_t>> order;  // (count, id)
+  for (const auto& kv : counts) order.push_back({kv.second, kv.first});
+  std::sort(order.begin(), order.end(),
+            [](const std::pair<int64_t, int32_t>& a, const std::pair<int64_t, int32_t>& b) {
+              if (a.first != b.first) return a.first > b.first;  // more visits first
+              return a.second < b.second;                        // then lower id
+            });
+  int keep = (int)std::min<size_t>((size_t)T, order.size());
+  int64_t total = 0;
+  for (int t = 0; t < keep; ++t) total += order[t].first;
+  for (int t = 0; t < T; ++t) {
+    if (t < keep) {
+      idx[t] = order[t].second;
+      cnt[t] = (uint16_t)order[t].first;
+      float c = (float)order[t].first;
+      float s = (float)total;
+      wts[t] = c / s;  // one IEEE fp32 division, round-to-nearest-even
+    } else {
+      idx[t] = -1;
+      cnt[t] = 0;
+      wts[t] = 0.0f;
+    }
+  }
+}
+
+template <typename F>
+void parallel_rows(int64_t n, int nthreads, F fn) {
+  if (nthreads <= 1 || n < 2) {
+    fn((int64_t)0, n);
+    return;
+  }
+  std::vector<std::thread> pool;
+  int64_t per = (n + nthreads - 1) / nthreads;
+  for (int t = 0; t < nthreads; ++t) {
+    int64_t lo = t * per, hi = std::min(n, lo + per);
+    if (lo >= hi) break;
+    pool.emplace_back([=]() { fn(lo, hi); });
+  }
+  for (auto& th : pool) th.join();
+}
+
+// Algorithm 1, line 1 for one neighbour: ReLU(Q h_v + q), Q is [m x d_in].
+void transform_row(const double* h, int d_in, const double* Q, const double* q, int m,
+                   double* out) {
+  for (int i = 0; i < m; ++i) {
+    double acc = 0.0;
+    for (int j = 0; j < d_in; ++j) acc += Q[(int64_t)i * d_in + j] * h[j];
+    acc += q[i];
+    out[i] = acc > 0.0 ? acc : 0.0;
+  }
+}
+
+// Algorithm 1, lines 2-3: z = ReLU(W concat(h_u, n_u) + w); z / ||z||_2.
+// W is [d_out x (d_in + m)]: the first d_in columns multiply the node's own
+// vector, the remaining m columns multiply the pooled neighbourhood vector.
+// A zero z (all pre-activations <= 0) stays zero (the paper divides without a
+// guard; this case does not arise with the workloads here).
+void combine_row(const double* h_self, int d_in, const double* n_u, int m, const double* W,
+                 const double* w, int d_out, double* out) {
+  const int K = d_in + m;
+  double sq = 0.0;
+  for (int o = 0; o < d_out; ++o) {
+    double acc = 0.0;
+    for (int j = 0; j < d_in; ++j) acc += W[(int64_t)o * K + j] * h_self[j];
+    for (int j = 0; j < m; ++j) acc += W[(int64_t)o * K + d_in + j] * n_u[j];
+    acc += w[o];
+    double z = acc > 0.0 ? acc : 0.0;
+    out[o] = z;
+    sq += z * z;
+  }
+  double norm = std::sqrt(sq);
+  for (int o = 0; o < d_out; ++o) out[o] = norm > 0.0 ? out[o] / norm : 0.0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int orc_version(void) { return 1; }
+
+// Philox4x32-10 block function, exposed for known-answer tests.
+void orc_philox4x32_10(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
+  philox4x32_10(ctr, key, out);
+}
+
+uint32_t orc_walk_word(uint64_t seed, uint32_t u, uint32_t w, uint32_t s) {
+  return walk_word(seed, u, w, s);
+}
+
+// Raw visit list of one source (for brute-force checks of the selection step).
+// visits_out must hold walks*hops entries; returns the number written, and the
+// edge steps taken in *steps.
+int64_t orc_walk_visits(const int64_t* off, const int32_t* col, int64_t num_pins,
+                        int64_t num_nodes, uint64_t seed, int64_t u, int walks, int hops,
+                        int32_t* visits_out, int64_t* steps) {
+  Graph g{off, col, num_pins, num_nodes};
+  std::vector<int32_t> v;
+  int64_t s = walk_from(g, seed, u, walks, hops, v);
+  for (size_t i = 0; i < v.size(); ++i) visits_out[i] = v[i];
+  if (steps) *steps = s;
+  return (int64_t)v.size();
+}
+
+// Importance neighbourhoods (Sec. 3.2) for sources[0..num_sources), or for
+// every node when sources is NULL. Outputs are [num_sources x T], row r
+// belonging to sources[r]. *total_steps receives the edge steps of all walks.
+void orc_build_neighborhoods(const int64_t* off, const int32_t* col, int64_t num_pins,
+                             int64_t num_nodes, uint64_t seed, int walks, int hops, int T,
+                             const int32_t* sources, int64_t num_sources, int32_t* idx,
+                             uint16_t* cnt, float* wts, int64_t* total_steps, int nthreads) {
+  Graph g{off, col, num_pins, num_nodes};
+  std::vector<int64_t> steps_per_thread(std::max(1, nthreads), 0);
+  std::vector<int64_t> chunk_steps;
+  int nt = std::max(1, nthreads);
+  int64_t per = (num_sources + nt - 1) / nt;
+  std::vector<std::thread> pool;
+  for (int t = 0; t < nt; ++t) {
+    int64_t lo = t * per, hi = std::min(num_sources, lo + per);
+    if (lo >= hi) break;
+    auto body = [&, t, lo, hi]() {
+      std::vector<int32_t> visits;
+      int64_t acc = 0;
+      for (int64_t r = lo; r < hi; ++r) {
+        int64_t u = sources ? (int64_t)sources[r] : r;
+        visits.clear();
+        acc += walk_from(g, seed, u, walks, hops, visits);
+        select_top_t(visits, T, idx + r * T, cnt + r * T, wts + r * T);
+      }
+      steps_per_thread[t] = acc;
+    };
+    if (nt == 1) body(); else pool.emplace_back(body);
+  }
+  for (auto& th : pool) th.join();
+  int64_t total = 0;
+  for (int64_t s : steps_per_thread) total += s;
+  if (total_steps) *total_steps = total;
+}
+
+// One CONVOLVE layer over a set of output rows, in the layer-wise dataflow of
+// Sec. 3.4: rows [0, n_transform) of h_in are projected once each with
+// Algorithm 1 line 1, then every output row pools its neighbours (importance
+// pooling: sum_t alpha_t * P[idx_t], Sec. 3.2) and applies lines 2-3.
+// h_out row r uses h_in row self_rows[r] (or r when self_rows is NULL).
+// Neighbour ids < 0 are padding and are skipped.
+void orc_convolve_layer(const double* h_in, int64_t n_in, int d_in, int64_t n_transform,
+                        const double* Q, const double* q, int m, const double* W,
+                        const double* w, int d_out, const int32_t* idx, const float* wts, int T,
+                        const int64_t* self_rows, int64_t n_out, double* h_out, int nthreads) {
+  (void)n_in;
+  std::vector<double> P((size_t)n_transform * (size_t)m);
+  parallel_rows(n_transform, nthreads, [&](int64_t lo, int64_t hi) {
+    for (int64_t v = lo; v < hi; ++v)
+      transform_row(h_in + v * d_in, d_in, Q, q, m, P.data() + v * m);
+  });
+  parallel_rows(n_out, nthreads, [&](int64_t lo, int64_t hi) {
+    std::vector<double> n_u((size_t)m);
+    for (int64_t r = lo; r < hi; ++r) {
+      std::fill(n_u.begin(), n_u.end(), 0.0);
+      for (int t = 0; t < T; ++t) {
+        int32_t v = idx[r * T + t];
+        if (v < 0) continue;
+        double a = (double)wts[r * T + t];
+        const double* pv = P.data() + (int64_t)v * m;
+        for (int i = 0; i < m; ++i) n_u[i] += a * pv[i];
+      }
+      int64_t self = self_rows ? self_rows[r] : r;
+      combine_row(h_in + self * d_in, d_in, n_u.data(), m, W, w, d_out, h_out + r * d_out);
+    }
+  });
+}
+
+// Algorithm 2, sampling part: S^(K) = M; S^(k-1) = S^(k) united with N(u) for
+// every u in S^(k). N(u) is read from a neighbourhood table with one row per
+// node (nbr_idx[u*T + t], padding < 0). Writes the sorted node ids of S^(k)
+// for k = 0..K into `sets` (concatenated, S^(0) first) and their sizes into
+// set_sizes[0..K]. Returns the total length, or -(required length) when
+// `cap` is too small (nothing written then).
+int64_t orc_minibatch_sets(const int32_t* targets, int64_t num_targets, int K,
+                           const int32_t* nbr_idx, int T, int64_t* set_sizes, int32_t* sets,
+                           int64_t cap) {
+  std::vector<std::set<int32_t>> S(K + 1);
+  for (int64_t i = 0; i < num_targets; ++i) S[K].insert(targets[i]);
+  for (int k = K; k >= 1; --k) {
+    S[k - 1] = S[k];
+    for (int32_t u : S[k])
+      for (int t = 0; t < T; ++t) {
+        int32_t v = nbr_idx[(int64_t)u * T + t];
+        if (v >= 0) S[k - 1].insert(v);
+      }
+  }
+  int64_t total = 0;
+  for (int k = 0; k <= K; ++k) total += (int64_t)S[k].size();
+  if (total > cap) return -total;
+  int64_t pos = 0;
+  for (int k = 0; k <= K; ++k) {
+    set_sizes[k] = (int64_t)S[k].size();
+    for (int32_t v : S[k]) sets[pos++] = v;
+  }
+  return total;
+}
+
+// Algorithm 2, embedding part, for the target set M: h^(0)_u = x_u on S^(0);
+// for k = 1..K every u in S^(k) gets CONVOLVE^(k)(h^(k-1)_u, {h^(k-1)_v : v in
+// N(u)}). Each neighbour's Algorithm-1 line-1 vector depends only on (k, v), so
+// it is evaluated once per distinct v within a layer. Layer parameters are
+// packed per layer: Qs[k] is [m_k x d_k], Ws[k] is [d_{k+1} x (d_k + m_k)].
+// x holds the features of every node (row v is node v). Outputs h^(K) for the
+// targets in the given order.
+void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, const double* x,
+                         int d0, const int32_t* nbr_idx, const float* nbr_w, int T,
+                         const double* const* Qs, const double* const* qs, const int* ms,
+                         const double* const* Ws, const double* const* ws, const int* d_outs,
+                         double* out, int nthreads) {
+  // Sampling (lines 1-6).
+  std::vector<std::vector<int32_t>> S(K + 1);
+  {
+    std::vector<std::set<int32_t>> Sset(K + 1);
+    for (int64_t i = 0; i < num_targets; ++i) Sset[K].insert(targets[i]);
+    for (int k = K; k >= 1; --k) {
+      Sset[k - 1] = Sset[k];
+      for (int32_t u : Sset[k])
+        for (int t = 0; t < T; ++t) {
+          int32_t v = nbr_idx[(int64_t)u * T + t];
+          if (v >= 0) Sset[k - 1].insert(v);
+        }
+    }
+    for (int k = 0; k <= K; ++k) S[k].assign(Sset[k].begin(), Sset[k].end());
+  }
+  // h^(0) on S^(0) (line 7).
+  std::map<int32_t, int64_t> pos_prev;  // node -> row in h_prev
+  std::vector<double> h_prev((size_t)S[0].size() * d0);
+  for (size_t i = 0; i < S[0].size(); ++i) {
+    pos_prev[S[0][i]] = (int64_t)i;
+    std::memcpy(h_prev.data() + i * d0, x + (int64_t)S[0][i] * d0, sizeof(double) * d0);
+  }
+  int d_prev = d0;
+  // Lines 8-12.
+  for (int k = 1; k <= K; ++k) {
+    const int m = ms[k - 1], d_out = d_outs[k - 1];
+    const double* Q = Qs[k - 1];
+    const double* q = qs[k - 1];
+    const double* W = Ws[k - 1];
+    const double* w = ws[k - 1];
+    // Line-1 vectors for every neighbour needed at this layer, once each.
+    std::vector<int32_t> need;
+    {
+      std::set<int32_t> ns;
+      for (int32_t u : S[k])
+        for (int t = 0; t < T; ++t) {
+          int32_t v = nbr_idx[(int64_t)u * T + t];
+          if (v >= 0) ns.insert(v);
+        }
+      need.assign(ns.begin(), ns.end());
+    }
+    std::map<int32_t, int64_t> pos_need;
+    for (size_t i = 0; i < need.size(); ++i) pos_need[need[i]] = (int64_t)i;
+    std::vector<double> Pn(need.size() * (size_t)m);
+    parallel_rows((int64_t)need.size(), nthreads, [&](int64_t lo, int64_t hi) {
+      for (int64_t i = lo; i < hi; ++i)
+        transform_row(h_prev.data() + pos_prev.at(need[i]) * d_prev, d_prev, Q, q, m,
+                      Pn.data() + i * m);
+    });
+    std::vector<double> h_next(S[k].size() * (size_t)d_out);
+    parallel_rows((int64_t)S[k].size(), nthreads, [&](int64_t lo, int64_t hi) {
+      std::vector<double> n_u((size_t)m);
+      for (int64_t i = lo; i < hi; ++i) {
+        int32_t u = S[k][i];
+        std::fill(n_u.begin(), n_u.end(), 0.0);
+        for (int t = 0; t < T; ++t) {
+          int32_t v = nbr_idx[(int64_t)u * T + t];
+          if (v < 0) continue;
+          double a = (double)nbr_w[(int64_t)u * T + t];
+          const double* pv = Pn.data() + pos_need.at(v) * m;
+          for (int j = 0; j < m; ++j) n_u[j] += a * pv[j];
+        }
+        combine_row(h_prev.data() + pos_prev.at(u) * d_prev, d_prev, n_u.data(), m, W, w,
+                    d_out, h_next.data() + i * d_out);
+      }
+    });
+    std::map<int32_t, int64_t> pos_next;
+    for (size_t i = 0; i < S[k].size(); ++i) pos_next[S[k][i]] = (int64_t)i;
+    h_prev.swap(h_next);
+    pos_prev.swap(pos_next);
+    d_prev = d_out;
+  }
+  for (int64_t i = 0; i < num_targets; ++i)
+    std::memcpy(out + i * d_prev, h_prev.data() + pos_prev.at(targets[i]) * d_prev,
+                sizeof(double) * d_prev);
+}
+
+// Eq. (1), Sec. 3.3: for each pair (q, i), the expectation over negatives of
+// max(0, z_q.z_n - z_q.z_i + margin). Readings: the expectation is the mean
+// over the shared negative set, and the minibatch loss is the mean over pairs.
+// Returns the minibatch loss; per_pair (nullable) receives each pair's term.
+double orc_max_margin_loss(const double* zq, const double* zpos, int64_t B, const double* zneg,
+                           int64_t n_neg, int d, double margin, double* per_pair) {
+  double total = 0.0;
+  for (int64_t b = 0; b < B; ++b) {
+    double pos = 0.0;
+    for (int j = 0; j < d; ++j) pos += zq[b * d + j] * zpos[b * d + j];
+    double acc = 0.0;
+    for (int64_t n = 0; n < n_neg; ++n) {
+      double neg = 0.0;
+      for (int j = 0; j < d; ++j) neg += zq[b * d + j] * zneg[n * d + j];
+      double v = neg - pos + margin;
+      acc += v > 0.0 ? v : 0.0;
+    }
+    double term = n_neg > 0 ? acc / (double)n_neg : 0.0;
+    if (per_pair) per_pair[b] = term;
+    total += term;
+  }
+  return B > 0 ? total / (double)B : 0.0;
+}
+
+}  // extern "C"
