@@ -1,0 +1,206 @@
+/*
+ * pinsage.h -- C ABI of libpinsage.so, the MI355X (gfx950) hot path of PinSage
+ * (Ying et al., "Graph Convolutional Neural Networks for Web-Scale Recommender
+ * Systems", KDD 2018).
+ *
+ * The library computes, on one GPU:
+ *   1. importance neighbourhoods by short random walks (Sec. 3.2,
+ *      "Importance-based neighborhoods"), and
+ *   2. K stacked CONVOLVE layers (Algorithm 1) over every node, evaluated
+ *      layer by layer so that each node's transformed vector is computed once
+ *      (Sec. 3.4),
+ *   3. the minibatch forward of Algorithm 2 with the max-margin loss (Eq. 1).
+ *
+ * Conventions shared by every entry point
+ *   - Graph (Sec. 3.1): a bipartite graph of pins I and boards C, V = I u C.
+ *     Node ids: pins are [0, num_pins), boards are [num_pins, num_nodes).
+ *     Undirected CSR holding both directions; each row sorted ascending.
+ *   - Pointers named "device" must be device memory (or memory the device can
+ *     read); all buffers are owned by the caller. The library keeps no device
+ *     allocation between calls except what is documented per entry point.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream). No call synchronises the host unless stated.
+ *   - Arguments are validated on the host before any HIP call; a bad argument
+ *     returns PINSAGE_EINVAL / PINSAGE_EUNSUPPORTED / PINSAGE_EWORKSPACE and
+ *     launches nothing. HIP failures return PINSAGE_EHIP; the message is in
+ *     pinsage_last_error() (thread-local).
+ *   - Results are deterministic: the same inputs give the same bits.
+ *   - Matrices are row-major. Storage dtype is fp32 or bf16; every sum is
+ *     accumulated in fp32; biases are fp32.
+ */
+#ifndef PINSAGE_H_
+#define PINSAGE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PINSAGE_ABI_VERSION 1
+
+enum {
+  PINSAGE_OK = 0,
+  PINSAGE_EINVAL = -1,       /* malformed argument (NULL, size, mismatch)    */
+  PINSAGE_EUNSUPPORTED = -2, /* well-formed but outside the supported limits */
+  PINSAGE_EWORKSPACE = -3,   /* workspace smaller than the size query says   */
+  PINSAGE_EHIP = -4          /* a HIP runtime call failed                    */
+};
+
+typedef enum { PINSAGE_I32 = 0, PINSAGE_I64 = 1 } pinsage_index_t;
+typedef enum { PINSAGE_F32 = 0, PINSAGE_BF16 = 1 } pinsage_dtype_t;
+
+/* Bipartite pin-board graph (Sec. 3.1). row_offsets: device, num_nodes + 1
+ * entries of offset_type, row_offsets[0] = 0, non-decreasing, last = nnz.
+ * col: device, nnz int32 node ids. I32 offsets require nnz < 2^31. */
+typedef struct {
+  int64_t num_pins;
+  int64_t num_boards;
+  int64_t nnz;
+  pinsage_index_t offset_type;
+  const void* row_offsets;
+  const int32_t* col;
+} pinsage_graph_t;
+
+/* Random-walk parameters (Sec. 3.2). Each of `walks_per_node` walks from a
+ * source u moves to a uniformly drawn CSR neighbour per edge step and ends
+ * after `hops` landings on a pin (or 2*hops edge steps, or a node with no
+ * edges). Every landing on a pin v != u adds one visit of v. The draw of step
+ * s of walk w uses word s%4 of Philox4x32-10 (Salmon et al., SC'11) at counter
+ * (u, w, s/4, 0) under key (lo32(seed), hi32(seed)); a word r selects the
+ * neighbour with index floor(r * deg / 2^32).
+ * Limits: 1 <= walks_per_node * hops <= 1024, 1 <= top_t <= 256. */
+typedef struct {
+  uint64_t seed;
+  int32_t walks_per_node;
+  int32_t hops;
+  int32_t top_t;
+} pinsage_walk_params_t;
+
+/* Importance neighbourhoods (Sec. 3.2), one row of top_t entries per source,
+ * in rank order (visit count descending, ties by lower node id):
+ *   idx     device int32  [rows][top_t], node id or -1 (padding, tail only)
+ *   counts  device uint16 [rows][top_t], visit counts (0 for padding)
+ *   weights device fp32   [rows][top_t], count / (sum of the row's kept
+ *           counts), one IEEE fp32 division; 0 for padding. May be NULL in
+ *           pinsage_build_neighborhoods (not written) and in the layer calls
+ *           (then derived from counts in-kernel, with the same division). */
+typedef struct {
+  int64_t rows;
+  int32_t top_t;
+  int32_t* idx;
+  uint16_t* counts;
+  float* weights;
+} pinsage_neighborhoods_t;
+
+/* One CONVOLVE layer's parameters (Algorithm 1; Sec. 3.2 "Stacking
+ * convolutions": shared by all nodes, distinct per layer).
+ *   Q device [m][d_in]            (storage dtype)
+ *   q device fp32 [m]
+ *   W device [d_out][d_in + m]    (storage dtype); columns [0, d_in) multiply
+ *                                 the node's own vector, [d_in, d_in + m) the
+ *                                 pooled neighbourhood vector
+ *   w device fp32 [d_out]
+ * Limits: d_in, m, d_out multiples of 16; d_in, m <= 8192; d_out <= 512. */
+typedef struct {
+  int32_t d_in;
+  int32_t m;
+  int32_t d_out;
+  pinsage_dtype_t dtype;
+  const void* Q;
+  const float* q;
+  const void* W;
+  const float* w;
+} pinsage_layer_t;
+
+/* Version of this ABI (PINSAGE_ABI_VERSION). */
+int pinsage_version(void);
+/* Static text for a status code. */
+const char* pinsage_status_string(int status);
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* pinsage_last_error(void);
+
+/* Importance neighbourhoods (Sec. 3.2) of sources[0..num_sources) -- or of
+ * every node 0..num_nodes-1 when sources is NULL (then num_sources must equal
+ * num_nodes). Row r of `out` belongs to sources[r]. A source id outside
+ * [0, num_nodes) yields an all-padding row. If total_steps is non-NULL
+ * (device uint64), it receives the number of edge steps all walks took.
+ * Out-of-range CSR entries end the walk that meets them (no out-of-bounds
+ * access); the graph is assumed well-formed otherwise. */
+int pinsage_build_neighborhoods(const pinsage_graph_t* graph,
+                                const pinsage_walk_params_t* walk,
+                                const int32_t* sources, int64_t num_sources,
+                                pinsage_neighborhoods_t* out,
+                                unsigned long long* total_steps, void* stream);
+
+/* Workspace bytes needed by pinsage_convolve_layer for these sizes. */
+int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
+                                    int64_t n_out, size_t* bytes);
+
+/* One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow (Sec. 3.4):
+ *   P[v]  = ReLU(Q h_in[v] + q)               for v in [0, n_transform)
+ *   n[r]  = sum_t weights[r][t] * P[idx[r][t]] (rank order; padding skipped)
+ *   z[r]  = ReLU(W concat(h_in[s(r)], n[r]) + w),  s(r) = self_rows[r] or r
+ *   h_out[r] = z[r] / ||z[r]||_2 (a zero z stays zero)   for r in [0, n_out)
+ * h_in: device [n_in][d_in]; h_out: device [n_out][d_out]; both in the
+ * layer's storage dtype. nbr->rows must equal n_out; neighbour ids must lie in
+ * [0, n_transform) (others are skipped). self_rows: device int32 or NULL.
+ * workspace: device, >= pinsage_convolve_workspace_size bytes, 256-aligned. */
+int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
+                           int64_t n_transform, const pinsage_neighborhoods_t* nbr,
+                           const int32_t* self_rows, void* h_out, int64_t n_out,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by pinsage_embed_all. */
+int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
+                                     const pinsage_layer_t* layers, int32_t num_layers,
+                                     size_t* bytes);
+
+/* All-node embedding: importance neighbourhoods of every node, then
+ * num_layers CONVOLVE layers over all nodes, layer by layer (Sec. 3.4), with
+ * h^(0) = x (Sec. 3.2). Only pins are neighbours, so each layer transforms
+ * rows [0, num_pins) once. x: device [num_nodes][layers[0].d_in];
+ * h_out: device [num_nodes][layers[K-1].d_out]; nbr_out: caller buffers with
+ * rows = num_nodes and top_t = walk->top_t (weights may be NULL).
+ * layers[k].d_in must equal layers[k-1].d_out; one storage dtype throughout. */
+int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                      const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                      pinsage_neighborhoods_t* nbr_out, void* h_out,
+                      unsigned long long* total_steps, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/* Max-margin loss, Eq. (1) (Sec. 3.3), with the expectation over negatives
+ * taken as the mean over the shared negative set (500 per minibatch in the
+ * paper):
+ *   per_pair[b] = mean_n max(0, zq[b].zneg[n] - zq[b].zpos[b] + margin)
+ *   *loss       = mean_b per_pair[b]
+ * zq, zpos: device [B][d]; zneg: device [n_neg][d]; storage dtype `dtype`;
+ * loss: device fp32 scalar; per_pair: device fp32 [B] or NULL.
+ * Limits: 1 <= B, 1 <= n_neg, 1 <= d <= 4096. */
+int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
+                            int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
+                            float* loss, float* per_pair, void* stream);
+
+/* Per-kernel timing (hipEvents recorded around every launch on the launch
+ * stream). pinsage_profile_enable(1) clears and starts collection;
+ * pinsage_profile_read() synchronises the recorded events and returns, for
+ * kernel class k (PINSAGE_KERNEL_*), the launch count and total milliseconds.
+ * Host-side bookkeeping only; not thread-safe against concurrent launches. */
+enum {
+  PINSAGE_KERNEL_WALK = 0,
+  PINSAGE_KERNEL_GEMM_Q = 1,
+  PINSAGE_KERNEL_POOL = 2,
+  PINSAGE_KERNEL_GEMM_W = 3,
+  PINSAGE_KERNEL_MINIBATCH = 4,
+  PINSAGE_KERNEL_LOSS = 5,
+  PINSAGE_KERNEL_COUNT = 6
+};
+int pinsage_profile_enable(int on);
+int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PINSAGE_H_ */

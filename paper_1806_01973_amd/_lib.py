@@ -1,0 +1,106 @@
+"""ctypes view of libpinsage.so (declarations mirror include/pinsage.h)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpinsage.so")
+
+PINSAGE_OK = 0
+PINSAGE_EINVAL = -1
+PINSAGE_EUNSUPPORTED = -2
+PINSAGE_EWORKSPACE = -3
+PINSAGE_EHIP = -4
+
+PINSAGE_I32, PINSAGE_I64 = 0, 1
+PINSAGE_F32, PINSAGE_BF16 = 0, 1
+
+KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS = range(6)
+KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss"]
+
+EXPORTED = [
+    "pinsage_version", "pinsage_status_string", "pinsage_last_error",
+    "pinsage_build_neighborhoods", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
+    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_max_margin_loss",
+    "pinsage_profile_enable", "pinsage_profile_read",
+]
+
+
+class Graph(ctypes.Structure):
+    _fields_ = [("num_pins", ctypes.c_int64), ("num_boards", ctypes.c_int64),
+                ("nnz", ctypes.c_int64), ("offset_type", ctypes.c_int),
+                ("row_offsets", ctypes.c_void_p), ("col", ctypes.c_void_p)]
+
+
+class WalkParams(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("walks_per_node", ctypes.c_int32),
+                ("hops", ctypes.c_int32), ("top_t", ctypes.c_int32)]
+
+
+class Neighborhoods(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("top_t", ctypes.c_int32),
+                ("idx", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("weights", ctypes.c_void_p)]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("m", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("dtype", ctypes.c_int), ("Q", ctypes.c_void_p), ("q", ctypes.c_void_p),
+                ("W", ctypes.c_void_p), ("w", ctypes.c_void_p)]
+
+
+class PinsageError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libpinsage.so; fails loudly if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    L.pinsage_version.restype = ctypes.c_int
+    L.pinsage_status_string.argtypes = [ctypes.c_int]
+    L.pinsage_status_string.restype = ctypes.c_char_p
+    L.pinsage_last_error.restype = ctypes.c_char_p
+    L.pinsage_build_neighborhoods.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
+                                              P, i64, ctypes.POINTER(Neighborhoods), P, P]
+    L.pinsage_convolve_workspace_size.argtypes = [ctypes.POINTER(Layer), i64, i64,
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64,
+                                         ctypes.POINTER(Neighborhoods), P, P, i64, P,
+                                         ctypes.c_size_t, P]
+    L.pinsage_embed_all_workspace_size.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(Layer),
+                                                   i32, ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_embed_all.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
+                                    ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Neighborhoods),
+                                    P, P, P, ctypes.c_size_t, P]
+    L.pinsage_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_int, ctypes.c_float,
+                                          P, P, P]
+    L.pinsage_profile_enable.argtypes = [ctypes.c_int]
+    L.pinsage_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
+                                       ctypes.POINTER(ctypes.c_double)]
+    for name in EXPORTED:
+        fn = getattr(L, name)
+        if fn.restype is None or fn.restype is ctypes.c_int:
+            fn.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def check(status: int, where: str) -> None:
+    if status != PINSAGE_OK:
+        detail = lib().pinsage_last_error().decode(errors="replace")
+        raise PinsageError(status, where, detail or
+                           lib().pinsage_status_string(status).decode())

@@ -1,0 +1,235 @@
+"""Python binding of libpinsage.so.
+
+Argument marshalling only: PyTorch provides device memory and the current HIP
+stream; every step of the hot path runs in the library's gfx950 kernels. The
+functions mirror the C entry points of include/pinsage.h.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return L.PINSAGE_F32
+    if dt == torch.bfloat16:
+        return L.PINSAGE_BF16
+    raise ValueError(f"storage dtype must be float32 or bfloat16, got {dt}")
+
+
+class DeviceGraph:
+    """Bipartite pin-board CSR resident on the GPU (pins [0, P), boards [P, P+B))."""
+
+    def __init__(self, offsets, col, num_pins: int, num_boards: int, device="cuda",
+                 offsets64: Optional[bool] = None):
+        offsets = torch.as_tensor(np.asarray(offsets) if not torch.is_tensor(offsets) else offsets)
+        col = torch.as_tensor(np.asarray(col) if not torch.is_tensor(col) else col)
+        nnz = int(col.numel())
+        if offsets64 is None:
+            offsets64 = nnz >= 2**31
+        self.num_pins, self.num_boards, self.nnz = int(num_pins), int(num_boards), nnz
+        self.offsets64 = bool(offsets64)
+        odt = torch.int64 if self.offsets64 else torch.int32
+        self.offsets = offsets.to(device=device, dtype=odt).contiguous()
+        self.col = col.to(device=device, dtype=torch.int32).contiguous()
+        if self.offsets.numel() != self.num_nodes + 1:
+            raise ValueError("offsets must have num_nodes + 1 entries")
+
+    @property
+    def num_nodes(self) -> int:
+        return self.num_pins + self.num_boards
+
+    def struct(self) -> L.Graph:
+        return L.Graph(self.num_pins, self.num_boards, self.nnz,
+                       L.PINSAGE_I64 if self.offsets64 else L.PINSAGE_I32,
+                       self.offsets.data_ptr(), self.col.data_ptr())
+
+
+@dataclass
+class Neighborhoods:
+    idx: torch.Tensor       # int32 [rows, T]
+    counts: torch.Tensor    # uint16 [rows, T]
+    weights: Optional[torch.Tensor]  # float32 [rows, T]
+
+    @property
+    def rows(self) -> int:
+        return int(self.idx.shape[0])
+
+    @property
+    def top_t(self) -> int:
+        return int(self.idx.shape[1])
+
+    def struct(self) -> L.Neighborhoods:
+        return L.Neighborhoods(self.rows, self.top_t, self.idx.data_ptr(), self.counts.data_ptr(),
+                               self.weights.data_ptr() if self.weights is not None else None)
+
+    @staticmethod
+    def empty(rows: int, T: int, weights: bool = True, device="cuda") -> "Neighborhoods":
+        return Neighborhoods(torch.empty((rows, T), dtype=torch.int32, device=device),
+                             torch.empty((rows, T), dtype=torch.uint16, device=device),
+                             torch.empty((rows, T), dtype=torch.float32, device=device)
+                             if weights else None)
+
+
+class DeviceLayer:
+    """One CONVOLVE layer's parameters on the GPU: Q [m, d_in], q [m] fp32,
+    W [d_out, d_in + m], w [d_out] fp32; Q and W in the storage dtype."""
+
+    def __init__(self, Q, q, W, w, dtype: torch.dtype = torch.float32, device="cuda"):
+        self.dtype = dtype
+        self.Q = torch.as_tensor(Q).to(device=device, dtype=dtype).contiguous()
+        self.W = torch.as_tensor(W).to(device=device, dtype=dtype).contiguous()
+        self.q = torch.as_tensor(q).to(device=device, dtype=torch.float32).contiguous()
+        self.w = torch.as_tensor(w).to(device=device, dtype=torch.float32).contiguous()
+        self.m, self.d_in = self.Q.shape
+        self.d_out = self.W.shape[0]
+        if self.W.shape[1] != self.d_in + self.m:
+            raise ValueError("W must be [d_out, d_in + m]")
+
+    def struct(self) -> L.Layer:
+        return L.Layer(self.d_in, self.m, self.d_out, _dtype_code(self.dtype), self.Q.data_ptr(),
+                       self.q.data_ptr(), self.W.data_ptr(), self.w.data_ptr())
+
+
+def build_neighborhoods(graph: DeviceGraph, walks: int, hops: int, T: int, seed: int,
+                        sources: Optional[torch.Tensor] = None, weights: bool = True,
+                        out: Optional[Neighborhoods] = None, count_steps: bool = True,
+                        stream=None):
+    """Importance neighbourhoods (Sec. 3.2). Returns (Neighborhoods, total_steps tensor|None)."""
+    lib = L.lib()
+    if sources is not None:
+        sources = _dev(sources, "sources", torch.int32)
+    rows = graph.num_nodes if sources is None else int(sources.numel())
+    nb = out if out is not None else Neighborhoods.empty(rows, T, weights, graph.col.device)
+    steps = torch.empty(1, dtype=torch.int64, device=graph.col.device) if count_steps else None
+    g, wp, ns = graph.struct(), L.WalkParams(seed, walks, hops, T), nb.struct()
+    st = lib.pinsage_build_neighborhoods(ctypes.byref(g), ctypes.byref(wp), _ptr(sources), rows,
+                                         ctypes.byref(ns), _ptr(steps), _stream(stream))
+    L.check(st, "pinsage_build_neighborhoods")
+    return nb, steps
+
+
+def convolve_workspace_size(layer: DeviceLayer, n_transform: int, n_out: int) -> int:
+    n = ctypes.c_size_t(0)
+    st = L.lib().pinsage_convolve_workspace_size(ctypes.byref(layer.struct()), n_transform, n_out,
+                                                 ctypes.byref(n))
+    L.check(st, "pinsage_convolve_workspace_size")
+    return int(n.value)
+
+
+def convolve_layer(layer: DeviceLayer, h_in: torch.Tensor, n_transform: int, nbr: Neighborhoods,
+                   self_rows: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow (Sec. 3.4)."""
+    lib = L.lib()
+    h_in = _dev(h_in, "h_in", layer.dtype)
+    if self_rows is not None:
+        self_rows = _dev(self_rows, "self_rows", torch.int32)
+    n_out = nbr.rows
+    if out is None:
+        out = torch.empty((n_out, layer.d_out), dtype=layer.dtype, device=h_in.device)
+    _dev(out, "out", layer.dtype)
+    need = convolve_workspace_size(layer, n_transform, n_out)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=h_in.device)
+    ns = nbr.struct()
+    st = lib.pinsage_convolve_layer(ctypes.byref(layer.struct()), _ptr(h_in), h_in.shape[0],
+                                    n_transform, ctypes.byref(ns), _ptr(self_rows), _ptr(out),
+                                    n_out, _ptr(workspace), workspace.numel(), _stream(stream))
+    L.check(st, "pinsage_convolve_layer")
+    return out
+
+
+def _layer_array(layers: Sequence[DeviceLayer]):
+    arr = (L.Layer * len(layers))()
+    for i, ly in enumerate(layers):
+        arr[i] = ly.struct()
+    return arr
+
+
+def embed_all_workspace_size(graph: DeviceGraph, layers: Sequence[DeviceLayer]) -> int:
+    n = ctypes.c_size_t(0)
+    st = L.lib().pinsage_embed_all_workspace_size(ctypes.byref(graph.struct()),
+                                                  _layer_array(layers), len(layers),
+                                                  ctypes.byref(n))
+    L.check(st, "pinsage_embed_all_workspace_size")
+    return int(n.value)
+
+
+class EmbedAll:
+    """Preallocated all-node embedding job (neighbourhoods + K layers, Sec. 3.4)."""
+
+    def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
+                 T: int, seed: int, weights: bool = True):
+        self.graph, self.layers = graph, list(layers)
+        self.walk = L.WalkParams(seed, walks, hops, T)
+        dev = graph.col.device
+        self.nbr = Neighborhoods.empty(graph.num_nodes, T, weights, dev)
+        self.out = torch.empty((graph.num_nodes, layers[-1].d_out), dtype=layers[-1].dtype,
+                               device=dev)
+        self.steps = torch.zeros(1, dtype=torch.int64, device=dev)
+        self.workspace = torch.empty(max(1, embed_all_workspace_size(graph, layers)),
+                                     dtype=torch.uint8, device=dev)
+        self._g = graph.struct()
+        self._layers = _layer_array(self.layers)
+        self._nbr = self.nbr.struct()
+
+    def run(self, x: torch.Tensor, stream=None) -> torch.Tensor:
+        x = _dev(x, "x", self.layers[0].dtype)
+        st = L.lib().pinsage_embed_all(ctypes.byref(self._g), ctypes.byref(self.walk),
+                                       self._layers, len(self.layers), _ptr(x),
+                                       ctypes.byref(self._nbr), _ptr(self.out), _ptr(self.steps),
+                                       _ptr(self.workspace), self.workspace.numel(),
+                                       _stream(stream))
+        L.check(st, "pinsage_embed_all")
+        return self.out
+
+
+def embed_all(graph: DeviceGraph, layers: List[DeviceLayer], x: torch.Tensor, walks: int,
+              hops: int, T: int, seed: int, stream=None):
+    job = EmbedAll(graph, layers, walks, hops, T, seed)
+    out = job.run(x, stream)
+    return job.nbr, out, job.steps
+
+
+def profile_enable(on: bool = True) -> None:
+    L.check(L.lib().pinsage_profile_enable(1 if on else 0), "pinsage_profile_enable")
+
+
+def profile_read() -> dict:
+    """{kernel name: (launches, total ms)} for launches timed since profile_enable."""
+    out = {}
+    for k, name in enumerate(L.KERNEL_NAMES):
+        n = ctypes.c_int64(0)
+        ms = ctypes.c_double(0)
+        L.check(L.lib().pinsage_profile_read(k, ctypes.byref(n), ctypes.byref(ms)),
+                "pinsage_profile_read")
+        out[name] = (int(n.value), float(ms.value))
+    return out

@@ -1,0 +1,448 @@
+// C ABI of libpinsage.so: argument validation, workspace layout, the
+// layer-wise driver (Sec. 3.4) and per-launch timing. Every floating-point or
+// graph step runs in the gfx950 kernels; this file only checks arguments and
+// sequences launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/pinsage.h"
+#include "kernels.h"
+
+namespace pinsage {
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(PINSAGE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline size_t elem_size(pinsage_dtype_t t) { return t == PINSAGE_BF16 ? 2 : 4; }
+
+// Rows of the pooled buffer processed per pool + W-GEMM pass: bounds the
+// workspace at (chunk x m) elements independent of the node count.
+constexpr int64_t kChunkRows = 1ll << 22;
+
+// ---- per-launch timing ----------------------------------------------------
+struct Pending {
+  int cls;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<Pending> g_pending;
+int64_t g_prof_count[kKCount];
+double g_prof_ms[kKCount];
+
+int check_graph(const pinsage_graph_t* g) {
+  if (!g) return fail(PINSAGE_EINVAL, "graph is NULL");
+  if (g->num_pins < 0 || g->num_boards < 0)
+    return fail(PINSAGE_EINVAL, "negative node counts (%lld pins, %lld boards)",
+                (long long)g->num_pins, (long long)g->num_boards);
+  const int64_t n = g->num_pins + g->num_boards;
+  if (n <= 0) return fail(PINSAGE_EINVAL, "graph has no nodes");
+  if (n >= (1ll << 31) - 1)
+    return fail(PINSAGE_EUNSUPPORTED, "num_nodes %lld exceeds int32 node ids", (long long)n);
+  if (g->nnz < 0) return fail(PINSAGE_EINVAL, "negative nnz");
+  if (g->offset_type != PINSAGE_I32 && g->offset_type != PINSAGE_I64)
+    return fail(PINSAGE_EINVAL, "unknown offset_type %d", (int)g->offset_type);
+  if (g->offset_type == PINSAGE_I32 && g->nnz >= (1ll << 31))
+    return fail(PINSAGE_EUNSUPPORTED, "nnz %lld needs int64 row offsets", (long long)g->nnz);
+  if (!g->row_offsets) return fail(PINSAGE_EINVAL, "row_offsets is NULL");
+  if (!g->col && g->nnz > 0) return fail(PINSAGE_EINVAL, "col is NULL");
+  return PINSAGE_OK;
+}
+
+int check_walk(const pinsage_walk_params_t* w) {
+  if (!w) return fail(PINSAGE_EINVAL, "walk params are NULL");
+  if (w->walks_per_node < 1 || w->hops < 1)
+    return fail(PINSAGE_EINVAL, "walks_per_node (%d) and hops (%d) must be >= 1",
+                w->walks_per_node, w->hops);
+  if ((int64_t)w->walks_per_node * w->hops > 1024)
+    return fail(PINSAGE_EUNSUPPORTED, "walks_per_node * hops = %lld exceeds 1024",
+                (long long)w->walks_per_node * w->hops);
+  if (w->top_t < 1 || w->top_t > 256)
+    return fail(PINSAGE_EUNSUPPORTED, "top_t %d outside [1, 256]", w->top_t);
+  return PINSAGE_OK;
+}
+
+int check_layer(const pinsage_layer_t* L, int k) {
+  if (!L) return fail(PINSAGE_EINVAL, "layer %d is NULL", k);
+  if (L->dtype != PINSAGE_F32 && L->dtype != PINSAGE_BF16)
+    return fail(PINSAGE_EINVAL, "layer %d: unknown dtype %d", k, (int)L->dtype);
+  if (L->d_in <= 0 || L->m <= 0 || L->d_out <= 0)
+    return fail(PINSAGE_EINVAL, "layer %d: dims must be positive (%d, %d, %d)", k, L->d_in, L->m,
+                L->d_out);
+  if (L->d_in % 16 || L->m % 16 || L->d_out % 16)
+    return fail(PINSAGE_EUNSUPPORTED, "layer %d: d_in, m, d_out must be multiples of 16", k);
+  if (L->d_in > 8192 || L->m > 8192 || L->d_out > 512)
+    return fail(PINSAGE_EUNSUPPORTED, "layer %d: dims above limits (d_in, m <= 8192; d_out <= 512)",
+                k);
+  if (!L->Q || !L->q || !L->W || !L->w)
+    return fail(PINSAGE_EINVAL, "layer %d: a parameter pointer is NULL", k);
+  return PINSAGE_OK;
+}
+
+int check_nbr(const pinsage_neighborhoods_t* n, int64_t rows, const char* what) {
+  if (!n) return fail(PINSAGE_EINVAL, "%s: neighbourhoods are NULL", what);
+  if (n->rows != rows)
+    return fail(PINSAGE_EINVAL, "%s: neighbourhood rows %lld != %lld", what, (long long)n->rows,
+                (long long)rows);
+  if (n->top_t < 1 || n->top_t > 256)
+    return fail(PINSAGE_EUNSUPPORTED, "%s: top_t %d outside [1, 256]", what, n->top_t);
+  if (rows > 0 && (!n->idx || !n->counts))
+    return fail(PINSAGE_EINVAL, "%s: idx or counts is NULL", what);
+  return PINSAGE_OK;
+}
+
+size_t convolve_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
+  const size_t es = elem_size(L->dtype);
+  const int64_t chunk = n_out < kChunkRows ? n_out : kChunkRows;
+  return align_up((size_t)n_transform * L->m * es) + align_up((size_t)chunk * L->m * es);
+}
+
+// Layer body shared by convolve_layer and embed_all; arguments already valid.
+int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
+              const pinsage_neighborhoods_t* nbr, const int32_t* self_rows, void* h_out,
+              int64_t n_out, void* ws, hipStream_t s) {
+  const bool bf16 = L->dtype == PINSAGE_BF16;
+  const size_t es = elem_size(L->dtype);
+  unsigned char* P = static_cast<unsigned char*>(ws);
+  unsigned char* nbuf = P + align_up((size_t)n_transform * L->m * es);
+
+  // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
+  GemmLaunch gq{};
+  gq.A0 = h_in;
+  gq.rowmap = nullptr;
+  gq.rows_a0 = n_in;
+  gq.lda0 = L->d_in;
+  gq.K0 = L->d_in;
+  gq.A1 = nullptr;
+  gq.lda1 = 0;
+  gq.K1 = 0;
+  gq.B = L->Q;
+  gq.bias = L->q;
+  gq.M = n_transform;
+  gq.N = L->m;
+  gq.C = P;
+  gq.bf16 = bf16;
+  gq.l2norm = false;
+  hipError_t e = launch_gemm(gq, s);
+  if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+
+  for (int64_t r0 = 0; r0 < n_out; r0 += kChunkRows) {
+    const int64_t rows = (n_out - r0) < kChunkRows ? (n_out - r0) : kChunkRows;
+    const int T = nbr->top_t;
+    PoolLaunch pl{};
+    pl.P = P;
+    pl.n_transform = n_transform;
+    pl.m = L->m;
+    pl.bf16 = bf16;
+    pl.idx = nbr->idx + r0 * T;
+    pl.counts = nbr->counts + r0 * T;
+    pl.weights = nbr->weights ? nbr->weights + r0 * T : nullptr;
+    pl.T = T;
+    pl.rows = rows;
+    pl.out = nbuf;
+    e = launch_pool(pl, s);
+    if (e != hipSuccess) return hip_fail(e, "pool launch");
+
+    // Algorithm 1 lines 2-3 on [h_self | n].
+    GemmLaunch gw{};
+    if (self_rows) {
+      gw.A0 = h_in;
+      gw.rowmap = self_rows + r0;
+    } else {
+      gw.A0 = static_cast<const unsigned char*>(h_in) + (size_t)r0 * L->d_in * es;
+      gw.rowmap = nullptr;
+    }
+    gw.rows_a0 = self_rows ? n_in : (n_in - r0);
+    gw.lda0 = L->d_in;
+    gw.K0 = L->d_in;
+    gw.A1 = nbuf;
+    gw.lda1 = L->m;
+    gw.K1 = L->m;
+    gw.B = L->W;
+    gw.bias = L->w;
+    gw.M = rows;
+    gw.N = L->d_out;
+    gw.C = static_cast<unsigned char*>(h_out) + (size_t)r0 * L->d_out * es;
+    gw.bf16 = bf16;
+    gw.l2norm = true;
+    e = launch_gemm(gw, s);
+    if (e != hipSuccess) return hip_fail(e, "W transform launch");
+  }
+  return PINSAGE_OK;
+}
+
+}  // namespace
+
+ProfileScope::ProfileScope(int cls, hipStream_t s) : cls_(cls), s_(s) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on) return;
+  if (hipEventCreate(&start_) != hipSuccess) {
+    start_ = nullptr;
+    return;
+  }
+  (void)hipEventRecord(start_, s_);
+}
+
+ProfileScope::~ProfileScope() {
+  if (!start_) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t stop = nullptr;
+  if (hipEventCreate(&stop) != hipSuccess) {
+    (void)hipEventDestroy(start_);
+    return;
+  }
+  (void)hipEventRecord(stop, s_);
+  g_pending.push_back({cls_, start_, stop});
+}
+
+}  // namespace pinsage
+
+using namespace pinsage;
+
+extern "C" {
+
+int pinsage_version(void) { return PINSAGE_ABI_VERSION; }
+
+const char* pinsage_status_string(int status) {
+  switch (status) {
+    case PINSAGE_OK: return "ok";
+    case PINSAGE_EINVAL: return "invalid argument";
+    case PINSAGE_EUNSUPPORTED: return "unsupported argument";
+    case PINSAGE_EWORKSPACE: return "workspace too small";
+    case PINSAGE_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* pinsage_last_error(void) { return g_last_error.c_str(); }
+
+int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                                const int32_t* sources, int64_t num_sources,
+                                pinsage_neighborhoods_t* out, unsigned long long* total_steps,
+                                void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if ((st = check_walk(walk))) return st;
+  const int64_t n = graph->num_pins + graph->num_boards;
+  if (num_sources < 0) return fail(PINSAGE_EINVAL, "negative num_sources");
+  if (!sources && num_sources != n)
+    return fail(PINSAGE_EINVAL, "sources is NULL but num_sources (%lld) != num_nodes (%lld)",
+                (long long)num_sources, (long long)n);
+  if ((st = check_nbr(out, num_sources, "build_neighborhoods"))) return st;
+  if (out->top_t != walk->top_t)
+    return fail(PINSAGE_EINVAL, "out->top_t %d != walk->top_t %d", out->top_t, walk->top_t);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (total_steps) {
+    hipError_t e = launch_zero_u64(total_steps, 1, s);
+    if (e != hipSuccess) return hip_fail(e, "step counter reset");
+  }
+  WalkLaunch a{};
+  a.row_offsets = graph->row_offsets;
+  a.offsets64 = graph->offset_type == PINSAGE_I64;
+  a.col = graph->col;
+  a.nnz = graph->nnz;
+  a.num_pins = graph->num_pins;
+  a.num_nodes = n;
+  a.sources = sources;
+  a.num_sources = num_sources;
+  a.seed = walk->seed;
+  a.walks = walk->walks_per_node;
+  a.hops = walk->hops;
+  a.top_t = walk->top_t;
+  a.idx = out->idx;
+  a.counts = out->counts;
+  a.weights = out->weights;
+  a.total_steps = total_steps;
+  hipError_t e = launch_walk_topt(a, s);
+  if (e != hipSuccess) return hip_fail(e, "walk launch");
+  return PINSAGE_OK;
+}
+
+int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
+                                    int64_t n_out, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_layer(layer, 0);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  if (n_transform < 0 || n_out < 0) return fail(PINSAGE_EINVAL, "negative row count");
+  *bytes = convolve_ws(layer, n_transform, n_out);
+  return PINSAGE_OK;
+}
+
+int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
+                           int64_t n_transform, const pinsage_neighborhoods_t* nbr,
+                           const int32_t* self_rows, void* h_out, int64_t n_out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int st = check_layer(layer, 0);
+  if (st) return st;
+  if (n_in < 0 || n_transform < 0 || n_out < 0) return fail(PINSAGE_EINVAL, "negative row count");
+  if (n_transform > n_in)
+    return fail(PINSAGE_EINVAL, "n_transform (%lld) > n_in (%lld)", (long long)n_transform,
+                (long long)n_in);
+  if (!self_rows && n_out > n_in)
+    return fail(PINSAGE_EINVAL, "n_out (%lld) > n_in (%lld) without self_rows", (long long)n_out,
+                (long long)n_in);
+  if ((st = check_nbr(nbr, n_out, "convolve_layer"))) return st;
+  if (n_out == 0 && n_transform == 0) return PINSAGE_OK;
+  if ((n_in > 0 && !h_in) || (n_out > 0 && !h_out))
+    return fail(PINSAGE_EINVAL, "h_in or h_out is NULL");
+  const size_t need = convolve_ws(layer, n_transform, n_out);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
+  return run_layer(layer, h_in, n_in, n_transform, nbr, self_rows, h_out, n_out, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph, const pinsage_layer_t* layers,
+                                     int32_t num_layers, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  if (num_layers < 1 || !layers) return fail(PINSAGE_EINVAL, "need at least one layer");
+  const int64_t n = graph->num_pins + graph->num_boards;
+  size_t conv = 0, h = 0;
+  for (int k = 0; k < num_layers; ++k) {
+    if ((st = check_layer(&layers[k], k))) return st;
+    const size_t c = convolve_ws(&layers[k], graph->num_pins, n);
+    conv = c > conv ? c : conv;
+    if (k + 1 < num_layers) {
+      const size_t hb = align_up((size_t)n * layers[k].d_out * elem_size(layers[k].dtype));
+      h = hb > h ? hb : h;
+    }
+  }
+  const int hbufs = num_layers > 2 ? 2 : (num_layers > 1 ? 1 : 0);
+  *bytes = conv + (size_t)hbufs * h;
+  return PINSAGE_OK;
+}
+
+int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                      const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                      pinsage_neighborhoods_t* nbr_out, void* h_out,
+                      unsigned long long* total_steps, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if ((st = check_walk(walk))) return st;
+  if (num_layers < 1 || !layers) return fail(PINSAGE_EINVAL, "need at least one layer");
+  for (int k = 0; k < num_layers; ++k) {
+    if ((st = check_layer(&layers[k], k))) return st;
+    if (layers[k].dtype != layers[0].dtype)
+      return fail(PINSAGE_EINVAL, "layer %d dtype differs from layer 0", k);
+    if (k > 0 && layers[k].d_in != layers[k - 1].d_out)
+      return fail(PINSAGE_EINVAL, "layer %d d_in %d != layer %d d_out %d", k, layers[k].d_in,
+                  k - 1, layers[k - 1].d_out);
+  }
+  const int64_t n = graph->num_pins + graph->num_boards;
+  if ((st = check_nbr(nbr_out, n, "embed_all"))) return st;
+  if (nbr_out->top_t != walk->top_t)
+    return fail(PINSAGE_EINVAL, "nbr_out->top_t %d != walk->top_t %d", nbr_out->top_t,
+                walk->top_t);
+  if (!x || !h_out) return fail(PINSAGE_EINVAL, "x or h_out is NULL");
+  size_t need = 0;
+  if ((st = pinsage_embed_all_workspace_size(graph, layers, num_layers, &need))) return st;
+  if (!workspace || workspace_bytes < need)
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
+  if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
+    return st;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  size_t conv = 0, h = 0;
+  for (int k = 0; k < num_layers; ++k) {
+    const size_t c = convolve_ws(&layers[k], graph->num_pins, n);
+    conv = c > conv ? c : conv;
+    if (k + 1 < num_layers) {
+      const size_t hb = align_up((size_t)n * layers[k].d_out * elem_size(layers[k].dtype));
+      h = hb > h ? hb : h;
+    }
+  }
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  unsigned char* hbuf[2] = {ws + conv, ws + conv + h};
+  const void* cur = x;
+  for (int k = 0; k < num_layers; ++k) {
+    void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
+    st = run_layer(&layers[k], cur, n, graph->num_pins, nbr_out, nullptr, dst, n, ws, s);
+    if (st) return st;
+    cur = dst;
+  }
+  return PINSAGE_OK;
+}
+
+int pinsage_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& p : g_pending) {
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
+  g_pending.clear();
+  for (int k = 0; k < kKCount; ++k) {
+    g_prof_count[k] = 0;
+    g_prof_ms[k] = 0.0;
+  }
+  g_prof_on = on != 0;
+  return PINSAGE_OK;
+}
+
+int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms) {
+  g_last_error.clear();
+  if (kernel < 0 || kernel >= kKCount) return fail(PINSAGE_EINVAL, "unknown kernel class %d", kernel);
+  if (!launches || !total_ms) return fail(PINSAGE_EINVAL, "NULL output");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& p : g_pending) {
+    hipError_t e = hipEventSynchronize(p.stop);
+    if (e != hipSuccess) return hip_fail(e, "profile event sync");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, p.start, p.stop);
+    if (e != hipSuccess) return hip_fail(e, "profile elapsed time");
+    g_prof_count[p.cls] += 1;
+    g_prof_ms[p.cls] += ms;
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
+  g_pending.clear();
+  *launches = g_prof_count[kernel];
+  *total_ms = g_prof_ms[kernel];
+  return PINSAGE_OK;
+}
+
+int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
+                            int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
+                            float* loss, float* per_pair, void* stream) {
+  g_last_error.clear();
+  (void)zq; (void)zpos; (void)B; (void)zneg; (void)n_neg; (void)d; (void)dtype; (void)margin;
+  (void)loss; (void)per_pair; (void)stream;
+  return fail(PINSAGE_EUNSUPPORTED, "max-margin loss is not built yet");
+}
+
+}  // extern "C"

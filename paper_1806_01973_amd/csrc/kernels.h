@@ -1,0 +1,88 @@
+// Host-side launchers of the gfx950 kernels (internal to libpinsage.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pinsage {
+
+// Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
+enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
+                   kKCount = 6 };
+
+// Records a start/stop hipEvent pair around a launch when timing is enabled.
+class ProfileScope {
+ public:
+  ProfileScope(int cls, hipStream_t s);
+  ~ProfileScope();
+ private:
+  int cls_;
+  hipStream_t s_;
+  hipEvent_t start_ = nullptr;
+};
+
+struct WalkLaunch {
+  const void* row_offsets;
+  bool offsets64;
+  const int32_t* col;
+  int64_t nnz;
+  int64_t num_pins;
+  int64_t num_nodes;
+  const int32_t* sources;  // nullable: row r is node r
+  int64_t num_sources;
+  uint64_t seed;
+  int walks;
+  int hops;
+  int top_t;
+  int32_t* idx;
+  uint16_t* counts;
+  float* weights;           // nullable
+  unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
+};
+hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
+
+// n[r] = sum_t alpha[r][t] * P[idx[r][t]] for rows [0, rows) of the given
+// neighbourhood slice; storage dtype bf16 when bf16 is true.
+struct PoolLaunch {
+  const void* P;
+  int64_t n_transform;
+  int m;
+  bool bf16;
+  const int32_t* idx;
+  const uint16_t* counts;
+  const float* weights;  // nullable: derived from counts
+  int T;
+  int64_t rows;
+  void* out;
+};
+hipError_t launch_pool(const PoolLaunch& a, hipStream_t s);
+
+// C[r][c] = epilogue(sum_k A[r][k] * B[c][k] + bias[c]) where the A row is the
+// concatenation of A0[rowmap ? rowmap[r] : r][0:K0] and A1[r][0:K1]. B is
+// [N][K0 + K1] row-major. Epilogue: ReLU, optionally followed by row L2
+// normalisation over all N columns.
+struct GemmLaunch {
+  const void* A0;
+  const int32_t* rowmap;  // nullable; entries outside [0, rows_a0) read as zero rows
+  int64_t rows_a0;
+  int64_t lda0;
+  int K0;
+  const void* A1;  // nullable when K1 == 0
+  int64_t lda1;
+  int K1;
+  const void* B;
+  const float* bias;
+  int64_t M;
+  int N;
+  void* C;
+  bool bf16;
+  bool l2norm;
+};
+hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
+
+// Fills n 64-bit words with zero (kept off hipMemsetAsync so callers may
+// capture the stream in a graph).
+hipError_t launch_zero_u64(unsigned long long* p, int64_t n, hipStream_t s);
+
+}  // namespace pinsage

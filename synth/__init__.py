@@ -19,4 +19,5 @@ from .graphs import (  # noqa: F401
     bf16_round,
     csr_from_edges,
     minibatch_targets,
+    random_neighborhoods,
 )

@@ -227,3 +227,23 @@ def csr_from_edges(num_pins: int, num_boards: int, edges) -> tuple:
     offsets = np.zeros(N + 1, np.int64)
     offsets[1:] = np.cumsum(np.bincount(src, minlength=N))
     return offsets, dst.astype(np.int32)
+
+
+def random_neighborhoods(n_rows: int, n_transform: int, T: int, seed: int,
+                         fill: float = 0.9):
+    """An arbitrary neighbourhood table as layer input: per row k <= T distinct
+    ids in [0, n_transform) (k = 0 for about (1 - fill) of the rows), padding
+    -1 at the tail, counts in 1..9 and independent positive weights in
+    [0.05, 1) (not normalised: a layer takes any weights)."""
+    rng = np.random.default_rng([seed, 5])
+    idx = np.full((n_rows, T), -1, np.int32)
+    counts = np.zeros((n_rows, T), np.uint16)
+    weights = np.zeros((n_rows, T), np.float32)
+    live = rng.random(n_rows) < fill
+    ks = np.where(live, rng.integers(1, min(T, n_transform) + 1, size=n_rows), 0)
+    for r in np.nonzero(ks)[0]:
+        k = int(ks[r])
+        idx[r, :k] = rng.choice(n_transform, size=k, replace=False)
+        counts[r, :k] = np.sort(rng.integers(1, 10, size=k))[::-1]
+        weights[r, :k] = rng.uniform(0.05, 1.0, size=k).astype(np.float32)
+    return idx, counts, weights

@@ -18,3 +18,14 @@ def orc():
     import oracle
     oracle.build()
     return oracle
+
+
+@pytest.fixture(scope="session")
+def medium_bundle(orc):
+    """The 1.2M-node pin-board workload with the oracle's neighbourhood table."""
+    import synth
+    wl = synth.WORKLOADS["medium"]
+    data = synth.make_workload(wl)
+    idx, cnt, wts, steps = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
+                                                   wl.seed, wl.walks, wl.hops, wl.T)
+    return {"wl": wl, "data": data, "idx": idx, "cnt": cnt, "wts": wts, "steps": steps}

@@ -1,0 +1,143 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+include/pinsage.h declares, and rejects malformed arguments on the host before
+any HIP call (the pointers passed here are never dereferenced)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pinsage.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_1806_01973_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libpinsage.so not built (run __graft_entry__.build())")
+    _lib.lib()
+    return _lib
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pinsage_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(L.lib(), n), n
+    assert sorted(L.EXPORTED) == names
+
+
+def test_version_and_status_strings(L):
+    lib = L.lib()
+    assert lib.pinsage_version() == 1
+    for code in (0, -1, -2, -3, -4):
+        assert lib.pinsage_status_string(code)
+    assert lib.pinsage_status_string(-99) == b"unknown status"
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def _graph(L, **kw):
+    g = dict(num_pins=10, num_boards=5, nnz=40, offset_type=L.PINSAGE_I32, row_offsets=FAKE,
+             col=FAKE)
+    g.update(kw)
+    return L.Graph(**g)
+
+
+def _layer(L, **kw):
+    d = dict(d_in=64, m=128, d_out=64, dtype=L.PINSAGE_F32, Q=FAKE, q=FAKE, W=FAKE, w=FAKE)
+    d.update(kw)
+    return L.Layer(**d)
+
+
+def test_build_neighborhoods_validation(L):
+    lib = L.lib()
+    walk = L.WalkParams(1, 10, 2, 8)
+    nb = L.Neighborhoods(15, 8, FAKE, FAKE, None)
+    call = lambda g, w, src, ns, n: lib.pinsage_build_neighborhoods(
+        ctypes.byref(g) if g is not None else None, ctypes.byref(w) if w is not None else None,
+        src, ns, ctypes.byref(n) if n is not None else None, None, None)
+    assert call(None, walk, None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L), None, None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L), walk, None, 14, nb) == L.PINSAGE_EINVAL  # NULL sources needs all nodes
+    assert b"num_sources" in lib.pinsage_last_error()
+    assert call(_graph(L, num_pins=-1), walk, None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L, nnz=2**31), walk, None, 15, nb) == L.PINSAGE_EUNSUPPORTED
+    assert call(_graph(L, offset_type=7), walk, None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L, num_pins=2**31), walk, None, 15, nb) == L.PINSAGE_EUNSUPPORTED
+    assert call(_graph(L), L.WalkParams(1, 600, 2, 8), None, 15, nb) == L.PINSAGE_EUNSUPPORTED
+    assert call(_graph(L), L.WalkParams(1, 0, 2, 8), None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L), L.WalkParams(1, 10, 2, 257), None, 15, nb) == L.PINSAGE_EUNSUPPORTED
+    assert call(_graph(L), walk, None, 15, L.Neighborhoods(15, 9, FAKE, FAKE, None)) == \
+        L.PINSAGE_EINVAL  # top_t mismatch
+    assert call(_graph(L), walk, None, 15, L.Neighborhoods(14, 8, FAKE, FAKE, None)) == \
+        L.PINSAGE_EINVAL  # row mismatch
+    assert call(_graph(L), walk, None, 15, L.Neighborhoods(15, 8, None, FAKE, None)) == \
+        L.PINSAGE_EINVAL
+
+
+def test_layer_validation_and_workspace_sizes(L):
+    lib = L.lib()
+    n = ctypes.c_size_t(0)
+    ly = _layer(L)
+    assert lib.pinsage_convolve_workspace_size(ctypes.byref(ly), 100, 300, ctypes.byref(n)) == 0
+    # P (100 x 128 fp32) + pooled rows (300 x 128 fp32), each 256-aligned.
+    assert n.value == 51200 + 153600
+    lyb = _layer(L, dtype=L.PINSAGE_BF16)
+    assert lib.pinsage_convolve_workspace_size(ctypes.byref(lyb), 100, 300, ctypes.byref(n)) == 0
+    assert n.value == 25600 + 76800
+    for bad, code in [(dict(d_in=60), L.PINSAGE_EUNSUPPORTED), (dict(d_out=1024), L.PINSAGE_EUNSUPPORTED),
+                      (dict(m=0), L.PINSAGE_EINVAL), (dict(Q=None), L.PINSAGE_EINVAL),
+                      (dict(dtype=5), L.PINSAGE_EINVAL)]:
+        b = _layer(L, **bad)
+        assert lib.pinsage_convolve_workspace_size(ctypes.byref(b), 1, 1, ctypes.byref(n)) == code
+    # Workspace too small: rejected before any launch.
+    nb = L.Neighborhoods(300, 8, FAKE, FAKE, None)
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, ctypes.byref(nb), None,
+                                    FAKE, 300, FAKE, 1024, None)
+    assert st == L.PINSAGE_EWORKSPACE
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 400, ctypes.byref(nb), None,
+                                    FAKE, 300, FAKE, 1 << 30, None)
+    assert st == L.PINSAGE_EINVAL  # n_transform > n_in
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, ctypes.byref(nb), None,
+                                    FAKE, 300, FAKE + 8, 1 << 30, None)
+    assert st == L.PINSAGE_EINVAL  # misaligned workspace
+    # embed_all: sizes, layer chaining, dtype consistency.
+    g = _graph(L)
+    layers = (L.Layer * 2)(_layer(L), _layer(L, d_in=64))
+    assert lib.pinsage_embed_all_workspace_size(ctypes.byref(g), layers, 2, ctypes.byref(n)) == 0
+    conv = 5120 + 7680  # P: 10 pins x 128 x 4; pooled: 15 x 128 x 4 (256-aligned)
+    hbuf = 3840         # h^(1): 15 x 64 x 4
+    assert n.value == conv + hbuf
+    bad = (L.Layer * 2)(_layer(L), _layer(L, d_in=128))
+    walk = L.WalkParams(1, 10, 2, 8)
+    nbr = L.Neighborhoods(15, 8, FAKE, FAKE, None)
+    st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), bad, 2, FAKE,
+                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None)
+    assert st == L.PINSAGE_EINVAL and b"d_in" in lib.pinsage_last_error()
+    mixed = (L.Layer * 2)(_layer(L), _layer(L, dtype=L.PINSAGE_BF16))
+    st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), mixed, 2, FAKE,
+                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None)
+    assert st == L.PINSAGE_EINVAL
+    st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
+                               ctypes.byref(nbr), FAKE, None, FAKE, 64, None)
+    assert st == L.PINSAGE_EWORKSPACE
+
+
+def test_profile_read_validation(L):
+    lib = L.lib()
+    n = ctypes.c_int64(0)
+    ms = ctypes.c_double(0)
+    assert lib.pinsage_profile_read(99, ctypes.byref(n), ctypes.byref(ms)) == L.PINSAGE_EINVAL
+    assert lib.pinsage_profile_enable(0) == 0
+    assert lib.pinsage_profile_read(0, ctypes.byref(n), ctypes.byref(ms)) == 0
+    assert n.value == 0 and ms.value == 0.0
