@@ -139,18 +139,23 @@ int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_tran
                                     int64_t n_out, size_t* bytes);
 
 /* One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow (Sec. 3.4):
- *   P[v]  = ReLU(Q h_in[v] + q)               for v in [0, n_transform)
+ *   P[i]  = ReLU(Q h_in[t(i)] + q)             for i in [0, n_transform),
+ *           t(i) = transform_rows[i] or i
  *   n[r]  = sum_t weights[r][t] * P[idx[r][t]] (rank order; padding skipped)
  *   z[r]  = ReLU(W concat(h_in[s(r)], n[r]) + w),  s(r) = self_rows[r] or r
  *   h_out[r] = z[r] / ||z[r]||_2 (a zero z stays zero)   for r in [0, n_out)
  * h_in: device [n_in][d_in]; h_out: device [n_out][d_out]; both in the
- * layer's storage dtype. nbr->rows must equal n_out; neighbour ids must lie in
- * [0, n_transform) (others are skipped). self_rows: device int32 or NULL.
+ * layer's storage dtype. nbr->rows must equal n_out; neighbour ids index the
+ * projected rows, i.e. lie in [0, n_transform) (others are skipped).
+ * transform_rows, self_rows: device int32 row maps into h_in, or NULL for the
+ * identity (entries outside [0, n_in) read as zero rows). Without
+ * transform_rows, n_transform <= n_in; without self_rows, n_out <= n_in.
  * workspace: device, >= pinsage_convolve_workspace_size bytes, 256-aligned. */
 int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
-                           int64_t n_transform, const pinsage_neighborhoods_t* nbr,
-                           const int32_t* self_rows, void* h_out, int64_t n_out,
-                           void* workspace, size_t workspace_bytes, void* stream);
+                           int64_t n_transform, const int32_t* transform_rows,
+                           const pinsage_neighborhoods_t* nbr, const int32_t* self_rows,
+                           void* h_out, int64_t n_out, void* workspace, size_t workspace_bytes,
+                           void* stream);
 
 /* Workspace bytes needed by pinsage_embed_all. */
 int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
@@ -176,11 +181,51 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
  *   per_pair[b] = mean_n max(0, zq[b].zneg[n] - zq[b].zpos[b] + margin)
  *   *loss       = mean_b per_pair[b]
  * zq, zpos: device [B][d]; zneg: device [n_neg][d]; storage dtype `dtype`;
- * loss: device fp32 scalar; per_pair: device fp32 [B] or NULL.
- * Limits: 1 <= B, 1 <= n_neg, 1 <= d <= 4096. */
+ * dot products and sums in fp32 in a fixed order. loss: device fp32 scalar;
+ * per_pair: device fp32 [B] (required: the mean is taken over it).
+ * Limits: 1 <= B, 1 <= n_neg, 1 <= d <= 1024. */
 int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
                             int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
                             float* loss, float* per_pair, void* stream);
+
+/* Training pairs of one minibatch (Sec. 3.3): pair b is (queries[b],
+ * positives[b]); every pair is scored against the same negatives (the shared
+ * negative set of Sec. 3.3); margin is Delta of Eq. (1). Device int32 node ids. */
+typedef struct {
+  int64_t num_pairs;
+  int64_t num_negatives;
+  const int32_t* queries;
+  const int32_t* positives;
+  const int32_t* negatives;
+  float margin;
+} pinsage_pairs_t;
+
+/* Workspace bytes needed by pinsage_minibatch_forward (sized for the largest
+ * frontiers: |S^(K)| <= 2B + n_neg, |S^(k-1)| <= |S^(k)| (T + 1), both <= N). */
+int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
+                                     const pinsage_walk_params_t* walk,
+                                     const pinsage_layer_t* layers, int32_t num_layers,
+                                     int64_t num_pairs, int64_t num_negatives, size_t* bytes);
+
+/* Minibatch forward of Algorithm 2 plus the loss of Eq. (1):
+ *   S^(K) = queries u positives u negatives; S^(k-1) = S^(k) u N(S^(k))
+ *   (neighbourhoods sampled by the walks of pinsage_build_neighborhoods, so
+ *   each equals the node's row of the all-node table); every set is sorted
+ *   and de-duplicated on the device and neighbour ids are re-indexed into the
+ *   compact sets (Sec. 3.3); then h^(k) = CONVOLVE^(k) for u in S^(k),
+ *   k = 1..K, with h^(0) = x (read in place through a row map), and the loss
+ *   over the pairs on h^(K).
+ * x: device [num_nodes][layers[0].d_in]; loss: device fp32 scalar;
+ * per_pair: device fp32 [B] or NULL; z_out: device [2B + n_neg][d_out] or
+ * NULL -- h^(K) of queries, then positives, then negatives; set_sizes: host
+ * int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|.
+ * This call synchronises `stream` K + 1 times to size the frontiers.
+ * Limits: as for the layers, plus d_out of the last layer <= 1024. */
+int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                              const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                              const pinsage_pairs_t* pairs, float* loss, float* per_pair,
+                              void* z_out, int64_t* set_sizes, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* Per-kernel timing (hipEvents recorded around every launch on the launch
  * stream). pinsage_profile_enable(1) clears and starts collection;

@@ -11,12 +11,14 @@ from .api import (  # noqa: F401
     DeviceGraph,
     DeviceLayer,
     EmbedAll,
+    Minibatch,
     Neighborhoods,
     build_neighborhoods,
     convolve_layer,
     convolve_workspace_size,
     embed_all,
     embed_all_workspace_size,
+    max_margin_loss,
     profile_enable,
     profile_read,
 )

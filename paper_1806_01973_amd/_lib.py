@@ -24,6 +24,7 @@ EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
     "pinsage_build_neighborhoods", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
     "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_max_margin_loss",
+    "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
     "pinsage_profile_enable", "pinsage_profile_read",
 ]
 
@@ -49,6 +50,12 @@ class Layer(ctypes.Structure):
     _fields_ = [("d_in", ctypes.c_int32), ("m", ctypes.c_int32), ("d_out", ctypes.c_int32),
                 ("dtype", ctypes.c_int), ("Q", ctypes.c_void_p), ("q", ctypes.c_void_p),
                 ("W", ctypes.c_void_p), ("w", ctypes.c_void_p)]
+
+
+class Pairs(ctypes.Structure):
+    _fields_ = [("num_pairs", ctypes.c_int64), ("num_negatives", ctypes.c_int64),
+                ("queries", ctypes.c_void_p), ("positives", ctypes.c_void_p),
+                ("negatives", ctypes.c_void_p), ("margin", ctypes.c_float)]
 
 
 class PinsageError(RuntimeError):
@@ -78,7 +85,7 @@ def lib():
                                               P, i64, ctypes.POINTER(Neighborhoods), P, P]
     L.pinsage_convolve_workspace_size.argtypes = [ctypes.POINTER(Layer), i64, i64,
                                                   ctypes.POINTER(ctypes.c_size_t)]
-    L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64,
+    L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64, P,
                                          ctypes.POINTER(Neighborhoods), P, P, i64, P,
                                          ctypes.c_size_t, P]
     L.pinsage_embed_all_workspace_size.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(Layer),
@@ -88,6 +95,14 @@ def lib():
                                     P, P, P, ctypes.c_size_t, P]
     L.pinsage_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_int, ctypes.c_float,
                                           P, P, P]
+    L.pinsage_minibatch_workspace_size.argtypes = [ctypes.POINTER(Graph),
+                                                   ctypes.POINTER(WalkParams),
+                                                   ctypes.POINTER(Layer), i32, i64, i64,
+                                                   ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_minibatch_forward.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
+                                            ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Pairs),
+                                            P, P, P, ctypes.POINTER(ctypes.c_int64), P,
+                                            ctypes.c_size_t, P]
     L.pinsage_profile_enable.argtypes = [ctypes.c_int]
     L.pinsage_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
                                        ctypes.POINTER(ctypes.c_double)]

@@ -146,12 +146,16 @@ def convolve_workspace_size(layer: DeviceLayer, n_transform: int, n_out: int) ->
 
 def convolve_layer(layer: DeviceLayer, h_in: torch.Tensor, n_transform: int, nbr: Neighborhoods,
                    self_rows: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
-                   workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                   workspace: Optional[torch.Tensor] = None, transform_rows=None,
+                   stream=None) -> torch.Tensor:
     """One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow (Sec. 3.4)."""
     lib = L.lib()
     h_in = _dev(h_in, "h_in", layer.dtype)
     if self_rows is not None:
         self_rows = _dev(self_rows, "self_rows", torch.int32)
+    if transform_rows is not None:
+        transform_rows = _dev(transform_rows, "transform_rows", torch.int32)
+        n_transform = int(transform_rows.numel())
     n_out = nbr.rows
     if out is None:
         out = torch.empty((n_out, layer.d_out), dtype=layer.dtype, device=h_in.device)
@@ -161,7 +165,8 @@ def convolve_layer(layer: DeviceLayer, h_in: torch.Tensor, n_transform: int, nbr
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=h_in.device)
     ns = nbr.struct()
     st = lib.pinsage_convolve_layer(ctypes.byref(layer.struct()), _ptr(h_in), h_in.shape[0],
-                                    n_transform, ctypes.byref(ns), _ptr(self_rows), _ptr(out),
+                                    n_transform, _ptr(transform_rows), ctypes.byref(ns),
+                                    _ptr(self_rows), _ptr(out),
                                     n_out, _ptr(workspace), workspace.numel(), _stream(stream))
     L.check(st, "pinsage_convolve_layer")
     return out
@@ -217,6 +222,70 @@ def embed_all(graph: DeviceGraph, layers: List[DeviceLayer], x: torch.Tensor, wa
     job = EmbedAll(graph, layers, walks, hops, T, seed)
     out = job.run(x, stream)
     return job.nbr, out, job.steps
+
+
+def max_margin_loss(zq: torch.Tensor, zpos: torch.Tensor, zneg: torch.Tensor, margin: float,
+                    stream=None):
+    """Eq. (1) with the mean over the shared negatives; returns (loss, per_pair)."""
+    dt = zq.dtype
+    for t, n in ((zq, "zq"), (zpos, "zpos"), (zneg, "zneg")):
+        _dev(t, n, dt)
+    B, d = zq.shape
+    loss = torch.empty(1, dtype=torch.float32, device=zq.device)
+    per = torch.empty(B, dtype=torch.float32, device=zq.device)
+    st = L.lib().pinsage_max_margin_loss(_ptr(zq), _ptr(zpos), B, _ptr(zneg), zneg.shape[0], d,
+                                         _dtype_code(dt), margin, _ptr(loss), _ptr(per),
+                                         _stream(stream))
+    L.check(st, "pinsage_max_margin_loss")
+    return loss, per
+
+
+class Minibatch:
+    """Minibatch forward of Algorithm 2 plus the loss of Eq. (1), with a
+    preallocated workspace sized for num_pairs pairs and num_negatives shared
+    negatives."""
+
+    def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
+                 T: int, seed: int, num_pairs: int, num_negatives: int):
+        self.graph, self.layers = graph, list(layers)
+        self.walk = L.WalkParams(seed, walks, hops, T)
+        self.B, self.n_neg = int(num_pairs), int(num_negatives)
+        self._g = graph.struct()
+        self._layers = _layer_array(self.layers)
+        n = ctypes.c_size_t(0)
+        st = L.lib().pinsage_minibatch_workspace_size(ctypes.byref(self._g), ctypes.byref(self.walk),
+                                                      self._layers, len(self.layers), self.B,
+                                                      self.n_neg, ctypes.byref(n))
+        L.check(st, "pinsage_minibatch_workspace_size")
+        dev = graph.col.device
+        self.workspace = torch.empty(max(1, int(n.value)), dtype=torch.uint8, device=dev)
+        self.loss = torch.empty(1, dtype=torch.float32, device=dev)
+        self.per_pair = torch.empty(self.B, dtype=torch.float32, device=dev)
+        d = self.layers[-1].d_out
+        self.z = torch.empty((2 * self.B + self.n_neg, d), dtype=self.layers[-1].dtype, device=dev)
+        self.set_sizes = (ctypes.c_int64 * (len(self.layers) + 1))()
+
+    def run(self, x: torch.Tensor, queries: torch.Tensor, positives: torch.Tensor,
+            negatives: torch.Tensor, margin: float, want_z: bool = True, stream=None):
+        x = _dev(x, "x", self.layers[0].dtype)
+        q = _dev(queries, "queries", torch.int32)
+        p = _dev(positives, "positives", torch.int32)
+        ng = _dev(negatives, "negatives", torch.int32)
+        if q.numel() != self.B or p.numel() != self.B or ng.numel() != self.n_neg:
+            raise ValueError("pair counts differ from the sizes this workspace was made for")
+        pairs = L.Pairs(self.B, self.n_neg, q.data_ptr(), p.data_ptr(), ng.data_ptr(), margin)
+        st = L.lib().pinsage_minibatch_forward(ctypes.byref(self._g), ctypes.byref(self.walk),
+                                               self._layers, len(self.layers), _ptr(x),
+                                               ctypes.byref(pairs), _ptr(self.loss),
+                                               _ptr(self.per_pair),
+                                               _ptr(self.z) if want_z else None, self.set_sizes,
+                                               _ptr(self.workspace), self.workspace.numel(),
+                                               _stream(stream))
+        L.check(st, "pinsage_minibatch_forward")
+        return self.loss
+
+    def sizes(self) -> list:
+        return [int(v) for v in self.set_sizes]
 
 
 def profile_enable(on: bool = True) -> None:

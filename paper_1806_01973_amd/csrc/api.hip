@@ -123,8 +123,8 @@ size_t convolve_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out)
 
 // Layer body shared by convolve_layer and embed_all; arguments already valid.
 int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
-              const pinsage_neighborhoods_t* nbr, const int32_t* self_rows, void* h_out,
-              int64_t n_out, void* ws, hipStream_t s) {
+              const int32_t* transform_rows, const pinsage_neighborhoods_t* nbr,
+              const int32_t* self_rows, void* h_out, int64_t n_out, void* ws, hipStream_t s) {
   const bool bf16 = L->dtype == PINSAGE_BF16;
   const size_t es = elem_size(L->dtype);
   unsigned char* P = static_cast<unsigned char*>(ws);
@@ -133,7 +133,7 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
   // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
   GemmLaunch gq{};
   gq.A0 = h_in;
-  gq.rowmap = nullptr;
+  gq.rowmap = transform_rows;
   gq.rows_a0 = n_in;
   gq.lda0 = L->d_in;
   gq.K0 = L->d_in;
@@ -295,16 +295,17 @@ int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_tran
 }
 
 int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
-                           int64_t n_transform, const pinsage_neighborhoods_t* nbr,
-                           const int32_t* self_rows, void* h_out, int64_t n_out, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+                           int64_t n_transform, const int32_t* transform_rows,
+                           const pinsage_neighborhoods_t* nbr, const int32_t* self_rows,
+                           void* h_out, int64_t n_out, void* workspace, size_t workspace_bytes,
+                           void* stream) {
   g_last_error.clear();
   int st = check_layer(layer, 0);
   if (st) return st;
   if (n_in < 0 || n_transform < 0 || n_out < 0) return fail(PINSAGE_EINVAL, "negative row count");
-  if (n_transform > n_in)
-    return fail(PINSAGE_EINVAL, "n_transform (%lld) > n_in (%lld)", (long long)n_transform,
-                (long long)n_in);
+  if (!transform_rows && n_transform > n_in)
+    return fail(PINSAGE_EINVAL, "n_transform (%lld) > n_in (%lld) without transform_rows",
+                (long long)n_transform, (long long)n_in);
   if (!self_rows && n_out > n_in)
     return fail(PINSAGE_EINVAL, "n_out (%lld) > n_in (%lld) without self_rows", (long long)n_out,
                 (long long)n_in);
@@ -317,8 +318,8 @@ int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
-  return run_layer(layer, h_in, n_in, n_transform, nbr, self_rows, h_out, n_out, workspace,
-                   static_cast<hipStream_t>(stream));
+  return run_layer(layer, h_in, n_in, n_transform, transform_rows, nbr, self_rows, h_out, n_out,
+                   workspace, static_cast<hipStream_t>(stream));
 }
 
 int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph, const pinsage_layer_t* layers,
@@ -392,7 +393,7 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   const void* cur = x;
   for (int k = 0; k < num_layers; ++k) {
     void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
-    st = run_layer(&layers[k], cur, n, graph->num_pins, nbr_out, nullptr, dst, n, ws, s);
+    st = run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n, ws, s);
     if (st) return st;
     cur = dst;
   }
@@ -440,9 +441,282 @@ int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const v
                             int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
                             float* loss, float* per_pair, void* stream) {
   g_last_error.clear();
-  (void)zq; (void)zpos; (void)B; (void)zneg; (void)n_neg; (void)d; (void)dtype; (void)margin;
-  (void)loss; (void)per_pair; (void)stream;
-  return fail(PINSAGE_EUNSUPPORTED, "max-margin loss is not built yet");
+  if (!zq || !zpos || !zneg || !loss || !per_pair)
+    return fail(PINSAGE_EINVAL, "a pointer argument is NULL (per_pair is required)");
+  if (B < 1 || n_neg < 1) return fail(PINSAGE_EINVAL, "need B >= 1 and n_neg >= 1");
+  if (d < 1 || d > 1024) return fail(PINSAGE_EUNSUPPORTED, "d %d outside [1, 1024]", d);
+  if (dtype != PINSAGE_F32 && dtype != PINSAGE_BF16)
+    return fail(PINSAGE_EINVAL, "unknown dtype %d", (int)dtype);
+  LossLaunch a{};
+  a.zq = zq;
+  a.zpos = zpos;
+  a.zneg = zneg;
+  a.B = B;
+  a.n_neg = n_neg;
+  a.d = d;
+  a.bf16 = dtype == PINSAGE_BF16;
+  a.margin = margin;
+  a.per_pair = per_pair;
+  a.loss = loss;
+  hipError_t e = launch_loss(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "loss launch");
+  return PINSAGE_OK;
+}
+
+}  // extern "C"
+
+namespace pinsage {
+namespace {
+
+constexpr int kMaxMinibatchLayers = 8;
+
+// Workspace layout of the minibatch forward; every region 256-aligned.
+struct MbPlan {
+  int K = 0, T = 0;
+  int64_t N = 0;
+  int64_t U[kMaxMinibatchLayers + 1] = {};  // frontier capacity per level
+  size_t flags = 0, pos = 0, tiles = 0, ctr = 0, rows = 0, pp = 0, conv = 0;
+  size_t set[kMaxMinibatchLayers + 1] = {};
+  size_t nidx[kMaxMinibatchLayers + 1] = {}, ncnt[kMaxMinibatchLayers + 1] = {},
+         nw[kMaxMinibatchLayers + 1] = {}, self[kMaxMinibatchLayers + 1] = {},
+         h[kMaxMinibatchLayers + 1] = {};
+  size_t total = 0;
+};
+
+int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
+              const pinsage_layer_t* layers, int K, int64_t B, int64_t n_neg, MbPlan* p) {
+  const int64_t N = g->num_pins + g->num_boards;
+  p->K = K;
+  p->T = w->top_t;
+  p->N = N;
+  const int64_t nt = 2 * B + n_neg;
+  p->U[K] = nt < N ? nt : N;
+  for (int k = K; k >= 1; --k) {
+    const int64_t grow = p->U[k] * (int64_t)(w->top_t + 1);
+    p->U[k - 1] = grow < N ? grow : N;
+  }
+  size_t cur = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = cur;
+    cur += align_up(bytes);
+    return at;
+  };
+  p->flags = take((size_t)N);
+  p->pos = take((size_t)N * 4);
+  p->tiles = take((size_t)scan_tiles(N) * 4);
+  p->ctr = take(64);
+  for (int k = 0; k <= K; ++k) p->set[k] = take((size_t)p->U[k] * 4);
+  for (int k = 1; k <= K; ++k) {
+    const size_t e = (size_t)p->U[k] * w->top_t;
+    p->nidx[k] = take(e * 4);
+    p->ncnt[k] = take(e * 2);
+    p->nw[k] = take(e * 4);
+    p->self[k] = take((size_t)p->U[k] * 4);
+    p->h[k] = take((size_t)p->U[k] * layers[k - 1].d_out * elem_size(layers[k - 1].dtype));
+  }
+  p->rows = take((size_t)nt * 4);
+  p->pp = take((size_t)B * 4);
+  size_t conv = 0;
+  for (int k = 1; k <= K; ++k) {
+    const size_t c = convolve_ws(&layers[k - 1], p->U[k - 1], p->U[k]);
+    conv = c > conv ? c : conv;
+  }
+  p->conv = take(conv);
+  p->total = cur;
+  return PINSAGE_OK;
+}
+
+int check_minibatch(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                    const pinsage_layer_t* layers, int32_t K, int64_t B, int64_t n_neg) {
+  int st = check_graph(graph);
+  if (st) return st;
+  if ((st = check_walk(walk))) return st;
+  if (K < 1 || K > kMaxMinibatchLayers || !layers)
+    return fail(PINSAGE_EUNSUPPORTED, "num_layers %d outside [1, %d]", K, kMaxMinibatchLayers);
+  for (int k = 0; k < K; ++k) {
+    if ((st = check_layer(&layers[k], k))) return st;
+    if (layers[k].dtype != layers[0].dtype)
+      return fail(PINSAGE_EINVAL, "layer %d dtype differs from layer 0", k);
+    if (k > 0 && layers[k].d_in != layers[k - 1].d_out)
+      return fail(PINSAGE_EINVAL, "layer %d d_in %d != layer %d d_out %d", k, layers[k].d_in,
+                  k - 1, layers[k - 1].d_out);
+  }
+  if (layers[K - 1].d_out > 1024)
+    return fail(PINSAGE_EUNSUPPORTED, "last layer d_out %d > 1024", layers[K - 1].d_out);
+  if (B < 1 || n_neg < 1) return fail(PINSAGE_EINVAL, "need num_pairs >= 1 and num_negatives >= 1");
+  return PINSAGE_OK;
+}
+
+int read_counters(const long long* dev, long long* host, int n, hipStream_t s) {
+  hipError_t e = hipMemcpyAsync(host, dev, sizeof(long long) * n, hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "frontier size copy");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "frontier size sync");
+  return PINSAGE_OK;
+}
+
+}  // namespace
+}  // namespace pinsage
+
+extern "C" {
+
+int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
+                                     const pinsage_walk_params_t* walk,
+                                     const pinsage_layer_t* layers, int32_t num_layers,
+                                     int64_t num_pairs, int64_t num_negatives, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_minibatch(graph, walk, layers, num_layers, num_pairs, num_negatives);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  MbPlan p;
+  make_plan(graph, walk, layers, num_layers, num_pairs, num_negatives, &p);
+  *bytes = p.total;
+  return PINSAGE_OK;
+}
+
+int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+                              const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                              const pinsage_pairs_t* pairs, float* loss, float* per_pair,
+                              void* z_out, int64_t* set_sizes, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!pairs) return fail(PINSAGE_EINVAL, "pairs is NULL");
+  const int64_t B = pairs->num_pairs, n_neg = pairs->num_negatives;
+  const int K = num_layers;
+  int st = check_minibatch(graph, walk, layers, K, B, n_neg);
+  if (st) return st;
+  if (!pairs->queries || !pairs->positives || !pairs->negatives)
+    return fail(PINSAGE_EINVAL, "pair id arrays must not be NULL");
+  if (!x || !loss) return fail(PINSAGE_EINVAL, "x or loss is NULL");
+  MbPlan p;
+  make_plan(graph, walk, layers, K, B, n_neg, &p);
+  if (!workspace || workspace_bytes < p.total)
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes,
+                p.total);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const int64_t N = p.N, T = p.T;
+  uint8_t* flags = reinterpret_cast<uint8_t*>(ws + p.flags);
+  int32_t* pos = reinterpret_cast<int32_t*>(ws + p.pos);
+  int32_t* tiles = reinterpret_cast<int32_t*>(ws + p.tiles);
+  long long* ctr = reinterpret_cast<long long*>(ws + p.ctr);
+  auto set_of = [&](int k) { return reinterpret_cast<int32_t*>(ws + p.set[k]); };
+  auto nidx_of = [&](int k) { return reinterpret_cast<int32_t*>(ws + p.nidx[k]); };
+  auto self_of = [&](int k) { return reinterpret_cast<int32_t*>(ws + p.self[k]); };
+  int32_t* rows = reinterpret_cast<int32_t*>(ws + p.rows);
+  int64_t size[kMaxMinibatchLayers + 1] = {}, npins[kMaxMinibatchLayers + 1] = {};
+  long long host[2];
+  hipError_t e;
+#define PINSAGE_TRY(expr, what)                 \
+  do {                                          \
+    e = (expr);                                 \
+    if (e != hipSuccess) return hip_fail(e, what); \
+  } while (0)
+
+  // Walks for one level: neighbourhoods of set k (global ids, weights kept).
+  auto walk_level = [&](int k) -> int {
+    WalkLaunch a{};
+    a.row_offsets = graph->row_offsets;
+    a.offsets64 = graph->offset_type == PINSAGE_I64;
+    a.col = graph->col;
+    a.nnz = graph->nnz;
+    a.num_pins = graph->num_pins;
+    a.num_nodes = N;
+    a.sources = set_of(k);
+    a.num_sources = size[k];
+    a.seed = walk->seed;
+    a.walks = walk->walks_per_node;
+    a.hops = walk->hops;
+    a.top_t = walk->top_t;
+    a.idx = nidx_of(k);
+    a.counts = reinterpret_cast<uint16_t*>(ws + p.ncnt[k]);
+    a.weights = reinterpret_cast<float*>(ws + p.nw[k]);
+    a.total_steps = nullptr;
+    PINSAGE_TRY(launch_walk_topt(a, s), "walk launch");
+    return PINSAGE_OK;
+  };
+  // Sorted unique set of level k from the flags, its size and pin count.
+  auto scan_level = [&](int k) -> int {
+    PINSAGE_TRY(launch_flag_scan(flags, N, tiles, pos, set_of(k), p.U[k], ctr, s), "frontier scan");
+    PINSAGE_TRY(launch_count_below(set_of(k), ctr, p.U[k], graph->num_pins, ctr + 1, s),
+                "pin count");
+    int r = read_counters(ctr, host, 2, s);
+    if (r) return r;
+    size[k] = host[0];
+    npins[k] = host[1];
+    if (size[k] > p.U[k])
+      return fail(PINSAGE_EHIP, "frontier %d holds %lld ids, capacity %lld", k, host[0],
+                  (long long)p.U[k]);
+    return PINSAGE_OK;
+  };
+
+  // Level K: the targets of the minibatch (Algorithm 2, S^(K) = M).
+  PINSAGE_TRY(launch_fill_zero_u8(flags, N, s), "flag reset");
+  PINSAGE_TRY(launch_mark(pairs->queries, B, N, flags, s), "mark");
+  PINSAGE_TRY(launch_mark(pairs->positives, B, N, flags, s), "mark");
+  PINSAGE_TRY(launch_mark(pairs->negatives, n_neg, N, flags, s), "mark");
+  if ((st = scan_level(K))) return st;
+  PINSAGE_TRY(launch_remap(pairs->queries, B, N, pos, rows, s), "remap");
+  PINSAGE_TRY(launch_remap(pairs->positives, B, N, pos, rows + B, s), "remap");
+  PINSAGE_TRY(launch_remap(pairs->negatives, n_neg, N, pos, rows + 2 * B, s), "remap");
+  if ((st = walk_level(K))) return st;
+  // Levels K-1 .. 0: S^(k) = S^(k+1) u N(S^(k+1)); re-index level k+1.
+  for (int k = K - 1; k >= 0; --k) {
+    PINSAGE_TRY(launch_fill_zero_u8(flags, N, s), "flag reset");
+    PINSAGE_TRY(launch_mark(set_of(k + 1), size[k + 1], N, flags, s), "mark");
+    PINSAGE_TRY(launch_mark(nidx_of(k + 1), size[k + 1] * T, N, flags, s), "mark");
+    if ((st = scan_level(k))) return st;
+    PINSAGE_TRY(launch_remap(nidx_of(k + 1), size[k + 1] * T, N, pos, nidx_of(k + 1), s), "remap");
+    PINSAGE_TRY(launch_remap(set_of(k + 1), size[k + 1], N, pos, self_of(k + 1), s), "remap");
+    if (k >= 1 && (st = walk_level(k))) return st;
+  }
+
+  // Layers k = 1..K on the compact sets (Algorithm 2, embedding loop).
+  unsigned char* conv_ws = ws + p.conv;
+  for (int k = 1; k <= K; ++k) {
+    const pinsage_layer_t* L = &layers[k - 1];
+    pinsage_neighborhoods_t nb{size[k], walk->top_t, nidx_of(k),
+                               reinterpret_cast<uint16_t*>(ws + p.ncnt[k]),
+                               reinterpret_cast<float*>(ws + p.nw[k])};
+    if (k == 1) {
+      // h^(0) = x read in place: P rows are x[S^(0) pins], self rows x[S^(1)].
+      st = run_layer(L, x, N, npins[0], set_of(0), &nb, set_of(1), ws + p.h[1], size[1], conv_ws,
+                     s);
+    } else {
+      st = run_layer(L, ws + p.h[k - 1], size[k - 1], npins[k - 1], nullptr, &nb, self_of(k),
+                     ws + p.h[k], size[k], conv_ws, s);
+    }
+    if (st) return st;
+  }
+
+  // Eq. (1) on h^(K), rows looked up through the level-K positions.
+  const pinsage_layer_t* LK = &layers[K - 1];
+  LossLaunch la{};
+  la.zq = ws + p.h[K];
+  la.q_rows = rows;
+  la.zpos = ws + p.h[K];
+  la.pos_rows = rows + B;
+  la.zneg = ws + p.h[K];
+  la.neg_rows = rows + 2 * B;
+  la.B = B;
+  la.n_neg = n_neg;
+  la.d = LK->d_out;
+  la.bf16 = LK->dtype == PINSAGE_BF16;
+  la.margin = pairs->margin;
+  la.per_pair = per_pair ? per_pair : reinterpret_cast<float*>(ws + p.pp);
+  la.loss = loss;
+  PINSAGE_TRY(launch_loss(la, s), "loss launch");
+  if (z_out)
+    PINSAGE_TRY(launch_gather_rows(ws + p.h[K], rows, 2 * B + n_neg,
+                                   (int64_t)LK->d_out * elem_size(LK->dtype), z_out, s),
+                "target gather");
+  if (set_sizes)
+    for (int k = 0; k <= K; ++k) set_sizes[k] = size[k];
+#undef PINSAGE_TRY
+  return PINSAGE_OK;
 }
 
 }  // extern "C"

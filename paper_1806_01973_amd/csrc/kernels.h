@@ -81,6 +81,43 @@ struct GemmLaunch {
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
 
+// Max-margin loss (Eq. 1): per_pair[b] = mean_n max(0, zq.zn - zq.zpos + margin),
+// *loss = mean_b per_pair[b]. Row maps index the three tables (NULL =
+// identity; negative entries read as zero vectors). d <= 1024.
+struct LossLaunch {
+  const void* zq;
+  const int32_t* q_rows;
+  const void* zpos;
+  const int32_t* pos_rows;
+  const void* zneg;
+  const int32_t* neg_rows;
+  int64_t B;
+  int64_t n_neg;
+  int d;
+  bool bf16;
+  float margin;
+  float* per_pair;
+  float* loss;
+};
+hipError_t launch_loss(const LossLaunch& a, hipStream_t s);
+
+// Frontier machinery of the minibatch forward (node flags + exclusive scan).
+hipError_t launch_fill_zero_u8(uint8_t* p, int64_t n, hipStream_t s);
+hipError_t launch_mark(const int32_t* ids, int64_t n, int64_t N, uint8_t* flags, hipStream_t s);
+int64_t scan_tiles(int64_t N);
+// set[0..total) = sorted flagged ids (entries past cap are dropped), pos[id] =
+// index of id in set (flagged ids only).
+hipError_t launch_flag_scan(const uint8_t* flags, int64_t N, int32_t* tile_sums, int32_t* pos,
+                            int32_t* set, int64_t cap, long long* total, hipStream_t s);
+// *count = entries of the sorted set (length *size_dev <= cap) below bound.
+hipError_t launch_count_below(const int32_t* set, const long long* size_dev, int64_t cap,
+                              int64_t bound, long long* count, hipStream_t s);
+// out[i] = pos[in[i]] for in[i] in [0, N), else -1 (in-place allowed).
+hipError_t launch_remap(const int32_t* in, int64_t n, int64_t N, const int32_t* pos, int32_t* out,
+                        hipStream_t s);
+hipError_t launch_gather_rows(const void* table, const int32_t* rows, int64_t n, int64_t row_bytes,
+                              void* out, hipStream_t s);
+
 // Fills n 64-bit words with zero (kept off hipMemsetAsync so callers may
 // capture the stream in a graph).
 hipError_t launch_zero_u64(unsigned long long* p, int64_t n, hipStream_t s);

@@ -18,6 +18,6 @@ from .graphs import (  # noqa: F401
     make_workload,
     bf16_round,
     csr_from_edges,
-    minibatch_targets,
+    minibatch_pairs,
     random_neighborhoods,
 )

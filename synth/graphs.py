@@ -63,8 +63,10 @@ WORKLOADS: Dict[str, Workload] = {
                        100, 3, 50, "f32", 2),
     "large": Workload("large", 10_000_000, 2_000_000, "zipf", 2.0, 2000, 1.5, 1024, 2048, 512,
                       2, 100, 3, 50, "bf16", 3),
+    # Same graph and walk seed as "medium" (the minibatch forward runs on that
+    # graph), bf16 storage.
     "minibatch": Workload("minibatch", 1_000_000, 200_000, "zipf", 2.0, 500, 1.5, 256, 512,
-                          256, 2, 100, 3, 50, "bf16", 4),
+                          256, 2, 100, 3, 50, "bf16", 2),
     "shard": Workload("shard", 80_000_000, 20_000_000, "zipf", 2.0, 5000, 1.5, 256, 512, 256,
                       2, 50, 3, 50, "bf16", 5, offsets64=True),
 }
@@ -207,12 +209,39 @@ def make_workload(wl: Workload):
             "layers": make_layers(wl)}
 
 
-def minibatch_targets(wl: Workload, batch: int, num_neg: int, rng_seed: Optional[int] = None):
-    """Query pins (uniform without replacement) and shared negative pins (uniform)."""
-    rng = np.random.default_rng([wl.seed if rng_seed is None else rng_seed, 4])
-    queries = rng.choice(wl.num_pins, size=batch, replace=False).astype(np.int32)
-    negs = rng.integers(0, wl.num_pins, size=num_neg).astype(np.int32)
-    return queries, negs
+def minibatch_pairs(wl: Workload, offsets: np.ndarray, col: np.ndarray, batch: int,
+                    num_neg: int, seed: int = 0):
+    """Training pairs for one minibatch: `batch` query pins drawn uniformly
+    without replacement, each paired with a positive pin that shares one of its
+    boards (a board drawn uniformly among the query's boards, then a pin other
+    than the query drawn uniformly from that board) -- a stand-in for the
+    engagement pairs the paper trains on -- and `num_neg` shared negative pins
+    drawn uniformly. Queries whose boards hold no other pin are redrawn."""
+    rng = np.random.default_rng([wl.seed, 4, seed])
+    P = wl.num_pins
+    queries, positives = [], []
+    taken = set()
+    while len(queries) < batch:
+        for q in rng.choice(P, size=2 * (batch - len(queries)) + 8, replace=False).tolist():
+            if q in taken or len(queries) == batch:
+                continue
+            lo, hi = int(offsets[q]), int(offsets[q + 1])
+            if hi == lo:
+                continue
+            b = int(col[lo + rng.integers(0, hi - lo)])
+            blo, bhi = int(offsets[b]), int(offsets[b + 1])
+            if bhi - blo < 2:
+                continue
+            while True:
+                v = int(col[blo + rng.integers(0, bhi - blo)])
+                if v != q:
+                    break
+            taken.add(q)
+            queries.append(q)
+            positives.append(v)
+    negatives = rng.integers(0, P, size=num_neg)
+    return (np.asarray(queries, np.int32), np.asarray(positives, np.int32),
+            negatives.astype(np.int32))
 
 
 def csr_from_edges(num_pins: int, num_boards: int, edges) -> tuple:

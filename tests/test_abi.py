@@ -102,13 +102,13 @@ def test_layer_validation_and_workspace_sizes(L):
         assert lib.pinsage_convolve_workspace_size(ctypes.byref(b), 1, 1, ctypes.byref(n)) == code
     # Workspace too small: rejected before any launch.
     nb = L.Neighborhoods(300, 8, FAKE, FAKE, None)
-    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, ctypes.byref(nb), None,
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, None, ctypes.byref(nb), None,
                                     FAKE, 300, FAKE, 1024, None)
     assert st == L.PINSAGE_EWORKSPACE
-    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 400, ctypes.byref(nb), None,
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 400, None, ctypes.byref(nb), None,
                                     FAKE, 300, FAKE, 1 << 30, None)
     assert st == L.PINSAGE_EINVAL  # n_transform > n_in
-    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, ctypes.byref(nb), None,
+    st = lib.pinsage_convolve_layer(ctypes.byref(ly), FAKE, 300, 100, None, ctypes.byref(nb), None,
                                     FAKE, 300, FAKE + 8, 1 << 30, None)
     assert st == L.PINSAGE_EINVAL  # misaligned workspace
     # embed_all: sizes, layer chaining, dtype consistency.
@@ -141,3 +141,43 @@ def test_profile_read_validation(L):
     assert lib.pinsage_profile_enable(0) == 0
     assert lib.pinsage_profile_read(0, ctypes.byref(n), ctypes.byref(ms)) == 0
     assert n.value == 0 and ms.value == 0.0
+
+
+def test_minibatch_validation_and_workspace(L):
+    lib = L.lib()
+    n = ctypes.c_size_t(0)
+    g = _graph(L)  # 15 nodes
+    walk = L.WalkParams(1, 10, 2, 4)
+    layers = (L.Layer * 2)(_layer(L), _layer(L))
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                3, 2, ctypes.byref(n)) == 0
+    # Frontier capacities: U2 = min(15, 2*3+2) = 8, U1 = U0 = 15 (capped by N).
+    a = lambda b: (b + 255) // 256 * 256
+    U = [15, 15, 8]
+    want = a(15) + a(60) + a(4) + a(64) + sum(a(u * 4) for u in U)
+    for k in (1, 2):
+        want += a(U[k] * 4 * 4) + a(U[k] * 4 * 2) + a(U[k] * 4 * 4) + a(U[k] * 4) + a(U[k] * 64 * 4)
+    want += a(8 * 4) + a(3 * 4)
+    conv = max(a(U[k - 1] * 128 * 4) + a(U[k] * 128 * 4) for k in (1, 2))
+    want += a(conv)
+    assert n.value == want
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                0, 2, ctypes.byref(n)) == L.PINSAGE_EINVAL
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 9,
+                                                3, 2, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
+    pairs = L.Pairs(3, 2, FAKE, None, FAKE, 0.1)
+    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
+                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE,
+                                       1 << 30, None)
+    assert st == L.PINSAGE_EINVAL
+    pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1)
+    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
+                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE, 16, None)
+    assert st == L.PINSAGE_EWORKSPACE
+    # Standalone loss: per_pair is required, d is bounded.
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, 64, L.PINSAGE_F32, 0.1, FAKE, None,
+                                     None)
+    assert st == L.PINSAGE_EINVAL
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, 2048, L.PINSAGE_F32, 0.1, FAKE, FAKE,
+                                     None)
+    assert st == L.PINSAGE_EUNSUPPORTED
