@@ -64,6 +64,17 @@ def _load():
     lib.orc_minibatch_embed.argtypes = [P, i64, i32, P, i32, P, P, i32, P, P, P, P, P, P, P,
                                         i32]
     lib.orc_minibatch_embed.restype = None
+    lib.orc_minibatch_sample.argtypes = [P, i64, i32, P, P, i64, i64, u64, i32, i32, i32, i32]
+    lib.orc_minibatch_sample.restype = ctypes.c_void_p
+    lib.orc_sample_sizes.argtypes = [P, i32, P]
+    lib.orc_sample_sizes.restype = None
+    lib.orc_sample_copy.argtypes = [P, i32, P, P, P, P]
+    lib.orc_sample_copy.restype = None
+    lib.orc_sample_free.argtypes = [P]
+    lib.orc_sample_free.restype = None
+    lib.orc_minibatch_embed_sampled.argtypes = [P, i64, i32, P, i64, P, i32, P, i64, P, P, i32,
+                                                P, P, P, P, P, P, P, i32]
+    lib.orc_minibatch_embed_sampled.restype = None
     lib.orc_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_double, P]
     lib.orc_max_margin_loss.restype = ctypes.c_double
     _lib = lib
@@ -198,6 +209,68 @@ def minibatch_embed(targets, x, layers, nbr_idx, nbr_w, nthreads=None):
     lib.orc_minibatch_embed(_ptr(tg), len(tg), K, _ptr(xd), xd.shape[1], _ptr(ix), _ptr(wt),
                             ix.shape[1], Qp, qp, _ptr(ms), Wp, wp, _ptr(ds), _ptr(out),
                             nthreads or default_threads())
+    return out
+
+
+def _layer_ptrs(layers):
+    K = len(layers)
+    keep = []
+    Qp, qp, Wp, wp = (ctypes.c_void_p * K)(), (ctypes.c_void_p * K)(), \
+        (ctypes.c_void_p * K)(), (ctypes.c_void_p * K)()
+    ms = np.zeros(K, np.int32)
+    ds = np.zeros(K, np.int32)
+    for k, L in enumerate(layers):
+        Q, q, W, w = (_c(L[n], np.float64) for n in ("Q", "q", "W", "w"))
+        keep += [Q, q, W, w]
+        Qp[k], qp[k], Wp[k], wp[k] = (a.ctypes.data for a in (Q, q, W, w))
+        ms[k] = Q.shape[0]
+        ds[k] = W.shape[0]
+    return keep, Qp, qp, Wp, wp, ms, ds
+
+
+def minibatch_sample(targets, K, offsets, col, num_pins, seed, walks, hops, T, nthreads=None):
+    """Algorithm 2 sampling with neighbourhoods computed on demand (Sec. 3.2 walks
+    for each needed node only). Returns {"sets": [S^(0..K)], "row_ids", "idx", "wts"}
+    with one neighbourhood row (sorted by node id) for every node of S^(1)."""
+    lib = _load()
+    tg = _c(targets, np.int32)
+    off = _c(offsets, np.int64)
+    cl = _c(col, np.int32)
+    h = lib.orc_minibatch_sample(_ptr(tg), len(tg), K, _ptr(off), _ptr(cl), num_pins,
+                                 len(off) - 1, seed, walks, hops, T, nthreads or default_threads())
+    try:
+        sizes = np.zeros(K + 2, np.int64)
+        lib.orc_sample_sizes(h, K, _ptr(sizes))
+        sets = np.empty(int(sizes[:K + 1].sum()), np.int32)
+        nrow = int(sizes[K + 1])
+        row_ids = np.empty(nrow, np.int32)
+        idx = np.empty((nrow, T), np.int32)
+        wts = np.empty((nrow, T), np.float32)
+        lib.orc_sample_copy(h, K, _ptr(sets), _ptr(row_ids), _ptr(idx), _ptr(wts))
+    finally:
+        lib.orc_sample_free(h)
+    out, pos = [], 0
+    for k in range(K + 1):
+        out.append(sets[pos:pos + sizes[k]])
+        pos += sizes[k]
+    return {"sets": out, "row_ids": row_ids, "idx": idx, "wts": wts}
+
+
+def minibatch_embed_sampled(targets, x_ids, x_rows, sample, layers, nthreads=None):
+    """Algorithm 2 embedding loop (fp64) from a sample: x_rows[i] is the feature
+    row of node x_ids[i] (sorted ids covering S^(0))."""
+    lib = _load()
+    tg = _c(targets, np.int32)
+    xi = _c(x_ids, np.int32)
+    xr = _c(x_rows, np.float64)
+    keep, Qp, qp, Wp, wp, ms, ds = _layer_ptrs(layers)
+    out = np.empty((len(tg), int(ds[-1])), np.float64)
+    ri, ix, wt = (_c(sample["row_ids"], np.int32), _c(sample["idx"], np.int32),
+                  _c(sample["wts"], np.float32))
+    lib.orc_minibatch_embed_sampled(_ptr(tg), len(tg), len(layers), _ptr(xi), len(xi), _ptr(xr),
+                                    xr.shape[1], _ptr(ri), len(ri), _ptr(ix), _ptr(wt),
+                                    ix.shape[1], Qp, qp, _ptr(ms), Wp, wp, _ptr(ds), _ptr(out),
+                                    nthreads or default_threads())
     return out
 
 

@@ -327,57 +327,42 @@ int64_t orc_minibatch_sets(const int32_t* targets, int64_t num_targets, int K,
   return total;
 }
 
-// Algorithm 2, embedding part, for the target set M: h^(0)_u = x_u on S^(0);
-// for k = 1..K every u in S^(k) gets CONVOLVE^(k)(h^(k-1)_u, {h^(k-1)_v : v in
-// N(u)}). Each neighbour's Algorithm-1 line-1 vector depends only on (k, v), so
-// it is evaluated once per distinct v within a layer. Layer parameters are
-// packed per layer: Qs[k] is [m_k x d_k], Ws[k] is [d_{k+1} x (d_k + m_k)].
-// x holds the features of every node (row v is node v). Outputs h^(K) for the
-// targets in the given order.
-void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, const double* x,
-                         int d0, const int32_t* nbr_idx, const float* nbr_w, int T,
-                         const double* const* Qs, const double* const* qs, const int* ms,
-                         const double* const* Ws, const double* const* ws, const int* d_outs,
-                         double* out, int nthreads) {
-  // Sampling (lines 1-6).
-  std::vector<std::vector<int32_t>> S(K + 1);
-  {
-    std::vector<std::set<int32_t>> Sset(K + 1);
-    for (int64_t i = 0; i < num_targets; ++i) Sset[K].insert(targets[i]);
-    for (int k = K; k >= 1; --k) {
-      Sset[k - 1] = Sset[k];
-      for (int32_t u : Sset[k])
-        for (int t = 0; t < T; ++t) {
-          int32_t v = nbr_idx[(int64_t)u * T + t];
-          if (v >= 0) Sset[k - 1].insert(v);
-        }
-    }
-    for (int k = 0; k <= K; ++k) S[k].assign(Sset[k].begin(), Sset[k].end());
-  }
-  // h^(0) on S^(0) (line 7).
+}  // extern "C"
+
+namespace {
+
+// Algorithm 2, embedding part (lines 7-13), shared by the full-table and the
+// sampled variants below. `x_row(v)` gives h^(0)_v = x_v and `nbr_row(u)` the
+// (ids, weights) of N(u); S holds the sorted sets S^(0..K). Each neighbour's
+// Algorithm-1 line-1 vector depends only on (k, v), so it is evaluated once
+// per distinct v within a layer.
+template <typename XRow, typename NbrRow>
+void minibatch_embed_impl(const int32_t* targets, int64_t num_targets, int K,
+                          const std::vector<std::vector<int32_t>>& S, XRow x_row, int d0,
+                          NbrRow nbr_row, int T, const double* const* Qs, const double* const* qs,
+                          const int* ms, const double* const* Ws, const double* const* ws,
+                          const int* d_outs, double* out, int nthreads) {
   std::map<int32_t, int64_t> pos_prev;  // node -> row in h_prev
   std::vector<double> h_prev((size_t)S[0].size() * d0);
   for (size_t i = 0; i < S[0].size(); ++i) {
     pos_prev[S[0][i]] = (int64_t)i;
-    std::memcpy(h_prev.data() + i * d0, x + (int64_t)S[0][i] * d0, sizeof(double) * d0);
+    std::memcpy(h_prev.data() + i * d0, x_row(S[0][i]), sizeof(double) * d0);
   }
   int d_prev = d0;
-  // Lines 8-12.
   for (int k = 1; k <= K; ++k) {
     const int m = ms[k - 1], d_out = d_outs[k - 1];
     const double* Q = Qs[k - 1];
     const double* q = qs[k - 1];
     const double* W = Ws[k - 1];
     const double* w = ws[k - 1];
-    // Line-1 vectors for every neighbour needed at this layer, once each.
     std::vector<int32_t> need;
     {
       std::set<int32_t> ns;
-      for (int32_t u : S[k])
-        for (int t = 0; t < T; ++t) {
-          int32_t v = nbr_idx[(int64_t)u * T + t];
-          if (v >= 0) ns.insert(v);
-        }
+      for (int32_t u : S[k]) {
+        const int32_t* ids = nbr_row(u).first;
+        for (int t = 0; t < T; ++t)
+          if (ids[t] >= 0) ns.insert(ids[t]);
+      }
       need.assign(ns.begin(), ns.end());
     }
     std::map<int32_t, int64_t> pos_need;
@@ -394,10 +379,11 @@ void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, con
       for (int64_t i = lo; i < hi; ++i) {
         int32_t u = S[k][i];
         std::fill(n_u.begin(), n_u.end(), 0.0);
+        const auto row = nbr_row(u);
         for (int t = 0; t < T; ++t) {
-          int32_t v = nbr_idx[(int64_t)u * T + t];
+          int32_t v = row.first[t];
           if (v < 0) continue;
-          double a = (double)nbr_w[(int64_t)u * T + t];
+          double a = (double)row.second[t];
           const double* pv = Pn.data() + pos_need.at(v) * m;
           for (int j = 0; j < m; ++j) n_u[j] += a * pv[j];
         }
@@ -414,6 +400,169 @@ void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, con
   for (int64_t i = 0; i < num_targets; ++i)
     std::memcpy(out + i * d_prev, h_prev.data() + pos_prev.at(targets[i]) * d_prev,
                 sizeof(double) * d_prev);
+}
+
+// Algorithm 2, sampling part: S^(K) = M; S^(k-1) = S^(k) united with N(u) for
+// every u in S^(k), with N given by `nbr_row`.
+template <typename NbrRow>
+std::vector<std::vector<int32_t>> minibatch_sets_impl(const int32_t* targets,
+                                                      int64_t num_targets, int K, int T,
+                                                      NbrRow nbr_row) {
+  std::vector<std::set<int32_t>> Sset(K + 1);
+  for (int64_t i = 0; i < num_targets; ++i) Sset[K].insert(targets[i]);
+  for (int k = K; k >= 1; --k) {
+    Sset[k - 1] = Sset[k];
+    for (int32_t u : Sset[k]) {
+      const int32_t* ids = nbr_row(u);
+      for (int t = 0; t < T; ++t)
+        if (ids[t] >= 0) Sset[k - 1].insert(ids[t]);
+    }
+  }
+  std::vector<std::vector<int32_t>> S(K + 1);
+  for (int k = 0; k <= K; ++k) S[k].assign(Sset[k].begin(), Sset[k].end());
+  return S;
+}
+
+// Sampled Algorithm 2 state: the sets S^(0..K) and the neighbourhood rows of
+// every node of S^(1) (which holds S^(2..K) too), each computed by the walks
+// of Sec. 3.2 for that node alone.
+struct Sample {
+  std::vector<std::vector<int32_t>> S;
+  std::vector<int32_t> rows_ids;  // sorted ids owning a neighbourhood row
+  std::vector<int32_t> idx;
+  std::vector<float> wts;
+  int T = 0;
+};
+
+}  // namespace
+
+extern "C" {
+
+void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, const double* x,
+                         int d0, const int32_t* nbr_idx, const float* nbr_w, int T,
+                         const double* const* Qs, const double* const* qs, const int* ms,
+                         const double* const* Ws, const double* const* ws, const int* d_outs,
+                         double* out, int nthreads) {
+  auto ids_of = [&](int32_t u) { return nbr_idx + (int64_t)u * T; };
+  auto S = minibatch_sets_impl(targets, num_targets, K, T, ids_of);
+  minibatch_embed_impl(
+      targets, num_targets, K, S, [&](int32_t v) { return x + (int64_t)v * d0; }, d0,
+      [&](int32_t u) {
+        return std::make_pair(nbr_idx + (int64_t)u * T, nbr_w + (int64_t)u * T);
+      },
+      T, Qs, qs, ms, Ws, ws, d_outs, out, nthreads);
+}
+
+// Sampling part of Algorithm 2 with neighbourhoods computed on demand, for
+// graphs too large for an all-node table on the host. Returns a handle; read it
+// with orc_sample_sizes / orc_sample_copy, release it with orc_sample_free.
+void* orc_minibatch_sample(const int32_t* targets, int64_t num_targets, int K,
+                           const int64_t* off, const int32_t* col, int64_t num_pins,
+                           int64_t num_nodes, uint64_t seed, int walks, int hops, int T,
+                           int nthreads) {
+  Graph g{off, col, num_pins, num_nodes};
+  Sample* smp = new Sample;
+  smp->T = T;
+  std::map<int32_t, int64_t> row_of;
+  auto ensure_rows = [&](const std::vector<int32_t>& nodes) {
+    std::vector<int32_t> todo;
+    for (int32_t u : nodes)
+      if (!row_of.count(u)) todo.push_back(u);
+    const int64_t base = (int64_t)smp->rows_ids.size();
+    smp->idx.resize((size_t)(base + (int64_t)todo.size()) * T);
+    smp->wts.resize((size_t)(base + (int64_t)todo.size()) * T);
+    std::vector<uint16_t> cnt((size_t)todo.size() * T);
+    parallel_rows((int64_t)todo.size(), nthreads, [&](int64_t lo, int64_t hi) {
+      std::vector<int32_t> visits;
+      for (int64_t i = lo; i < hi; ++i) {
+        visits.clear();
+        walk_from(g, seed, todo[i], walks, hops, visits);
+        select_top_t(visits, T, smp->idx.data() + (base + i) * T, cnt.data() + i * T,
+                     smp->wts.data() + (base + i) * T);
+      }
+    });
+    for (size_t i = 0; i < todo.size(); ++i) {
+      row_of[todo[i]] = base + (int64_t)i;
+      smp->rows_ids.push_back(todo[i]);
+    }
+  };
+  // Expand level by level so that every node of S^(k), k >= 1, has its row.
+  std::vector<std::set<int32_t>> Sset(K + 1);
+  for (int64_t i = 0; i < num_targets; ++i) Sset[K].insert(targets[i]);
+  for (int k = K; k >= 1; --k) {
+    std::vector<int32_t> level(Sset[k].begin(), Sset[k].end());
+    ensure_rows(level);
+    Sset[k - 1] = Sset[k];
+    for (int32_t u : level) {
+      const int32_t* ids = smp->idx.data() + row_of.at(u) * T;
+      for (int t = 0; t < T; ++t)
+        if (ids[t] >= 0) Sset[k - 1].insert(ids[t]);
+    }
+  }
+  smp->S.resize(K + 1);
+  for (int k = 0; k <= K; ++k) smp->S[k].assign(Sset[k].begin(), Sset[k].end());
+  // Store rows sorted by node id.
+  std::vector<size_t> order(smp->rows_ids.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = i;
+  std::sort(order.begin(), order.end(),
+            [&](size_t a, size_t b) { return smp->rows_ids[a] < smp->rows_ids[b]; });
+  std::vector<int32_t> ids2(order.size()), idx2(order.size() * T);
+  std::vector<float> w2(order.size() * T);
+  for (size_t i = 0; i < order.size(); ++i) {
+    ids2[i] = smp->rows_ids[order[i]];
+    std::memcpy(idx2.data() + i * T, smp->idx.data() + order[i] * T, sizeof(int32_t) * T);
+    std::memcpy(w2.data() + i * T, smp->wts.data() + order[i] * T, sizeof(float) * T);
+  }
+  smp->rows_ids.swap(ids2);
+  smp->idx.swap(idx2);
+  smp->wts.swap(w2);
+  return smp;
+}
+
+// sizes[0..K] = |S^(k)|, sizes[K+1] = number of neighbourhood rows.
+void orc_sample_sizes(void* h, int K, int64_t* sizes) {
+  Sample* smp = static_cast<Sample*>(h);
+  for (int k = 0; k <= K; ++k) sizes[k] = (int64_t)smp->S[k].size();
+  sizes[K + 1] = (int64_t)smp->rows_ids.size();
+}
+
+// sets: concatenated S^(0..K); row_ids, idx, wts: the neighbourhood rows.
+void orc_sample_copy(void* h, int K, int32_t* sets, int32_t* row_ids, int32_t* idx, float* wts) {
+  Sample* smp = static_cast<Sample*>(h);
+  int64_t p = 0;
+  for (int k = 0; k <= K; ++k)
+    for (int32_t v : smp->S[k]) sets[p++] = v;
+  std::memcpy(row_ids, smp->rows_ids.data(), sizeof(int32_t) * smp->rows_ids.size());
+  std::memcpy(idx, smp->idx.data(), sizeof(int32_t) * smp->idx.size());
+  std::memcpy(wts, smp->wts.data(), sizeof(float) * smp->wts.size());
+}
+
+void orc_sample_free(void* h) { delete static_cast<Sample*>(h); }
+
+// Algorithm 2 embedding loop on a sample: x_ids (sorted) with their feature
+// rows x_rows [n_x][d0] must cover S^(0); row_ids (sorted) with idx/wts
+// [n_rows][T] must cover S^(1).
+void orc_minibatch_embed_sampled(const int32_t* targets, int64_t num_targets, int K,
+                                 const int32_t* x_ids, int64_t n_x, const double* x_rows, int d0,
+                                 const int32_t* row_ids, int64_t n_rows, const int32_t* idx,
+                                 const float* wts, int T, const double* const* Qs,
+                                 const double* const* qs, const int* ms,
+                                 const double* const* Ws, const double* const* ws,
+                                 const int* d_outs, double* out, int nthreads) {
+  auto find = [](const int32_t* ids, int64_t n, int32_t v) -> int64_t {
+    const int32_t* p = std::lower_bound(ids, ids + n, v);
+    return (p != ids + n && *p == v) ? (int64_t)(p - ids) : -1;
+  };
+  auto ids_of = [&](int32_t u) { return idx + find(row_ids, n_rows, u) * T; };
+  auto S = minibatch_sets_impl(targets, num_targets, K, T, ids_of);
+  minibatch_embed_impl(
+      targets, num_targets, K, S,
+      [&](int32_t v) { return x_rows + find(x_ids, n_x, v) * d0; }, d0,
+      [&](int32_t u) {
+        const int64_t r = find(row_ids, n_rows, u);
+        return std::make_pair(idx + r * T, wts + r * T);
+      },
+      T, Qs, qs, ms, Ws, ws, d_outs, out, nthreads);
 }
 
 // Eq. (1), Sec. 3.3: for each pair (q, i), the expectation over negatives of

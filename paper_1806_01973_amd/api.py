@@ -49,8 +49,10 @@ class DeviceGraph:
 
     def __init__(self, offsets, col, num_pins: int, num_boards: int, device="cuda",
                  offsets64: Optional[bool] = None):
-        offsets = torch.as_tensor(np.asarray(offsets) if not torch.is_tensor(offsets) else offsets)
-        col = torch.as_tensor(np.asarray(col) if not torch.is_tensor(col) else col)
+        if not torch.is_tensor(offsets):
+            offsets = torch.as_tensor(np.asarray(offsets))
+        if not torch.is_tensor(col):
+            col = torch.as_tensor(np.asarray(col))
         nnz = int(col.numel())
         if offsets64 is None:
             offsets64 = nnz >= 2**31

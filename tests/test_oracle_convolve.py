@@ -188,3 +188,24 @@ def test_max_margin_loss_closed_form(orc):
     # Well-separated negatives give zero loss.
     loss, _ = orc.max_margin_loss(zq[:1], zpos[:1], np.array([[-1.0, 0.0]]), 0.5)
     assert loss == 0.0
+
+
+def test_sampled_route_equals_full_table(orc):
+    # The on-demand route (neighbourhoods walked only for the nodes a target set
+    # needs, features given only for S^(0)) must reproduce the full-table route.
+    wl = synth.WORKLOADS["tiny"]
+    data = synth.make_workload(wl)
+    idx, cnt, wts, _ = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
+                                               wl.seed, wl.walks, wl.hops, wl.T)
+    targets = np.array([3, 2001, 77, 1500, 2499, 3], np.int32)
+    smp = orc.minibatch_sample(targets, 2, data["offsets"], data["col"], wl.num_pins, wl.seed,
+                               wl.walks, wl.hops, wl.T)
+    full_sets = orc.minibatch_sets(targets, 2, idx)
+    for a, b in zip(smp["sets"], full_sets):
+        np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(smp["row_ids"], full_sets[1])
+    np.testing.assert_array_equal(smp["idx"], idx[full_sets[1]])
+    s0 = smp["sets"][0]
+    got = orc.minibatch_embed_sampled(targets, s0, data["x"][s0], smp, data["layers"])
+    want = orc.minibatch_embed(targets, data["x"], data["layers"], idx, wts)
+    np.testing.assert_array_equal(got, want)
