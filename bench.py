@@ -1,14 +1,21 @@
-"""Benchmark: all-node PinSage embedding on one MI355X.
+"""Benchmark: the PinSage hot path on one MI355X.
 
-One step = the whole hot path over the 1.2M-node pin-board workload (1M pins,
-200k boards, fp32, dims 256 -> 512 -> 256, 100 walks x 3 hops, T = 50):
-importance neighbourhoods of every node, then K = 2 CONVOLVE layers over every
-node, layer by layer. Inputs are resident in HBM before timing starts.
+Default (the headline line): all-node embedding of the 1.2M-node pin-board
+workload (1M pins, 200k boards, fp32, dims 256 -> 512 -> 256, 100 walks x 3
+hops, T = 50). One step = importance neighbourhoods of every node, then K = 2
+CONVOLVE layers over every node, layer by layer. Inputs are resident in HBM
+before timing starts.
 
-Prints one JSON line: node embeddings/s for the whole step (the headline),
-walk steps/s, per-kernel times from hipEvents recorded around every launch in
-the timed region, the roofline of the dominant kernel and the CPU oracle timed
-on a bounded sample of the same workload.
+Other workloads (measurement of the other rows; not the headline):
+  --workload tiny | large | shard   all-node embedding of that graph
+  --workload minibatch              one step = the minibatch forward of
+                                    Algorithm 2 (2,048 pairs, 500 shared
+                                    negatives) plus the loss of Eq. 1
+
+Prints one JSON line: throughput of the whole step, walk steps/s, per-kernel
+times from hipEvents recorded around every launch in the timed region, the
+roofline of the dominant kernel and the CPU oracle timed on a bounded sample
+of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--workload medium] [--no-cpu-baseline]
   python bench.py --copy-calibration   # plain copy of a known size, for counter scaling
@@ -30,6 +37,9 @@ METRIC = "node embeddings/sec (K=2 layerwise, all nodes) + walk steps/sec, 1 MI3
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2}
+DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1}
+DEVICE_GENERATED = ("large", "shard")
 
 
 def log(msg: str) -> None:
@@ -67,31 +77,69 @@ def copy_calibration(gib: float = 1.0, reps: int = 5) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
 
 
-def cpu_baseline(data, wl, threads: int) -> dict:
+def load_inputs(wl):
+    """Inputs on the GPU plus host views the CPU baseline needs."""
+    import numpy as np
+    import torch
+
+    import paper_1806_01973_amd as ps
+    import synth
+
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    t0 = time.perf_counter()
+    if wl.name in DEVICE_GENERATED:
+        from synth.device_gen import make_features_device, make_graph_device
+        offsets, col, E = make_graph_device(wl, log=log)
+        x = make_features_device(wl, offsets, col, log=log)
+        host = {"offsets": offsets.cpu().numpy(), "col": col.cpu().numpy()}
+        x_rows = lambda n: x[:n].float().cpu().numpy()
+    else:
+        data = synth.make_workload(wl)
+        offsets, col, E = data["offsets"], data["col"], data["num_edges"]
+        x = torch.as_tensor(data["x"]).to(device="cuda", dtype=tdt)
+        host = {"offsets": offsets, "col": col}
+        x_rows = lambda n: data["x"][:n]
+    layers_np = synth.make_layers(wl)
+    g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards, offsets64=wl.offsets64)
+    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt) for L in layers_np]
+    torch.cuda.synchronize()
+    log(f"inputs for {wl.name}: {wl.num_nodes} nodes, {E} edges in "
+        f"{time.perf_counter() - t0:.1f}s")
+    return {"g": g, "x": x, "layers": layers, "layers_np": layers_np, "num_edges": int(E),
+            "host": host, "x_rows": x_rows}
+
+
+def cpu_baseline_embed(inp, wl, threads: int) -> dict:
     """The oracle as it stands, on a bounded sample of the same workload:
     neighbourhoods of a node sample, and each layer on a row sample (pins
     projected in the same pin:node proportion). Extrapolated per node."""
     import numpy as np
     import oracle
 
-    n_walk = 400_000
-    n_rows = 120_000
     N, P = wl.num_nodes, wl.num_pins
+    n_walk = min(N, 400_000)
+    p = P / N
+    flops_row = 0.0
+    d_prev = wl.d_in
+    for _ in range(wl.K):
+        flops_row += 2 * (p * d_prev * wl.m + (d_prev + wl.m) * wl.d_out)
+        d_prev = wl.d_out
+    n_rows = int(min(N, 120_000, 150e9 / flops_row))
     rng = np.random.default_rng(123)
     src = np.sort(rng.choice(N, n_walk, replace=False)).astype(np.int32)
     t0 = time.perf_counter()
-    idx, cnt, wts, steps = oracle.build_neighborhoods(data["offsets"], data["col"], P, wl.seed,
-                                                      wl.walks, wl.hops, wl.T, sources=src,
-                                                      nthreads=threads)
+    idx, cnt, wts, steps = oracle.build_neighborhoods(inp["host"]["offsets"], inp["host"]["col"],
+                                                      P, wl.seed, wl.walks, wl.hops, wl.T,
+                                                      sources=src, nthreads=threads)
     t_walk = time.perf_counter() - t0
     # Layer sample: rows [0, n_rows) of the node features, n_transform pins
     # among them, neighbour ids folded into that range.
-    n_tr = int(round(n_rows * P / N))
+    n_tr = max(1, int(round(n_rows * p)))
     idx_s = np.where(idx[:n_rows] >= 0, idx[:n_rows] % n_tr, -1).astype(np.int32)
     wts_s = wts[:n_rows]
-    h = data["x"][:n_rows]
+    h = inp["x_rows"](n_rows)
     t_layers = 0.0
-    for L in data["layers"]:
+    for L in inp["layers_np"]:
         t0 = time.perf_counter()
         h = oracle.convolve_layer(h, n_tr, L["Q"], L["q"], L["W"], L["w"], idx_s, wts_s,
                                   nthreads=threads)
@@ -100,18 +148,177 @@ def cpu_baseline(data, wl, threads: int) -> dict:
     return {"value": 1.0 / per_node, "unit": "node embeddings/s", "cores": threads,
             "kind": "oracle",
             "sample": (f"neighbourhoods of {n_walk} random nodes ({t_walk:.1f}s, "
-                       f"{steps / t_walk:.3g} walk steps/s) + both layers on {n_rows} rows "
-                       f"with {n_tr} projected pins ({t_layers:.1f}s), fp64, extrapolated "
+                       f"{steps / t_walk:.3g} walk steps/s) + all {wl.K} layers on {n_rows} "
+                       f"rows with {n_tr} projected pins ({t_layers:.1f}s), fp64, extrapolated "
                        f"per node"),
             "walk_steps_per_s": steps / t_walk}
+
+
+def kernel_table(prof, steps):
+    kernels = {}
+    for name, (n_launch, ms) in prof.items():
+        if n_launch:
+            kernels[name] = {"launches": n_launch, "avg_ms": ms / n_launch,
+                             "ms_per_step": ms / steps}
+    return kernels
+
+
+def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_stored,
+                  walk_steps, steps):
+    """Algorithmic work per launch and achieved rates. A step's work of a kernel
+    class is divided by its launches per step (large layers run in row chunks)."""
+    esz = 2 if wl.dtype == "bf16" else 4
+    peak_tf = MFMA_PEAK_TFLOPS[wl.dtype]
+    idx_bytes = N * wl.T * 4 + (N * wl.T * 4 if weights_stored else N * wl.T * 2)
+
+    def per_launch(name, per_step):
+        return per_step / (kernels[name]["launches"] / steps)
+
+    if "pool" in kernels:
+        k = kernels["pool"]
+        k["algo_bytes_per_launch"] = per_launch(
+            "pool", sum(live_entries * L.m * esz + idx_bytes + N * L.m * esz for L in layers))
+        k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
+        k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
+    for name, fl in (("gemm_q", sum(2.0 * n_transform * L.d_in * L.m for L in layers)),
+                     ("gemm_w", sum(2.0 * N * (L.d_in + L.m) * L.d_out for L in layers))):
+        if name in kernels:
+            k = kernels[name]
+            k["algo_flops_per_launch"] = per_launch(name, fl)
+            k["achieved_TFLOPs"] = k["algo_flops_per_launch"] / (k["avg_ms"] * 1e-3) / 1e12
+            k["frac_mfma"] = k["achieved_TFLOPs"] / peak_tf
+    if "walk_topt" in kernels and walk_steps:
+        k = kernels["walk_topt"]
+        off_b = 8 if wl.offsets64 else 4
+        k["edge_steps_per_launch"] = per_launch("walk_topt", walk_steps)
+        k["algo_bytes_per_launch"] = k["edge_steps_per_launch"] * (2 * off_b + 4)
+        k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
+        k["edge_steps_per_s"] = k["edge_steps_per_launch"] / (k["avg_ms"] * 1e-3)
+
+
+def roofline_of(kernels, wl):
+    dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
+    kd = kernels[dominant]
+    if dominant in ("gemm_q", "gemm_w"):
+        return {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
+                "peak": MFMA_PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s", "frac": kd["frac_mfma"],
+                "traffic": None}
+    src_file = {"pool": "pool.hip", "walk_topt": "walk.hip"}.get(dominant, "")
+    tr = load_traffic(src_file, wl.name) if src_file else None
+    return {"kernel": dominant, "bound": "hbm", "achieved": kd.get("achieved_GBs"),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": (kd["achieved_GBs"] / HBM_PEAK_GBS) if "achieved_GBs" in kd else None,
+            "traffic": None if tr is None else tr["bytes_per_launch"]}
+
+
+def timed(run, steps, warmup):
+    import torch
+
+    import paper_1806_01973_amd as ps
+    for i in range(warmup):
+        run(i)
+    torch.cuda.synchronize()
+    log(f"warmup done ({warmup} steps)")
+    ps.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run(warmup + i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ps.profile_read()
+    ps.profile_enable(False)
+    log(f"timed {steps} steps in {elapsed:.3f}s")
+    return elapsed, prof
+
+
+def bench_embed_all(args, wl, inp):
+    import torch
+
+    import paper_1806_01973_amd as ps
+    job = ps.EmbedAll(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed,
+                      weights=wl.name != "shard")
+    stream = torch.cuda.current_stream()
+    elapsed, prof = timed(lambda i: job.run(inp["x"], stream), args.steps, args.warmup)
+    N = wl.num_nodes
+    walk_steps = int(job.steps.item())
+    kernels = kernel_table(prof, args.steps)
+    live = sum(int((job.nbr.idx[r0:r0 + (1 << 22)] >= 0).sum(dtype=torch.int64).item())
+               for r0 in range(0, N, 1 << 22))
+    add_rooflines(kernels, wl, inp["layers"], N, wl.num_pins, live, job.nbr.weights is not None,
+                  walk_steps, args.steps)
+    value = N * args.steps / elapsed
+    extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
+             "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps}}
+    return value, "node embeddings/s", METRIC, elapsed, kernels, extra
+
+
+def bench_minibatch(args, wl, inp):
+    import numpy as np
+    import torch
+
+    import paper_1806_01973_amd as ps
+    import synth
+    B, n_neg = 2048, 500
+    total = args.steps + args.warmup
+    sets = [synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], B, n_neg,
+                                  seed=i) for i in range(total)]
+    dev = [[torch.as_tensor(a).cuda() for a in s] for s in sets]
+    mb = ps.Minibatch(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed, B, n_neg)
+    stream = torch.cuda.current_stream()
+    sizes = []
+
+    def run(i):
+        q, p, n = dev[i]
+        mb.run(inp["x"], q, p, n, 0.1, want_z=False, stream=stream)
+        sizes.append(mb.sizes())
+
+    elapsed, prof = timed(run, args.steps, args.warmup)
+    kernels = kernel_table(prof, args.steps)
+    timed_sizes = np.array(sizes[args.warmup:], dtype=np.float64)
+    mean_sizes = timed_sizes.mean(axis=0).tolist()
+    value = B * args.steps / elapsed
+    extra = {"walk_steps_per_s": None,
+             "config_extra": {"pairs": B, "negatives": n_neg, "margin": 0.1,
+                              "mean_frontier_sizes": mean_sizes,
+                              "loss_last": float(mb.loss.item())}}
+    metric = "minibatch forward (Algorithm 2) + max-margin loss, training pairs/sec, 1 MI355X"
+    return value, "training pairs/s", metric, elapsed, kernels, extra
+
+
+def cpu_baseline_minibatch(inp, wl, threads):
+    """The oracle's Algorithm 2 route (on-demand neighbourhoods) and Eq. 1 for one
+    full minibatch of the same shape."""
+    import oracle
+    import synth
+    q, p, n = synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], 2048, 500,
+                                    seed=10_000)
+    targets = __import__("numpy").concatenate([q, p, n]).astype("int32")
+    t0 = time.perf_counter()
+    smp = oracle.minibatch_sample(targets, wl.K, inp["host"]["offsets"], inp["host"]["col"],
+                                  wl.num_pins, wl.seed, wl.walks, wl.hops, wl.T, nthreads=threads)
+    s0 = smp["sets"][0]
+    import torch
+    x_rows = inp["x"][torch.as_tensor(s0).long().cuda()].double().cpu().numpy()
+    t1 = time.perf_counter()
+    z = oracle.minibatch_embed_sampled(targets, s0, x_rows, smp, inp["layers_np"],
+                                       nthreads=threads)
+    oracle.max_margin_loss(z[:2048], z[2048:4096], z[4096:], 0.1)
+    t2 = time.perf_counter()
+    secs = (t1 - t0) + (t2 - t1)
+    return {"value": 2048 / secs, "unit": "training pairs/s", "cores": threads, "kind": "oracle",
+            "sample": (f"one minibatch of 2048 pairs + 500 negatives: on-demand walks "
+                       f"{t1 - t0:.1f}s, fp64 Algorithm 2 + Eq. 1 {t2 - t1:.1f}s (feature "
+                       f"gather excluded)")}
 
 
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="medium")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="medium",
+                    choices=["tiny", "medium", "minibatch", "large", "shard"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
@@ -121,121 +328,44 @@ def main() -> int:
               "multi-GPU mode; run it with --gpus 1.", file=sys.stderr)
         return 2
 
-    import numpy as np
     import torch
 
     if args.copy_calibration:
         copy_calibration()
         return 0
 
-    import paper_1806_01973_amd as ps
     import synth
 
     wl = synth.WORKLOADS[args.workload]
-    t0 = time.perf_counter()
-    data = synth.make_workload(wl)
-    log(f"generated {wl.name}: {wl.num_nodes} nodes, {data['num_edges']} edges "
-        f"in {time.perf_counter() - t0:.1f}s")
-    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards,
-                       offsets64=wl.offsets64)
-    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt) for L in data["layers"]]
-    x = torch.as_tensor(data["x"]).to(device="cuda", dtype=tdt)
-    job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
-    stream = torch.cuda.current_stream()
-
-    for _ in range(args.warmup):
-        job.run(x, stream)
-    torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps)")
-
-    ps.profile_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        job.run(x, stream)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ps.profile_read()
-    ps.profile_enable(False)
-    log(f"timed {args.steps} steps in {elapsed:.3f}s")
-
-    N = wl.num_nodes
-    steps_per_run = int(job.steps.item())
-    ms_per_step = 1e3 * elapsed / args.steps
-    value = N * args.steps / elapsed
-
-    # Algorithmic work per launch.
-    esz = 2 if wl.dtype == "bf16" else 4
-    live = (job.nbr.idx >= 0).sum().item()
-    idx_bytes = N * wl.T * 4 + (N * wl.T * 4 if job.nbr.weights is not None else N * wl.T * 2)
-    pool_bytes = [live * L.m * esz + idx_bytes + N * L.m * esz for L in layers]
-    gq_flops = [2.0 * wl.num_pins * L.d_in * L.m for L in layers]
-    gw_flops = [2.0 * N * (L.d_in + L.m) * L.d_out for L in layers]
-    off_b = 8 if wl.offsets64 else 4
-    walk_bytes = steps_per_run * (2 * off_b + 4)
-
-    kernels = {}
-    for name, (n_launch, ms) in prof.items():
-        if n_launch == 0:
-            continue
-        kernels[name] = {"launches": n_launch, "avg_ms": ms / n_launch,
-                         "ms_per_step": ms / args.steps}
-    # Pool: algorithmic bytes per launch (both layers alike when m is equal).
-    pool_avg_bytes = sum(pool_bytes) / len(pool_bytes)
-    if "pool" in kernels:
-        k = kernels["pool"]
-        k["algo_bytes_per_launch"] = pool_avg_bytes
-        k["achieved_GBs"] = pool_avg_bytes / (k["avg_ms"] * 1e-3) / 1e9
-        k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
-    peak_tf = MFMA_PEAK_TFLOPS[wl.dtype]
-    for name, fl in (("gemm_q", gq_flops), ("gemm_w", gw_flops)):
-        if name in kernels:
-            k = kernels[name]
-            k["algo_flops_per_launch"] = sum(fl) / len(fl)
-            k["achieved_TFLOPs"] = k["algo_flops_per_launch"] / (k["avg_ms"] * 1e-3) / 1e12
-            k["frac_mfma"] = k["achieved_TFLOPs"] / peak_tf
-    walk_steps_per_s = None
-    if "walk_topt" in kernels:
-        k = kernels["walk_topt"]
-        k["edge_steps_per_launch"] = steps_per_run
-        k["algo_bytes_per_launch"] = walk_bytes
-        k["achieved_GBs"] = walk_bytes / (k["avg_ms"] * 1e-3) / 1e9
-        walk_steps_per_s = steps_per_run / (k["avg_ms"] * 1e-3)
-
-    dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
-    kd = kernels[dominant]
-    if dominant in ("gemm_q", "gemm_w"):
-        roof = {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
-                "peak": peak_tf, "unit": "TFLOP/s", "frac": kd["frac_mfma"], "traffic": None}
+    args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[wl.name]
+    args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[wl.name]
+    inp = load_inputs(wl)
+    if wl.name == "minibatch":
+        value, unit, metric, elapsed, kernels, extra = bench_minibatch(args, wl, inp)
     else:
-        src_file = {"pool": "pool.hip", "walk_topt": "walk.hip"}[dominant]
-        tr = load_traffic(src_file, wl.name)
-        roof = {"kernel": dominant, "bound": "hbm", "achieved": kd["achieved_GBs"],
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kd["achieved_GBs"] / HBM_PEAK_GBS,
-                "traffic": None if tr is None else tr["bytes_per_launch"]}
+        value, unit, metric, elapsed, kernels, extra = bench_embed_all(args, wl, inp)
 
     result = {
-        "metric": METRIC,
+        "metric": metric,
         "value": value,
-        "unit": "node embeddings/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": 1e3 * elapsed / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
-                               f"{data['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
+                               f"{inp['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
                                f"T={wl.T}, K={wl.K}, dims {wl.d_in}->{wl.m}->{wl.d_out} "
                                f"{wl.dtype}",
-                   "nodes": N, "edges": int(data["num_edges"]), "walk_steps_per_step": steps_per_run,
-                   "gpu": torch.cuda.get_device_name(0)},
-        "walk_steps_per_s": walk_steps_per_s,
-        "roofline": roof,
+                   "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
+                   **extra["config_extra"]},
+        "walk_steps_per_s": extra["walk_steps_per_s"],
+        "roofline": roofline_of(kernels, wl),
         "kernels": kernels,
         "cpu_baseline": None,
     }
@@ -243,7 +373,9 @@ def main() -> int:
         import oracle
         threads = oracle.default_threads()
         log(f"timing the oracle on a sample ({threads} threads)")
-        result["cpu_baseline"] = cpu_baseline(data, wl, threads)
+        result["cpu_baseline"] = (cpu_baseline_minibatch(inp, wl, threads)
+                                  if wl.name == "minibatch" else
+                                  cpu_baseline_embed(inp, wl, threads))
     print(json.dumps(result), flush=True)
     return 0
 

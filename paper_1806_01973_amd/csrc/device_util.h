@@ -47,21 +47,60 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ __forceinline__ int wave_inclusive_sum(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(v, o);
-    if (lane >= o) v += t;
+// ---- cross-lane exchange through DPP (VALU, no LDS traffic) ----------------
+// Controls (gfx9 encoding): quad_perm 0xB1 / 0x4E read lane ^ 1 / lane ^ 2;
+// row_ror:n (0x120 + n) reads lane (i - n) mod 16 within each row of 16 lanes;
+// row_shr:n (0x110 + n) reads lane i - n within the row (lanes without a
+// source keep `old`); row_bcast:15 / :31 (0x142 / 0x143) read lane 15 of the
+// previous row / lane 31.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ int dpp(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xF, false);
+}
+
+// Value held by lane (lane ^ M), M a power of two below 64.
+template <int M>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v, int lane) {
+  const int x = (int)v;
+  if constexpr (M == 1) {
+    return (uint32_t)dpp<0xB1>(x, x);
+  } else if constexpr (M == 2) {
+    return (uint32_t)dpp<0x4E>(x, x);
+  } else if constexpr (M == 4) {
+    const int up = dpp<0x12C>(x, x);    // lane i + 4 (row_ror:12)
+    const int down = dpp<0x124>(x, x);  // lane i - 4 (row_ror:4)
+    return (uint32_t)((lane & 4) ? down : up);
+  } else if constexpr (M == 8) {
+    return (uint32_t)dpp<0x128>(x, x);  // row_ror:8
+  } else if constexpr (M == 16) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle(x, 0x1F | (16 << 10));  // bit-mode xor 16
+  } else {
+    return (uint32_t)__shfl_xor(x, M);
   }
+}
+
+// Inclusive scans over the 64 lanes: Hillis-Steele inside rows of 16, then the
+// row totals are carried across rows with the two row broadcasts.
+__device__ __forceinline__ int wave_inclusive_sum(int v, int /*lane*/) {
+  v += dpp<0x111>(0, v);
+  v += dpp<0x112>(0, v);
+  v += dpp<0x114>(0, v);
+  v += dpp<0x118>(0, v);
+  v += dpp<0x142, 0xA>(0, v);
+  v += dpp<0x143, 0xC>(0, v);
   return v;
 }
 
-__device__ __forceinline__ int wave_inclusive_max(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(v, o);
-    if (lane >= o) v = v > t ? v : t;
-  }
+__device__ __forceinline__ int imax(int a, int b) { return a > b ? a : b; }
+
+// Identity -1 (the values scanned here are >= -1).
+__device__ __forceinline__ int wave_inclusive_max(int v, int /*lane*/) {
+  v = imax(v, dpp<0x111>(-1, v));
+  v = imax(v, dpp<0x112>(-1, v));
+  v = imax(v, dpp<0x114>(-1, v));
+  v = imax(v, dpp<0x118>(-1, v));
+  v = imax(v, dpp<0x142, 0xA>(-1, v));
+  v = imax(v, dpp<0x143, 0xC>(-1, v));
   return v;
 }
 
@@ -72,10 +111,13 @@ __device__ __forceinline__ float wave_sum_f32(float v) {
   return v;
 }
 
+// Wave-wide max / sum of values >= -1 (resp. any int), same on every lane.
+__device__ __forceinline__ int wave_max_i32(int v) {
+  return __builtin_amdgcn_readlane(wave_inclusive_max(v, 0), 63);
+}
+
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  return __builtin_amdgcn_readlane(wave_inclusive_sum(v, 0), 63);
 }
 
 }  // namespace pinsage

@@ -9,11 +9,12 @@
 //   2. each lane pulls E consecutive slots into registers and the wave sorts
 //      the 64*E visit ids with a register bitonic network (cross-lane stages
 //      through lane shuffles), so equal ids become runs;
-//   3. run boundaries and two wave scans give every distinct id its visit
-//      count c and its rank p in id order; the distinct ids are parked in LDS
-//      by p;
-//   4. a second bitonic sort of the keys (0xFFFF - c) << 16 | p puts the
-//      distinct ids in (count desc, id asc) order; the first T are written.
+//   3. run boundaries and a wave max-scan give every distinct id its visit
+//      count (held at the run's last element);
+//   4. the count classes are visited from the highest count down: as ids are
+//      ascending, an entry's rank in (count desc, id asc) order is the number
+//      of entries in the classes above plus its position in its own class;
+//      ranks below T are written with their weights.
 // Walk randomness: Philox4x32-10 at counter (u, w, s/4, 0), key = seed, word
 // s%4 for edge step s; neighbour index floor(r * deg / 2^32).
 #include "device_util.h"
@@ -24,35 +25,58 @@ namespace {
 
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;
 constexpr int kWavesPerBlock = 4;
+constexpr int kMaxTopT = 256;
+// Second half of a wave's LDS strip: the kept counts, by rank.
+constexpr int kStripOut = kMaxTopT;
 
+// Ascending bitonic sort of the 64*E keys held E per lane (element index
+// lane*E + e). Stages with stride >= E pair lanes (lane ^ stride/E, same e);
+// their direction depends on the lane only. Shorter strides pair registers
+// of one lane.
+template <int M, int E>
+__device__ __forceinline__ void cross_lane_stage(uint32_t (&k)[E], int lane, bool take_min) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const uint32_t other = lane_xor<M>(k[e], lane);
+    const uint32_t lo = k[e] < other ? k[e] : other;
+    const uint32_t hi = k[e] < other ? other : k[e];
+    k[e] = take_min ? lo : hi;
+  }
+}
+
+// Ascending bitonic sort of the 64*E keys held E per lane (element index
+// lane*E + e). Stages with stride >= E pair lanes (lane ^ stride/E, same e)
+// through DPP/swizzle exchanges; their direction depends on the lane only.
+// Shorter strides pair registers of one lane.
 template <int E>
 __device__ __forceinline__ void bitonic_sort_wave(uint32_t (&k)[E], int lane) {
+  const int lane_base = lane * E;
 #pragma unroll
   for (int size = 2; size <= kWave * E; size <<= 1) {
 #pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       if (stride >= E) {
-        const int lane_mask = stride / E;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const uint32_t other = __shfl_xor(k[e], lane_mask);
-          const int i = lane * E + e;
-          const bool ascending = (i & size) == 0;
-          const bool lower = (i & stride) == 0;
-          const uint32_t lo = k[e] < other ? k[e] : other;
-          const uint32_t hi = k[e] < other ? other : k[e];
-          k[e] = (ascending == lower) ? lo : hi;
+        const bool up = (lane_base & size) == 0;
+        const bool lower = (lane_base & stride) == 0;
+        const bool take_min = up == lower;
+        switch (stride / E) {
+          case 1: cross_lane_stage<1>(k, lane, take_min); break;
+          case 2: cross_lane_stage<2>(k, lane, take_min); break;
+          case 4: cross_lane_stage<4>(k, lane, take_min); break;
+          case 8: cross_lane_stage<8>(k, lane, take_min); break;
+          case 16: cross_lane_stage<16>(k, lane, take_min); break;
+          default: cross_lane_stage<32>(k, lane, take_min); break;
         }
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           if ((e & stride) == 0) {
-            const int i = lane * E + e;
-            const bool ascending = (i & size) == 0;
+            const bool up = size < E ? ((e & size) == 0) : ((lane_base & size) == 0);
             const uint32_t a = k[e], b = k[e + stride];
-            const bool swap = ascending ? (a > b) : (a < b);
-            k[e] = swap ? b : a;
-            k[e + stride] = swap ? a : b;
+            const uint32_t lo = a < b ? a : b;
+            const uint32_t hi = a < b ? b : a;
+            k[e] = up ? lo : hi;
+            k[e + stride] = up ? hi : lo;
           }
         }
       }
@@ -65,9 +89,73 @@ __device__ __forceinline__ uint32_t pick_word(const uint4& r, int s) {
   return q == 0 ? r.x : (q == 1 ? r.y : (q == 2 ? r.z : r.w));
 }
 
+// One walk (Sec. 3.2): from the source u, uniform neighbour choice per edge
+// step, ends after `hops` pin landings, 2*hops steps, a node without edges or
+// an out-of-range CSR entry. Landings go to `mine[0..hops)`; the source itself
+// is recorded as empty.
+template <typename OffT>
+struct Walker {
+  int64_t u, cur, next_at;
+  uint32_t w;
+  int landed, s;
+  bool exists, active;
+  uint4 rnd;
+  uint32_t* mine;
+
+  __device__ void start(int64_t src, int walk, uint32_t* slots, bool present) {
+    u = src;
+    cur = src;
+    next_at = 0;
+    w = (uint32_t)walk;
+    landed = 0;
+    s = 0;
+    exists = present;
+    active = present;
+    rnd = make_uint4(0, 0, 0, 0);
+    mine = slots;
+  }
+  // Chooses the next CSR position from the row [lo, hi) of the current node.
+  __device__ void pick(int64_t lo, int64_t hi, int64_t nnz, uint32_t k0, uint32_t k1) {
+    if (!active) return;
+    const int64_t deg = hi - lo;
+    if (deg <= 0 || lo < 0 || hi > nnz) {
+      active = false;
+      return;
+    }
+    if ((s & 3) == 0)
+      rnd = philox4x32_10(make_uint4((uint32_t)u, w, (uint32_t)(s >> 2), 0u), k0, k1);
+    const uint32_t r = pick_word(rnd, s);
+    next_at = lo + (int64_t)(((uint64_t)r * (uint64_t)deg) >> 32);
+  }
+  // Moves to node nxt (read from col[next_at]) and records a pin landing.
+  __device__ void land(int32_t nxt, int64_t num_pins, int64_t num_nodes, int hops) {
+    if (!active) return;
+    if (nxt < 0 || (int64_t)nxt >= num_nodes) {
+      active = false;
+      return;
+    }
+    cur = nxt;
+    ++s;
+    if (cur < num_pins) {
+      mine[landed] = (cur != u) ? (uint32_t)cur : kEmpty;
+      ++landed;
+    }
+    if (landed >= hops || s >= 2 * hops) active = false;
+  }
+  // Pads the unused landing slots; returns the edge steps taken.
+  __device__ uint32_t finish(int hops) {
+    if (!exists) return 0;
+    for (int h = landed; h < hops; ++h) mine[h] = kEmpty;
+    return (uint32_t)s;
+  }
+};
+
 template <typename OffT, int E>
 __global__ __launch_bounds__(256) void walk_topt_kernel(WalkLaunch a) {
-  __shared__ uint32_t strip_all[kWavesPerBlock][kWave * E];
+  // Per wave: the visit slots (64*E), reused to stage the output row
+  // (ids at [0, T), counts at [kStripOut, kStripOut + T)).
+  constexpr int kStrip = kWave * E > 2 * kMaxTopT ? kWave * E : 2 * kMaxTopT;
+  __shared__ uint32_t strip_all[kWavesPerBlock][kStrip];
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   uint32_t* strip = strip_all[wave];
@@ -77,12 +165,13 @@ __global__ __launch_bounds__(256) void walk_topt_kernel(WalkLaunch a) {
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
   const int T = a.top_t;
+  unsigned long long wave_steps = 0;
 
   for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < a.num_sources;
        row += (int64_t)gridDim.x * kWavesPerBlock) {
     const int64_t u = a.sources ? (int64_t)a.sources[row] : row;
     const bool live = u >= 0 && u < a.num_nodes;
-    uint32_t my_steps = 0;
+    uint32_t my_steps = 0;  // this lane's edge steps for this source
 
     // ---- 1. walks -------------------------------------------------------
 #pragma unroll
@@ -91,36 +180,35 @@ __global__ __launch_bounds__(256) void walk_topt_kernel(WalkLaunch a) {
       if (slot >= WH || !live) strip[slot] = kEmpty;
     }
     if (live) {
-      for (int w = lane; w < a.walks; w += kWave) {
-        uint32_t* mine = strip + w * a.hops;
-        int64_t cur = u;
-        int landed = 0;
-        int s = 0;
-        uint4 rnd = make_uint4(0, 0, 0, 0);
-        while (landed < a.hops && s < 2 * a.hops) {
-          const int64_t lo = (int64_t)off[cur];
-          const int64_t hi = (int64_t)off[cur + 1];
-          const int64_t deg = hi - lo;
-          if (deg <= 0 || lo < 0 || hi > a.nnz) break;
-          if ((s & 3) == 0)
-            rnd = philox4x32_10(make_uint4((uint32_t)u, (uint32_t)w, (uint32_t)(s >> 2), 0u), k0,
-                                k1);
-          const uint32_t r = pick_word(rnd, s);
-          const int64_t j = (int64_t)(((uint64_t)r * (uint64_t)deg) >> 32);
-          const int32_t nxt = col[lo + j];
-          if (nxt < 0 || (int64_t)nxt >= a.num_nodes) break;
-          cur = nxt;
-          ++s;
-          if (cur < a.num_pins) {
-            mine[landed] = (cur != u) ? (uint32_t)cur : kEmpty;
-            ++landed;
+      // Two walks per lane in lockstep (w0 and w0 + 64): their dependent
+      // offset -> neighbour reads overlap.
+      for (int w0 = lane; w0 < a.walks; w0 += 2 * kWave) {
+        Walker<OffT> A, B;
+        A.start(u, w0, strip + w0 * a.hops, true);
+        B.start(u, w0 + kWave, strip + (w0 + kWave) * a.hops, w0 + kWave < a.walks);
+        while (A.active || B.active) {
+          int64_t loA = 0, hiA = 0, loB = 0, hiB = 0;
+          if (A.active) {
+            loA = (int64_t)off[A.cur];
+            hiA = (int64_t)off[A.cur + 1];
           }
+          if (B.active) {
+            loB = (int64_t)off[B.cur];
+            hiB = (int64_t)off[B.cur + 1];
+          }
+          A.pick(loA, hiA, a.nnz, k0, k1);
+          B.pick(loB, hiB, a.nnz, k0, k1);
+          const int32_t nA = A.active ? col[A.next_at] : 0;
+          const int32_t nB = B.active ? col[B.next_at] : 0;
+          A.land(nA, a.num_pins, a.num_nodes, a.hops);
+          B.land(nB, a.num_pins, a.num_nodes, a.hops);
         }
-        for (int h = landed; h < a.hops; ++h) mine[h] = kEmpty;
-        my_steps += (uint32_t)s;
+        my_steps += A.finish(a.hops) + B.finish(a.hops);
       }
     }
     wave_lds_sync();
+
+    if (a.total_steps) wave_steps += (unsigned)wave_sum_i32((int)my_steps);
 
     // ---- 2. sort visits by id -------------------------------------------
     uint32_t key[E];
@@ -129,88 +217,101 @@ __global__ __launch_bounds__(256) void walk_topt_kernel(WalkLaunch a) {
     wave_lds_sync();
     bitonic_sort_wave<E>(key, lane);
 
-    // ---- 3. runs -> (count, rank in id order) ----------------------------
+    // ---- 3. runs -> visit count of each distinct id (at the run's tail) --
     const uint32_t prev_last = __shfl_up(key[E - 1], 1);
     const uint32_t next_first = __shfl_down(key[0], 1);
-    bool head[E], tail[E];
-    int lane_heads = 0;
+    bool head[E];
     int lane_last_head = -1;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int i = lane * E + e;
-      const bool valid = key[e] != kEmpty;
-      const bool has_prev = i > 0;
       const uint32_t prev = e == 0 ? prev_last : key[e - 1];
-      const uint32_t next = e == E - 1 ? (lane == kWave - 1 ? kEmpty : next_first) : key[e + 1];
-      head[e] = valid && (!has_prev || prev != key[e]);
-      tail[e] = valid && next != key[e];
-      if (head[e]) {
-        ++lane_heads;
-        lane_last_head = i;
-      }
+      head[e] = key[e] != kEmpty && (i == 0 || prev != key[e]);
+      if (head[e]) lane_last_head = i;
     }
-    const int incl_heads = wave_inclusive_sum(lane_heads, lane);
-    const int distinct = __shfl(incl_heads, kWave - 1);
-    int run_heads = incl_heads - lane_heads;
     const int incl_last = wave_inclusive_max(lane_last_head, lane);
     int head_pos = __shfl_up(incl_last, 1);
     if (lane == 0) head_pos = -1;
-    uint32_t key2[E];
+    int cnt[E];
+    int lane_cmax = 0;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int i = lane * E + e;
-      if (head[e]) {
-        head_pos = i;
-        ++run_heads;
-      }
-      key2[e] = kEmpty;
-      if (tail[e]) {
-        const uint32_t c = (uint32_t)(i - head_pos + 1);
-        const uint32_t p = (uint32_t)(run_heads - 1);
-        key2[e] = ((0xFFFFu - c) << 16) | p;
-        strip[p] = key[e];
-      }
+      if (head[e]) head_pos = i;
+      const uint32_t next = e == E - 1 ? (lane == kWave - 1 ? kEmpty : next_first) : key[e + 1];
+      const bool tail = key[e] != kEmpty && next != key[e];
+      cnt[e] = tail ? i - head_pos + 1 : 0;
+      lane_cmax = cnt[e] > lane_cmax ? cnt[e] : lane_cmax;
     }
-    wave_lds_sync();
 
-    // ---- 4. order by (count desc, id asc); keep the first T ---------------
-    bitonic_sort_wave<E>(key2, lane);
-    const int keep = distinct < T ? distinct : T;
-    int my_sum = 0;
+    // ---- 4. rank by (count desc, id asc); keep the first T ---------------
+    // Ids ascend across (lane, e), so inside one count class the rank order is
+    // the position order. Classes are visited from the highest count down; an
+    // entry's rank is the number of entries in the classes above plus its
+    // position in its own class (a wave scan per class).
+    int rank[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int i = lane * E + e;
-      if (i < keep) my_sum += (int)(0xFFFFu - (key2[e] >> 16));
+    for (int e = 0; e < E; ++e) rank[e] = T;  // T = not kept
+    int placed = 0;    // entries in the classes visited so far
+    int kept_sum = 0;  // sum of the kept counts
+    int c = wave_max_i32(lane_cmax);
+    while (c > 0 && placed < T) {
+      int lc = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) lc += cnt[e] == c ? 1 : 0;
+      const int incl = wave_inclusive_sum(lc, lane);
+      const int total_c = __builtin_amdgcn_readlane(incl, kWave - 1);
+      int r = placed + incl - lc;
+      int below = 0;
+      // Branch-free: every element takes the same instruction path.
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const bool in = cnt[e] == c;
+        rank[e] = (in && r < T) ? r : rank[e];
+        r += in ? 1 : 0;
+        below = (cnt[e] < c && cnt[e] > below) ? cnt[e] : below;
+      }
+      const int take = total_c < T - placed ? total_c : T - placed;
+      kept_sum += take * c;
+      placed += total_c;
+      c = wave_max_i32(below);
     }
-    const int total = wave_sum_i32(my_sum);
-    const int64_t base = row * (int64_t)T;
+    const int keep = placed < T ? placed : T;
+
+    // ---- 5. write the row -------------------------------------------------
+    // The kept entries are placed by rank in the wave's LDS strip (ids, then
+    // counts), then written with contiguous stores.
+    wave_lds_sync();
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const int i = lane * E + e;
-      if (i < T) {
-        if (i < keep) {
-          const uint32_t c = 0xFFFFu - (key2[e] >> 16);
-          const uint32_t p = key2[e] & 0xFFFFu;
-          a.idx[base + i] = (int32_t)strip[p];
-          a.counts[base + i] = (uint16_t)c;
-          if (a.weights) a.weights[base + i] = (float)c / (float)total;
-        } else {
-          a.idx[base + i] = -1;
-          a.counts[base + i] = 0;
-          if (a.weights) a.weights[base + i] = 0.0f;
-        }
+      if (rank[e] < T) {
+        strip[rank[e]] = key[e];
+        strip[kStripOut + rank[e]] = (uint32_t)cnt[e];
       }
     }
-    for (int i = kWave * E + lane; i < T; i += kWave) {
-      a.idx[base + i] = -1;
-      a.counts[base + i] = 0;
-      if (a.weights) a.weights[base + i] = 0.0f;
-    }
-    if (a.total_steps) {
-      const int steps = wave_sum_i32((int)my_steps);
-      if (lane == 0 && steps) atomicAdd(a.total_steps, (unsigned long long)steps);
+    wave_lds_sync();
+    const int64_t base = row * (int64_t)T;
+    for (int i = lane; i < T; i += kWave) {
+      const bool kept = i < keep;
+      const uint32_t cc = kept ? strip[kStripOut + i] : 0u;
+      a.idx[base + i] = kept ? (int32_t)strip[i] : -1;
+      a.counts[base + i] = (uint16_t)cc;
+      if (a.weights) a.weights[base + i] = kept ? (float)cc / (float)kept_sum : 0.0f;
     }
     wave_lds_sync();
+  }
+  // Edge steps: one sum per wave over all its sources, one atomic per block
+  // (a per-source atomic on the single counter serialises at its L2 channel).
+  if (a.total_steps) {
+    __shared__ unsigned long long block_steps[kWavesPerBlock];
+    const unsigned long long ws = (unsigned long long)wave_steps;
+    if (lane == 0) block_steps[wave] = ws;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long t = 0;
+      for (int w = 0; w < kWavesPerBlock; ++w) t += block_steps[w];
+      if (t) atomicAdd(a.total_steps, t);
+    }
   }
 }
 
@@ -223,7 +324,9 @@ template <typename OffT>
 hipError_t launch_for_offsets(const WalkLaunch& a, hipStream_t s) {
   const int wh = a.walks * a.hops;
   const int64_t blocks_needed = (a.num_sources + kWavesPerBlock - 1) / kWavesPerBlock;
-  const int64_t cap = 1ll << 22;
+  // Enough resident blocks to fill the chip several times over; waves then
+  // loop over sources.
+  const int64_t cap = 1ll << 14;
   const dim3 grid((unsigned)(blocks_needed < cap ? blocks_needed : cap));
   const dim3 block(256);
   if (wh <= 64) hipLaunchKernelGGL((walk_topt_kernel<OffT, 1>), grid, block, 0, s, a);
