@@ -347,16 +347,16 @@ hipError_t launch_cfg(const GemmLaunch& a, hipStream_t s) {
 
 // Tile shapes per (dtype, epilogue, output width).
 #ifndef PINSAGE_CFG_Q_BF16
-#define PINSAGE_CFG_Q_BF16 Cfg<true, 256, 128, 2, 2, false, 32>
+#define PINSAGE_CFG_Q_BF16 Cfg<true, 128, 128, 2, 2, false, 32>
 #endif
 #ifndef PINSAGE_CFG_Q_F32
-#define PINSAGE_CFG_Q_F32 Cfg<false, 128, 128, 2, 2, false, 32>
+#define PINSAGE_CFG_Q_F32 Cfg<false, 256, 256, 4, 4, false, 16>
 #endif
 #ifndef PINSAGE_CFG_W256_BF16
-#define PINSAGE_CFG_W256_BF16 Cfg<true, 128, 256, 2, 2, true, 32>
+#define PINSAGE_CFG_W256_BF16 Cfg<true, 256, 256, 4, 4, true, 32, false>
 #endif
 #ifndef PINSAGE_CFG_W256_F32
-#define PINSAGE_CFG_W256_F32 Cfg<false, 128, 256, 2, 4, true, 32>
+#define PINSAGE_CFG_W256_F32 Cfg<false, 256, 256, 4, 4, true, 32>
 #endif
 #ifndef PINSAGE_CFG_W512_BF16
 #define PINSAGE_CFG_W512_BF16 Cfg<true, 128, 512, 2, 4, true, 32>
