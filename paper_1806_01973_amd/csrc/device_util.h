@@ -38,6 +38,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Two fp32 values to a packed bf16 pair (low half = lo) with the gfx950
+// conversion instruction: round to nearest, ties to even, like f32_to_bf16.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 // Orders LDS accesses of one wavefront across its lanes (all lanes of a wave
 // execute in lockstep; this keeps the compiler from reordering LDS traffic
 // across the point and waits for outstanding LDS operations).

@@ -5,24 +5,32 @@
 // two row sources (self rows through an optional row map, then the pooled
 // rows), B [N x K] row-major (the PyTorch Linear layout of Q and W).
 //
-// Work split: a 256-thread block (4 waves) owns a BM x BN output tile; waves
-// form a WAVES_M x WAVES_N grid and each wave owns (BM/WAVES_M) x
-// (BN/WAVES_N), i.e. TM x TN blocks of 32 x 32. K runs in chunks of BK: the
-// next chunk's global 16-byte vectors are loaded into registers while the
-// current chunk is multiplied out of LDS. Tiles are stored K-contiguous in
-// LDS with a 16-byte row pad so each lane's fragment read is one conflict-free
-// 16-byte LDS read.
+// Work split: a block of WAVES_M x WAVES_N waves owns a BM x BN output tile;
+// each wave owns (BM/WAVES_M) x (BN/WAVES_N), i.e. TM x TN blocks of 32 x 32.
 //
-// fp32 storage: v_mfma_f32_32x32x2_f32; the 2 k-values of one MFMA step come
-// from the two half-waves, and step j of a chunk pairs half h with chunk
-// column h*(BK/2) + j, so each lane reads BK/2 consecutive values of its row.
-// bf16 storage: v_mfma_f32_32x32x16_bf16 (gfx950); half h supplies chunk
-// columns 16*j + 8*h .. +7. Accumulation is fp32 in both cases.
+// K pipeline: K runs in chunks of 64 bytes per row (32 bf16 / 16 fp32
+// columns). Chunks travel global -> LDS by DMA (global_load_lds_dwordx4, no
+// register staging) into a ring of STAGES LDS stages, STAGES - 1 chunks ahead
+// of the MFMAs; one barrier per chunk. A stage packs rows in groups of 16; one
+// DMA instruction of a wave fills one group (1 KB, row r of the group at
+// 64 r): lanes 4r .. 4r+3 carry the four 16-byte vectors of row r, so a quad
+// of lanes reads one contiguous 64-byte piece of a row. Inside a row, vector v
+// sits in slot v ^ f(r), f(r) = ((r >> 1) ^ (r >> 3)) & 3, which spreads the
+// 16 (resp. 8) rows of one LDS fragment read over distinct banks. Missing rows
+// and the K tail read a static zero row, so loads never branch.
+//
+// fp32 storage: v_mfma_f32_32x32x2_f32; step st of a chunk pairs half-wave h
+// with chunk column 8h + st (two 16-byte reads per fragment). bf16 storage:
+// v_mfma_f32_32x32x16_bf16 (gfx950); k-step ks takes vector 2ks + h. fp32
+// accumulation in both cases. The weight fragment is the MFMA's first
+// operand, so the accumulators hold C^T blocks: a lane owns one output row
+// and runs of 4 adjacent output columns, stored as one 8-byte (bf16) or
+// 16-byte (fp32) vector.
 //
 // Epilogue: + bias, ReLU, store in the storage dtype; with L2 the block spans
-// all N columns, row sums of squares are reduced across lanes with a fixed
-// butterfly and across waves in a fixed order through LDS, and every row is
-// scaled by 1/||z|| (zero rows stay zero).
+// all N columns, and a row's sum of squares is added over the lane's own
+// columns, its partner half-wave and then the waves of the row band in a fixed
+// order through LDS; every row is scaled by 1/||z|| (zero rows stay zero).
 //
 // Tile order is XCD-aware: hardware hands block b to XCD b % 8; blocks are
 // renumbered so that each XCD gets a contiguous run of tiles, keeping the
@@ -36,32 +44,44 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <bool BF16, int BM_, int BN_, int WAVES_M_, int WAVES_N_, bool L2_, int BK_ = 32,
-          bool PREFETCH_ = true>
+// A row of zeros as long as the widest A row (d_in + m <= 16384 fp32): rows
+// that do not exist and the K tail read from here. Never written.
+constexpr int kMaxGemmK = 16384;
+__device__ __attribute__((aligned(16))) float g_zero_row[kMaxGemmK];
+
+constexpr int kChunkRowBytes = 64;   // bytes of one row per K chunk
+constexpr int kGroupBytes = 1024;    // 16 rows x 64 bytes: one DMA instruction
+
+// Slot of 16-byte vector v of row r (r mod 16) inside the row's 64 bytes.
+__device__ __forceinline__ int vec_slot(int r, int v) { return v ^ (((r >> 1) ^ (r >> 3)) & 3); }
+
+template <bool BF16, int BM_, int BN_, int WAVES_M_, int WAVES_N_, bool L2_, int STAGES_>
 struct Cfg {
   static constexpr bool kBf16 = BF16;
-  static constexpr bool kPrefetch = PREFETCH_;  // read next k-step fragments early
   static constexpr bool kTwoSources = L2_;  // the W layer reads [h_self | n]
+  static constexpr bool L2 = L2_;
   static constexpr int BM = BM_, BN = BN_;
   static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
-  static constexpr int THREADS = 64 * WAVES_M * WAVES_N;
-  static constexpr bool L2 = L2_;
-  static constexpr int ESZ = BF16 ? 2 : 4;      // bytes per element
-  static constexpr int VEC = 16 / ESZ;           // elements per 16-byte vector
-  static constexpr int BK = BK_;                 // K chunk (elements)
-  static constexpr int LDK = BK + VEC;           // LDS row stride (elements)
+  static constexpr int NWAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * NWAVES;
+  static constexpr int STAGES = STAGES_;
+  static constexpr int ESZ = BF16 ? 2 : 4;       // bytes per element
+  static constexpr int VEC = 16 / ESZ;            // elements per 16-byte vector
+  static constexpr int BK = kChunkRowBytes / ESZ; // K columns per chunk
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   static constexpr int TM = WM / 32, TN = WN / 32;
-  static constexpr int VROW = BK / VEC;          // 16-byte vectors per chunk row
-  static constexpr int A_VECS = BM * VROW / THREADS;  // per thread
-  static constexpr int B_VECS = BN * VROW / THREADS;
-  static constexpr int RSTEP = THREADS / VROW;        // rows between a thread's vectors
-  static constexpr int STAGE_BYTES = (BM + BN) * LDK * ESZ;
+  static constexpr int A_GROUPS = BM / 16;
+  static constexpr int GROUPS = (BM + BN) / 16;
+  static constexpr int DPW = GROUPS / NWAVES;     // DMA instructions per wave per chunk
+  static constexpr int PENDING = (STAGES - 2) * DPW;
+  static constexpr int STAGE_BYTES = GROUPS * kGroupBytes;
   static constexpr int RED_BYTES = L2 ? WAVES_N * BM * 4 : 0;
+  static constexpr int BIAS_BYTES = BN * 4;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES + RED_BYTES + BIAS_BYTES;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile is a multiple of 32x32");
-  static_assert((BM * VROW) % THREADS == 0 && (BN * VROW) % THREADS == 0, "even vector split");
-  static_assert(THREADS % VROW == 0, "a thread keeps one K offset");
-  static_assert(2 * STAGE_BYTES + RED_BYTES <= 160 * 1024, "LDS budget of one workgroup");
+  static_assert(GROUPS % NWAVES == 0, "every wave issues the same DMA count");
+  static_assert(STAGES >= 2 && PENDING <= 63, "vmcnt range");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
 __device__ __forceinline__ int xcd_tile(int b, int nt) {
@@ -70,15 +90,38 @@ __device__ __forceinline__ int xcd_tile(int b, int nt) {
   return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
 }
 
+// One 16-byte-per-lane DMA from global memory into LDS: lane l's vector lands
+// at byte lds_base + 16 l (lds_base wave-uniform, via M0).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory");
+}
+
+// Waits until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// Workgroup barrier after this wave's LDS operations have completed.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+}
+
 template <typename C>
 __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
-  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, LDK = C::LDK, VEC = C::VEC;
-  constexpr int TM = C::TM, TN = C::TN, VROW = C::VROW, THREADS = C::THREADS;
-  constexpr int ESZ = C::ESZ;
-  // LDS: two stages of (A tile, B tile), K-contiguous padded rows, then the
-  // cross-wave row-norm partials.
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES + C::RED_BYTES];
-  float* red = reinterpret_cast<float*>(smem + 2 * C::STAGE_BYTES);
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, VEC = C::VEC;
+  constexpr int TM = C::TM, TN = C::TN, THREADS = C::THREADS, ESZ = C::ESZ;
+  constexpr int DPW = C::DPW, STAGES = C::STAGES;
+  // LDS: the stage ring, then the cross-wave row-norm partials and the
+  // block's bias slice.
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS_BYTES];
+  float* red = reinterpret_cast<float*>(smem + STAGES * C::STAGE_BYTES);
+  float* bias_s = reinterpret_cast<float*>(smem + STAGES * C::STAGE_BYTES + C::RED_BYTES);
+  const uint32_t smem_base =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -90,66 +133,65 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   const int64_t m0 = (int64_t)(tile / tiles_n) * BM;
   const int n0 = (tile % tiles_n) * BN;
   const int K = a.K0 + a.K1;
+  // Bias slice of the block (zero past N).
+  for (int c = tid; c < BN; c += THREADS) bias_s[c] = n0 + c < a.N ? a.bias[n0 + c] : 0.0f;
 
-  // ---- per-thread load slots (fixed across the K loop) -------------------
-  // Thread t loads the 16-byte vector (row r0 + i*RSTEP, column kv) of each
-  // chunk, i < A_VECS (resp. B_VECS).
-  const int r0 = tid / VROW;
-  const int kv = (tid % VROW) * VEC;
-  const unsigned char* a0_row[C::A_VECS];
-  const unsigned char* a1_row[C::kTwoSources ? C::A_VECS : 1];
+  // ---- DMA slots (fixed across the K loop) --------------------------------
+  // Slot d of this wave fills group wave*DPW + d of every stage: A groups
+  // first, then B groups. Lane l serves row 16 * group + (l >> 2) and LDS
+  // slot l & 3 of it, i.e. column vector vec_slot(l >> 2, l & 3). Source-1
+  // pointers are biased by -K0 columns so both sources take the column kk;
+  // rows that do not exist point at the zero row.
+  const unsigned char* const zrow = reinterpret_cast<const unsigned char*>(g_zero_row);
+  const int64_t k0b = (int64_t)a.K0 * ESZ;
+  const unsigned char* p0[DPW];
+  const unsigned char* p1[C::kTwoSources ? DPW : 1];
 #pragma unroll
-  for (int i = 0; i < C::A_VECS; ++i) {
-    const int64_t gr = m0 + r0 + i * C::RSTEP;
-    a0_row[i] = nullptr;
-    if constexpr (C::kTwoSources) a1_row[i] = nullptr;
-    if (gr < a.M) {
-      const int64_t src = a.rowmap ? (int64_t)a.rowmap[gr] : gr;
-      if (src >= 0 && src < a.rows_a0)
-        a0_row[i] = static_cast<const unsigned char*>(a.A0) + src * a.lda0 * ESZ;
-      if constexpr (C::kTwoSources)
-        a1_row[i] = static_cast<const unsigned char*>(a.A1) + gr * a.lda1 * ESZ;
-    }
-  }
-  const unsigned char* b_row[C::B_VECS];
-#pragma unroll
-  for (int i = 0; i < C::B_VECS; ++i) {
-    const int r = r0 + i * C::RSTEP;
-    b_row[i] = (n0 + r < a.N)
-                   ? static_cast<const unsigned char*>(a.B) + (int64_t)(n0 + r) * K * ESZ
-                   : nullptr;
-  }
-
-  uint4 a_stage[C::A_VECS], b_stage[C::B_VECS];
-  auto load_chunk = [&](int kc) {
-    const int kk = kc + kv;
-#pragma unroll
-    for (int i = 0; i < C::A_VECS; ++i) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kk < a.K0) {
-        if (a0_row[i]) v = *reinterpret_cast<const uint4*>(a0_row[i] + (int64_t)kk * ESZ);
-      } else if constexpr (C::kTwoSources) {
-        if (kk < K && a1_row[i])
-          v = *reinterpret_cast<const uint4*>(a1_row[i] + (int64_t)(kk - a.K0) * ESZ);
+  for (int d = 0; d < DPW; ++d) {
+    const int grp = wave * DPW + d;
+    const int rr = lane >> 2;
+    if (grp < C::A_GROUPS) {
+      const int64_t gr = m0 + grp * 16 + rr;
+      const bool in_m = gr < a.M;
+      const int64_t src = !in_m ? -1 : (a.rowmap ? (int64_t)a.rowmap[gr] : gr);
+      p0[d] = (src >= 0 && src < a.rows_a0)
+                  ? static_cast<const unsigned char*>(a.A0) + src * a.lda0 * ESZ
+                  : zrow;
+      if constexpr (C::kTwoSources) {
+        const unsigned char* q =
+            in_m ? static_cast<const unsigned char*>(a.A1) + gr * a.lda1 * ESZ : zrow;
+        p1[d] = reinterpret_cast<const unsigned char*>(reinterpret_cast<uintptr_t>(q) - k0b);
       }
-      a_stage[i] = v;
+    } else {
+      const int r = n0 + (grp - C::A_GROUPS) * 16 + rr;
+      p0[d] = r < a.N ? static_cast<const unsigned char*>(a.B) + (int64_t)r * K * ESZ : zrow;
+      if constexpr (C::kTwoSources) p1[d] = p0[d];
     }
+  }
+  const int kvec = vec_slot(lane >> 2, lane & 3) * VEC;
+  const int nchunks = (K + BK - 1) / BK;
+  // Tiles start their K sweep at different chunks (rotation by tile index):
+  // rows of A and B sit at power-of-two strides, and blocks that all read the
+  // same K columns at once would pile onto a few L2 channels.
+  const int kshift = tile % nchunks;
+  // Issues the DMAs of the chunk-th chunk of this tile's sweep into its
+  // stage. Sweep positions past the end read the zero row, which keeps the
+  // in-flight count uniform for wait_vmcnt.
+  auto issue = [&](int chunk) __attribute__((always_inline)) {
+    int kc = chunk + kshift;
+    kc = chunk >= nchunks ? nchunks : (kc >= nchunks ? kc - nchunks : kc);
+    const int kk = kc * BK + kvec;
+    const bool kin = kk < K;
+    const int64_t off = (int64_t)kk * ESZ;
+    const uint32_t dst = smem_base + (uint32_t)((chunk % STAGES) * C::STAGE_BYTES) +
+                         (uint32_t)(wave * DPW * kGroupBytes);
 #pragma unroll
-    for (int i = 0; i < C::B_VECS; ++i) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (b_row[i] && kk < K) v = *reinterpret_cast<const uint4*>(b_row[i] + (int64_t)kk * ESZ);
-      b_stage[i] = v;
+    for (int d = 0; d < DPW; ++d) {
+      const unsigned char* p;
+      if constexpr (C::kTwoSources) p = (kk < a.K0 ? p0[d] : p1[d]) + off;
+      else p = p0[d] + off;
+      dma16(kin ? p : zrow, __builtin_amdgcn_readfirstlane(dst + d * kGroupBytes));
     }
-  };
-  auto store_chunk = [&](unsigned char* stage) {
-    unsigned char* As = stage + (r0 * LDK + kv) * ESZ;
-    unsigned char* Bs = stage + (BM * LDK + r0 * LDK + kv) * ESZ;
-#pragma unroll
-    for (int i = 0; i < C::A_VECS; ++i)
-      *reinterpret_cast<uint4*>(As + i * C::RSTEP * LDK * ESZ) = a_stage[i];
-#pragma unroll
-    for (int i = 0; i < C::B_VECS; ++i)
-      *reinterpret_cast<uint4*>(Bs + i * C::RSTEP * LDK * ESZ) = b_stage[i];
   };
 
   f32x16 acc[TM][TN];
@@ -164,176 +206,171 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   const int half = lane >> 5;
   const int a_base_row = wm * C::WM;
   const int b_base_row = wn * C::WN;
+  // Byte offset of a lane's fragment row (block-relative row r of A, resp.
+  // B) in a stage. Fragment rows start at multiples of 32, so the row's place
+  // in its group (lane & 15) and hence its vector slots depend on the lane.
+  auto frag_off = [&](int r) __attribute__((always_inline)) {
+    return (r >> 4) * kGroupBytes + (r & 15) * kChunkRowBytes;
+  };
+  const int fa_off = frag_off(a_base_row + row_in_blk);
+  const int fb_off = C::A_GROUPS * kGroupBytes + frag_off(b_base_row + row_in_blk);
+  // Byte offset of the vector a lane reads in half-step hs.
+  auto vec_off = [&](int hs) __attribute__((always_inline)) {
+    const int v = C::kBf16 ? 2 * hs + half : 2 * half + hs;
+    return vec_slot(lane & 15, v) * 16;
+  };
+  const int voff0 = vec_off(0), voff1 = vec_off(1);
 
-  // Multiplies one LDS stage into the accumulators; the fragments of the
-  // next k-step are read while the current MFMAs issue.
-  auto compute = [&](const unsigned char* stage) {
-    const unsigned char* As = stage;
-    const unsigned char* Bs = stage + BM * LDK * ESZ;
-    if constexpr (!C::kBf16) {
-      // Half h covers chunk columns [h*BK/2, (h+1)*BK/2), read 8 at a time.
-      constexpr int GROUPS = (BK / 2) / 8;
-      constexpr int NB = C::kPrefetch ? 2 : 1;
-      float fa[NB][TM][8], fb[NB][TN][8];
-      auto load = [&](int g, float (&xa)[TM][8], float (&xb)[TN][8]) {
+  // A chunk is multiplied in two half-steps hs = 0, 1. bf16: half-step hs is
+  // the MFMA k-step hs, half-wave h reads column vector 2hs + h. fp32: MFMA
+  // steps 4hs .. 4hs+3, half-wave h reads vector 2h + hs (column 8h + st).
+  constexpr int FW = 4;  // 32-bit words per fragment per half-step
+  typedef uint32_t frag_t __attribute__((ext_vector_type(FW)));
+  struct Frags {
+    frag_t a[TM], b[TN];
+  };
+  auto read_frags = [&](const unsigned char* stage, int hs, Frags& f)
+      __attribute__((always_inline)) {
+    const int v = hs ? voff1 : voff0;
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const float* p = reinterpret_cast<const float*>(As) +
-                           (a_base_row + i * 32 + row_in_blk) * LDK + half * (BK / 2) + 8 * g;
-          const float4 x = *reinterpret_cast<const float4*>(p);
-          const float4 y = *reinterpret_cast<const float4*>(p + 4);
-          xa[i][0] = x.x; xa[i][1] = x.y; xa[i][2] = x.z; xa[i][3] = x.w;
-          xa[i][4] = y.x; xa[i][5] = y.y; xa[i][6] = y.z; xa[i][7] = y.w;
-        }
+    for (int i = 0; i < TM; ++i)
+      f.a[i] = *reinterpret_cast<const frag_t*>(stage + fa_off + i * 2 * kGroupBytes + v);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const float* p = reinterpret_cast<const float*>(Bs) +
-                           (b_base_row + j * 32 + row_in_blk) * LDK + half * (BK / 2) + 8 * g;
-          const float4 x = *reinterpret_cast<const float4*>(p);
-          const float4 y = *reinterpret_cast<const float4*>(p + 4);
-          xb[j][0] = x.x; xb[j][1] = x.y; xb[j][2] = x.z; xb[j][3] = x.w;
-          xb[j][4] = y.x; xb[j][5] = y.y; xb[j][6] = y.z; xb[j][7] = y.w;
-        }
-      };
-      if constexpr (C::kPrefetch) load(0, fa[0], fb[0]);
+    for (int j = 0; j < TN; ++j)
+      f.b[j] = *reinterpret_cast<const frag_t*>(stage + fb_off + j * 2 * kGroupBytes + v);
+  };
+  auto mfma_half = [&](const Frags& f) __attribute__((always_inline)) {
+    if constexpr (C::kBf16) {
 #pragma unroll
-      for (int g = 0; g < GROUPS; ++g) {
-        const int cb = C::kPrefetch ? (g & 1) : 0;
-        if constexpr (C::kPrefetch) {
-          if (g + 1 < GROUPS) load(g + 1, fa[(g + 1) & 1], fb[(g + 1) & 1]);
-        } else {
-          load(g, fa[0], fb[0]);
-        }
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[cb][i][st], fb[cb][j][st],
-                                                               acc[i][j], 0, 0, 0);
-      }
-    } else {
-      constexpr int KSTEPS = BK / 16;
-      constexpr int NB = C::kPrefetch ? 2 : 1;
-      bf16x8 fa[NB][TM], fb[NB][TN];
-      auto load = [&](int ks, bf16x8 (&xa)[TM], bf16x8 (&xb)[TN]) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          xa[i] = *reinterpret_cast<const bf16x8*>(
-              As + ((a_base_row + i * 32 + row_in_blk) * LDK + 16 * ks + half * 8) * 2);
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          xb[j] = *reinterpret_cast<const bf16x8*>(
-              Bs + ((b_base_row + j * 32 + row_in_blk) * LDK + 16 * ks + half * 8) * 2);
-      };
-      if constexpr (C::kPrefetch) load(0, fa[0], fb[0]);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, f.b[j]), __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j],
+              0, 0, 0);
+    } else {
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
-        const int cb = C::kPrefetch ? (ks & 1) : 0;
-        if constexpr (C::kPrefetch) {
-          if (ks + 1 < KSTEPS) load(ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-        } else {
-          load(ks, fa[0], fb[0]);
-        }
+      for (int st = 0; st < 4; ++st)
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fb[cb][j], acc[i][j],
-                                                                0, 0, 0);
-      }
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                __uint_as_float(f.b[j][st]), __uint_as_float(f.a[i][st]), acc[i][j], 0, 0, 0);
     }
   };
+  auto stage_of = [&](int chunk) __attribute__((always_inline)) {
+    return smem + (chunk % STAGES) * C::STAGE_BYTES;
+  };
 
-  // Double-buffered K loop: one barrier per chunk; the next chunk's global
-  // loads are in flight while the current stage is multiplied out.
-  const int nchunks = (K + BK - 1) / BK;
-  load_chunk(0);
-  store_chunk(smem);
-  __syncthreads();
-  for (int it = 0; it < nchunks; ++it) {
-    const unsigned char* cur = smem + (it & 1) * C::STAGE_BYTES;
-    unsigned char* nxt = smem + ((it + 1) & 1) * C::STAGE_BYTES;
-    const bool more = it + 1 < nchunks;
-    if (more) load_chunk((it + 1) * BK);
-    compute(cur);
-    if (more) store_chunk(nxt);
-    __syncthreads();
+  // Ring protocol: chunks 0..STAGES-2 are in flight before the loop. Before
+  // the fragments of chunk c+1 are read, each wave waits for its DMAs of that
+  // chunk (STAGES - 2 younger chunks may stay in flight) and for its own LDS
+  // reads of chunk c, then a barrier makes all DMAs visible and frees chunk
+  // c's stage, which receives chunk c + STAGES. The half-step MFMAs issued
+  // just before the barrier keep the matrix pipe busy across it.
+#pragma unroll
+  for (int c = 0; c < STAGES - 1; ++c) issue(c);
+  wait_vmcnt<C::PENDING>();
+  lds_barrier();
+  issue(STAGES - 1);
+  Frags f0, f1;
+  read_frags(stage_of(0), 0, f0);
+  // The last chunk is peeled off so the loop body has no branch: every
+  // half-step's fragment reads then have a known count of younger reads.
+  // Scheduling barriers pin the order: fragment reads go out right before a
+  // half-step's 16 MFMAs that hide their latency.
+  for (int c = 0; c + 1 < nchunks; ++c) {
+    read_frags(stage_of(c), 1, f1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_half(f0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<C::PENDING>();
+    lds_barrier();
+    read_frags(stage_of(c + 1), 0, f0);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(c + STAGES);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_half(f1);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  read_frags(stage_of(nchunks - 1), 1, f1);
+  mfma_half(f0);
+  mfma_half(f1);
+  wait_vmcnt<0>();  // drain the zero-row DMAs issued past the end
+  __syncthreads();  // bias slice (and, below, row partials) visible
 
   // ---- epilogue -----------------------------------------------------------
-  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) +
-  // e%4, column l%32 of the block.
-  float bias_v[TN];
-  int col_of[TN];
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    col_of[j] = n0 + b_base_row + j * 32 + row_in_blk;
-    bias_v[j] = col_of[j] < a.N ? a.bias[col_of[j]] : 0.0f;
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
+  // Lane l: output row m0 + a_base_row + 32i + l%32; for group g of tile j,
+  // output columns c0(j, g) + 0..3 with c0 = b_base_row + 32j + 8g + 4(l/32)
+  // inside the block. N is a multiple of 16, so a group is all in or all out;
+  // columns past N have zero weights and zero bias, so they stay zero.
+  // Row bands are finished one at a time to keep few accumulators live.
+  auto c0 = [&](int j, int g) __attribute__((always_inline)) { return b_base_row + j * 32 + 8 * g + 4 * half; };
+  auto bias_relu = [&](int i) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float z = acc[i][j][e] + bias_v[j];
-        acc[i][j][e] = (z > 0.0f && col_of[j] < a.N) ? z : 0.0f;
+      for (int g = 0; g < 4; ++g) {
+        const float4 bv = *reinterpret_cast<const float4*>(bias_s + c0(j, g));
+        acc[i][j][4 * g + 0] = fmaxf(acc[i][j][4 * g + 0] + bv.x, 0.0f);
+        acc[i][j][4 * g + 1] = fmaxf(acc[i][j][4 * g + 1] + bv.y, 0.0f);
+        acc[i][j][4 * g + 2] = fmaxf(acc[i][j][4 * g + 2] + bv.z, 0.0f);
+        acc[i][j][4 * g + 3] = fmaxf(acc[i][j][4 * g + 3] + bv.w, 0.0f);
       }
-
-  if constexpr (C::L2) {
-    // Row partial sums over this wave's columns.
-    float part[TM][16];
+  };
+  auto store_band = [&](int i, float scale) __attribute__((always_inline)) {
+    const int64_t r = m0 + a_base_row + i * 32 + row_in_blk;
+    if (r >= a.M) return;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float s = 0.0f;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) s = fmaf(acc[i][j][e], acc[i][j][e], s);
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-        part[i][e] = s;
-      }
-    if (row_in_blk == 0) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = a_base_row + i * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-          red[wn * BM + r] = part[i][e];
+      for (int g = 0; g < 4; ++g) {
+        const int c = n0 + c0(j, g);
+        if (c >= a.N) continue;
+        const int64_t o = r * a.N + c;
+        const float v0 = acc[i][j][4 * g] * scale, v1 = acc[i][j][4 * g + 1] * scale;
+        const float v2 = acc[i][j][4 * g + 2] * scale, v3 = acc[i][j][4 * g + 3] * scale;
+        if constexpr (C::kBf16) {
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + o) =
+              make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+        } else {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.C) + o) = make_float4(v0, v1, v2, v3);
         }
+      }
+  };
+
+  if constexpr (!C::L2) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      bias_relu(i);
+      store_band(i, 1.0f);
+    }
+  } else {
+    // Sum of squares of each row: over the lane's columns, then its partner
+    // half-wave (lane ^ 32), then the WAVES_N waves of the row band in a
+    // fixed order through LDS.
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      bias_relu(i);
+      float s = 0.0f;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s = fmaf(acc[i][j][e], acc[i][j][e], s);
+      s += __shfl_xor(s, 32);
+      if (half == 0) red[wn * BM + a_base_row + i * 32 + row_in_blk] = s;
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+      const int r = a_base_row + i * 32 + row_in_blk;
+      float ss = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = a_base_row + i * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-        float ss = 0.0f;
-#pragma unroll
-        for (int w = 0; w < C::WAVES_N; ++w) ss += red[w * BM + r];
-        const float inv = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j][e] *= inv;
-      }
-  }
-
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t r = m0 + a_base_row + i * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-      if (r >= a.M) continue;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        if (col_of[j] >= a.N) continue;
-        const int64_t o = r * a.N + col_of[j];
-        if constexpr (C::kBf16) static_cast<uint16_t*>(a.C)[o] = f32_to_bf16(acc[i][j][e]);
-        else static_cast<float*>(a.C)[o] = acc[i][j][e];
-      }
+      for (int w = 0; w < C::WAVES_N; ++w) ss += red[w * BM + r];
+      store_band(i, ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f);
     }
+  }
 }
 
 template <typename C>
@@ -347,22 +384,22 @@ hipError_t launch_cfg(const GemmLaunch& a, hipStream_t s) {
 
 // Tile shapes per (dtype, epilogue, output width).
 #ifndef PINSAGE_CFG_Q_BF16
-#define PINSAGE_CFG_Q_BF16 Cfg<true, 128, 128, 2, 2, false, 32>
+#define PINSAGE_CFG_Q_BF16 Cfg<true, 256, 256, 2, 2, false, 4>
 #endif
 #ifndef PINSAGE_CFG_Q_F32
-#define PINSAGE_CFG_Q_F32 Cfg<false, 256, 256, 4, 4, false, 16>
+#define PINSAGE_CFG_Q_F32 Cfg<false, 256, 256, 4, 4, false, 4>
 #endif
 #ifndef PINSAGE_CFG_W256_BF16
-#define PINSAGE_CFG_W256_BF16 Cfg<true, 256, 256, 4, 4, true, 32, false>
+#define PINSAGE_CFG_W256_BF16 Cfg<true, 256, 256, 2, 2, true, 4>
 #endif
 #ifndef PINSAGE_CFG_W256_F32
-#define PINSAGE_CFG_W256_F32 Cfg<false, 256, 256, 4, 4, true, 32>
+#define PINSAGE_CFG_W256_F32 Cfg<false, 256, 256, 4, 4, true, 3>
 #endif
 #ifndef PINSAGE_CFG_W512_BF16
-#define PINSAGE_CFG_W512_BF16 Cfg<true, 128, 512, 2, 4, true, 32>
+#define PINSAGE_CFG_W512_BF16 Cfg<true, 128, 512, 2, 4, true, 3>
 #endif
 #ifndef PINSAGE_CFG_W512_F32
-#define PINSAGE_CFG_W512_F32 Cfg<false, 128, 512, 2, 4, true, 16>
+#define PINSAGE_CFG_W512_F32 Cfg<false, 128, 512, 2, 4, true, 3>
 #endif
 
 template <bool BF16>
@@ -372,8 +409,8 @@ hipError_t launch_typed(const GemmLaunch& a, hipStream_t s) {
     else return launch_cfg<PINSAGE_CFG_Q_F32>(a, s);
   }
   // The block must span every output column for the fused row norm.
-  if (a.N <= 64) return launch_cfg<Cfg<BF16, 128, 64, 4, 1, true, 32>>(a, s);
-  if (a.N <= 128) return launch_cfg<Cfg<BF16, 128, 128, 2, 2, true, 32>>(a, s);
+  if (a.N <= 64) return launch_cfg<Cfg<BF16, 128, 64, 4, 1, true, 4>>(a, s);
+  if (a.N <= 128) return launch_cfg<Cfg<BF16, 128, 128, 2, 2, true, 4>>(a, s);
   if (a.N <= 256) {
     if constexpr (BF16) return launch_cfg<PINSAGE_CFG_W256_BF16>(a, s);
     else return launch_cfg<PINSAGE_CFG_W256_F32>(a, s);
