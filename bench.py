@@ -77,7 +77,7 @@ def copy_calibration(gib: float = 1.0, reps: int = 5) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
 
 
-def load_inputs(wl):
+def load_inputs(wl, dataflow="pool_then_dense"):
     """Inputs on the GPU plus host views the CPU baseline needs."""
     import numpy as np
     import torch
@@ -101,7 +101,8 @@ def load_inputs(wl):
         x_rows = lambda n: data["x"][:n]
     layers_np = synth.make_layers(wl)
     g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards, offsets64=wl.offsets64)
-    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt) for L in layers_np]
+    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt, dataflow=dataflow)
+              for L in layers_np]
     torch.cuda.synchronize()
     log(f"inputs for {wl.name}: {wl.num_nodes} nodes, {E} edges in "
         f"{time.perf_counter() - t0:.1f}s")
@@ -117,14 +118,14 @@ def cpu_baseline_embed(inp, wl, threads: int) -> dict:
     import oracle
 
     N, P = wl.num_nodes, wl.num_pins
-    n_walk = min(N, 400_000)
+    n_walk = min(N, 1_500_000)
     p = P / N
     flops_row = 0.0
     d_prev = wl.d_in
     for _ in range(wl.K):
         flops_row += 2 * (p * d_prev * wl.m + (d_prev + wl.m) * wl.d_out)
         d_prev = wl.d_out
-    n_rows = int(min(N, 120_000, 150e9 / flops_row))
+    n_rows = int(min(N, 400_000, 600e9 / flops_row))
     rng = np.random.default_rng(123)
     src = np.sort(rng.choice(N, n_walk, replace=False)).astype(np.int32)
     t0 = time.perf_counter()
@@ -174,14 +175,21 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
     def per_launch(name, per_step):
         return per_step / (kernels[name]["launches"] / steps)
 
+    # The pool gathers m-wide rows of P (pool then dense) or d_out-wide rows of
+    # R = P W_n^T (dense then pool); the W GEMM then has K = d_in + m, resp. d_in.
+    split = [L.dataflow == "dense_then_pool" for L in layers]
+    width = [L.d_out if sp else L.m for L, sp in zip(layers, split)]
     if "pool" in kernels:
         k = kernels["pool"]
         k["algo_bytes_per_launch"] = per_launch(
-            "pool", sum(live_entries * L.m * esz + idx_bytes + N * L.m * esz for L in layers))
+            "pool", sum(live_entries * w * esz + idx_bytes + N * w * esz for w in width))
         k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
         k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
     for name, fl in (("gemm_q", sum(2.0 * n_transform * L.d_in * L.m for L in layers)),
-                     ("gemm_w", sum(2.0 * N * (L.d_in + L.m) * L.d_out for L in layers))):
+                     ("gemm_r", sum(2.0 * n_transform * L.m * L.d_out
+                                    for L, sp in zip(layers, split) if sp)),
+                     ("gemm_w", sum(2.0 * N * (L.d_in + (0 if sp else L.m)) * L.d_out
+                                    for L, sp in zip(layers, split)))):
         if name in kernels:
             k = kernels[name]
             k["algo_flops_per_launch"] = per_launch(name, fl)
@@ -199,7 +207,7 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
 def roofline_of(kernels, wl):
     dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     kd = kernels[dominant]
-    if dominant in ("gemm_q", "gemm_w"):
+    if dominant in ("gemm_q", "gemm_r", "gemm_w"):
         return {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
                 "peak": MFMA_PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s", "frac": kd["frac_mfma"],
                 "traffic": None}
@@ -319,6 +327,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="medium",
                     choices=["tiny", "medium", "minibatch", "large", "shard"])
+    ap.add_argument("--dataflow", default="pool_then_dense",
+                    choices=["pool_then_dense", "dense_then_pool"],
+                    help="layer evaluation order (same values; see pinsage_dataflow_t)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
@@ -339,7 +350,7 @@ def main() -> int:
     wl = synth.WORKLOADS[args.workload]
     args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[wl.name]
     args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[wl.name]
-    inp = load_inputs(wl)
+    inp = load_inputs(wl, args.dataflow)
     if wl.name == "minibatch":
         value, unit, metric, elapsed, kernels, extra = bench_minibatch(args, wl, inp)
     else:
@@ -361,7 +372,8 @@ def main() -> int:
         "config": {"workload": f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
                                f"{inp['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
                                f"T={wl.T}, K={wl.K}, dims {wl.d_in}->{wl.m}->{wl.d_out} "
-                               f"{wl.dtype}",
+                               f"{wl.dtype}, layer dataflow {args.dataflow}",
+                   "dataflow": args.dataflow,
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
         "walk_steps_per_s": extra["walk_steps_per_s"],

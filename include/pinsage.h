@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 1
+#define PINSAGE_ABI_VERSION 2
 
 enum {
   PINSAGE_OK = 0,
@@ -94,6 +94,19 @@ typedef struct {
   float* weights;
 } pinsage_neighborhoods_t;
 
+/* Order in which a layer evaluates Algorithm 1 (both give the same values in
+ * exact arithmetic; they differ only in rounding):
+ *   POOL_THEN_DENSE  Algorithm 1 as written: P = ReLU(Q h + q) for every pin,
+ *                    n_u = weighted mean of P over N(u) (m-wide rows),
+ *                    z_u = ReLU(W [h_u ; n_u] + w).
+ *   DENSE_THEN_POOL  the neighbour half of W is applied before the pool, as
+ *                    the weighted mean is linear: with W = [W_s | W_n],
+ *                    R = P W_n^T for every pin (d_out-wide rows),
+ *                    g_u = weighted mean of R over N(u),
+ *                    z_u = ReLU(W_s h_u + g_u + w).
+ *                    The gather reads d_out instead of m values per neighbour. */
+typedef enum { PINSAGE_POOL_THEN_DENSE = 0, PINSAGE_DENSE_THEN_POOL = 1 } pinsage_dataflow_t;
+
 /* One CONVOLVE layer's parameters (Algorithm 1; Sec. 3.2 "Stacking
  * convolutions": shared by all nodes, distinct per layer).
  *   Q device [m][d_in]            (storage dtype)
@@ -102,6 +115,7 @@ typedef struct {
  *                                 the node's own vector, [d_in, d_in + m) the
  *                                 pooled neighbourhood vector
  *   w device fp32 [d_out]
+ *   dataflow                      evaluation order (above)
  * Limits: d_in, m, d_out multiples of 16; d_in, m <= 8192; d_out <= 512. */
 typedef struct {
   int32_t d_in;
@@ -112,6 +126,7 @@ typedef struct {
   const float* q;
   const void* W;
   const float* w;
+  pinsage_dataflow_t dataflow;
 } pinsage_layer_t;
 
 /* Version of this ABI (PINSAGE_ABI_VERSION). */
@@ -144,6 +159,8 @@ int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_tran
  *   n[r]  = sum_t weights[r][t] * P[idx[r][t]] (rank order; padding skipped)
  *   z[r]  = ReLU(W concat(h_in[s(r)], n[r]) + w),  s(r) = self_rows[r] or r
  *   h_out[r] = z[r] / ||z[r]||_2 (a zero z stays zero)   for r in [0, n_out)
+ * (with DENSE_THEN_POOL, n[r] is never formed: the pool runs over rows of
+ * P W_n^T, see pinsage_dataflow_t).
  * h_in: device [n_in][d_in]; h_out: device [n_out][d_out]; both in the
  * layer's storage dtype. nbr->rows must equal n_out; neighbour ids index the
  * projected rows, i.e. lie in [0, n_transform) (others are skipped).
@@ -239,7 +256,8 @@ enum {
   PINSAGE_KERNEL_GEMM_W = 3,
   PINSAGE_KERNEL_MINIBATCH = 4,
   PINSAGE_KERNEL_LOSS = 5,
-  PINSAGE_KERNEL_COUNT = 6
+  PINSAGE_KERNEL_GEMM_R = 6, /* neighbour half of W per pin (DENSE_THEN_POOL) */
+  PINSAGE_KERNEL_COUNT = 7
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

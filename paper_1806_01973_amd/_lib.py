@@ -16,9 +16,12 @@ PINSAGE_EHIP = -4
 
 PINSAGE_I32, PINSAGE_I64 = 0, 1
 PINSAGE_F32, PINSAGE_BF16 = 0, 1
+PINSAGE_POOL_THEN_DENSE, PINSAGE_DENSE_THEN_POOL = 0, 1
+DATAFLOWS = {"pool_then_dense": PINSAGE_POOL_THEN_DENSE, "dense_then_pool": PINSAGE_DENSE_THEN_POOL}
 
-KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS = range(6)
-KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss"]
+(KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
+ KERNEL_GEMM_R) = range(7)
+KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
@@ -49,7 +52,7 @@ class Neighborhoods(ctypes.Structure):
 class Layer(ctypes.Structure):
     _fields_ = [("d_in", ctypes.c_int32), ("m", ctypes.c_int32), ("d_out", ctypes.c_int32),
                 ("dtype", ctypes.c_int), ("Q", ctypes.c_void_p), ("q", ctypes.c_void_p),
-                ("W", ctypes.c_void_p), ("w", ctypes.c_void_p)]
+                ("W", ctypes.c_void_p), ("w", ctypes.c_void_p), ("dataflow", ctypes.c_int)]
 
 
 class Pairs(ctypes.Structure):

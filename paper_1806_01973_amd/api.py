@@ -102,9 +102,18 @@ class Neighborhoods:
 
 class DeviceLayer:
     """One CONVOLVE layer's parameters on the GPU: Q [m, d_in], q [m] fp32,
-    W [d_out, d_in + m], w [d_out] fp32; Q and W in the storage dtype."""
+    W [d_out, d_in + m], w [d_out] fp32; Q and W in the storage dtype.
 
-    def __init__(self, Q, q, W, w, dtype: torch.dtype = torch.float32, device="cuda"):
+    dataflow: "pool_then_dense" (Algorithm 1 as written: pool m-wide
+    transformed rows, then W) or "dense_then_pool" (the neighbour half of W is
+    applied per pin first, so the pool gathers d_out-wide rows); both compute
+    the same layer."""
+
+    def __init__(self, Q, q, W, w, dtype: torch.dtype = torch.float32, device="cuda",
+                 dataflow: str = "pool_then_dense"):
+        if dataflow not in L.DATAFLOWS:
+            raise ValueError(f"dataflow must be one of {sorted(L.DATAFLOWS)}, got {dataflow!r}")
+        self.dataflow = dataflow
         self.dtype = dtype
         self.Q = torch.as_tensor(Q).to(device=device, dtype=dtype).contiguous()
         self.W = torch.as_tensor(W).to(device=device, dtype=dtype).contiguous()
@@ -117,7 +126,8 @@ class DeviceLayer:
 
     def struct(self) -> L.Layer:
         return L.Layer(self.d_in, self.m, self.d_out, _dtype_code(self.dtype), self.Q.data_ptr(),
-                       self.q.data_ptr(), self.W.data_ptr(), self.w.data_ptr())
+                       self.q.data_ptr(), self.W.data_ptr(), self.w.data_ptr(),
+                       L.DATAFLOWS[self.dataflow])
 
 
 def build_neighborhoods(graph: DeviceGraph, walks: int, hops: int, T: int, seed: int,

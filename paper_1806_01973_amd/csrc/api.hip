@@ -100,6 +100,8 @@ int check_layer(const pinsage_layer_t* L, int k) {
                 k);
   if (!L->Q || !L->q || !L->W || !L->w)
     return fail(PINSAGE_EINVAL, "layer %d: a parameter pointer is NULL", k);
+  if (L->dataflow != PINSAGE_POOL_THEN_DENSE && L->dataflow != PINSAGE_DENSE_THEN_POOL)
+    return fail(PINSAGE_EINVAL, "layer %d: unknown dataflow %d", k, (int)L->dataflow);
   return PINSAGE_OK;
 }
 
@@ -115,48 +117,111 @@ int check_nbr(const pinsage_neighborhoods_t* n, int64_t rows, const char* what) 
   return PINSAGE_OK;
 }
 
-size_t convolve_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
+// Workspace of one layer.
+//   POOL_THEN_DENSE: P [n_transform][m] | pooled chunk [<= kChunkRows][m]
+//   DENSE_THEN_POOL: R [n_transform][d_out] | P chunk [<= kChunkRows][m] |
+//                    pooled chunk [<= kChunkRows][d_out]
+struct LayerWs {
+  size_t table = 0, pchunk = 0, pooled = 0;
+  size_t total() const { return table + pchunk + pooled; }
+};
+
+LayerWs layer_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
   const size_t es = elem_size(L->dtype);
-  const int64_t chunk = n_out < kChunkRows ? n_out : kChunkRows;
-  return align_up((size_t)n_transform * L->m * es) + align_up((size_t)chunk * L->m * es);
+  const int64_t out_chunk = n_out < kChunkRows ? n_out : kChunkRows;
+  const int64_t tr_chunk = n_transform < kChunkRows ? n_transform : kChunkRows;
+  LayerWs w;
+  if (L->dataflow == PINSAGE_DENSE_THEN_POOL) {
+    w.table = align_up((size_t)n_transform * L->d_out * es);
+    w.pchunk = align_up((size_t)tr_chunk * L->m * es);
+    w.pooled = align_up((size_t)out_chunk * L->d_out * es);
+  } else {
+    w.table = align_up((size_t)n_transform * L->m * es);
+    w.pooled = align_up((size_t)out_chunk * L->m * es);
+  }
+  return w;
 }
 
-// Layer body shared by convolve_layer and embed_all; arguments already valid.
+size_t convolve_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
+  return layer_ws(L, n_transform, n_out).total();
+}
+
+// Algorithm 1 line 1 for rows [c0, c0 + rows) of the transformed set:
+// C = ReLU(h_in[t(i)] Q^T + q).
+hipError_t launch_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
+                            const int32_t* transform_rows, int64_t c0, int64_t rows, void* C,
+                            hipStream_t s) {
+  const size_t es = elem_size(L->dtype);
+  GemmLaunch g{};
+  if (transform_rows) {
+    g.A0 = h_in;
+    g.rowmap = transform_rows + c0;
+    g.rows_a0 = n_in;
+  } else {
+    g.A0 = static_cast<const unsigned char*>(h_in) + (size_t)c0 * L->d_in * es;
+    g.rows_a0 = n_in - c0;
+  }
+  g.lda0 = L->d_in;
+  g.K0 = L->d_in;
+  g.B = L->Q;
+  g.bias = L->q;
+  g.M = rows;
+  g.N = L->m;
+  g.C = C;
+  g.bf16 = L->dtype == PINSAGE_BF16;
+  g.relu = true;
+  return launch_gemm(g, s);
+}
+
+// Layer body shared by convolve_layer, embed_all and the minibatch forward;
+// arguments already valid.
 int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
               const int32_t* transform_rows, const pinsage_neighborhoods_t* nbr,
               const int32_t* self_rows, void* h_out, int64_t n_out, void* ws, hipStream_t s) {
   const bool bf16 = L->dtype == PINSAGE_BF16;
+  const bool split = L->dataflow == PINSAGE_DENSE_THEN_POOL;
   const size_t es = elem_size(L->dtype);
-  unsigned char* P = static_cast<unsigned char*>(ws);
-  unsigned char* nbuf = P + align_up((size_t)n_transform * L->m * es);
+  const LayerWs lw = layer_ws(L, n_transform, n_out);
+  unsigned char* table = static_cast<unsigned char*>(ws);  // P, or R when split
+  unsigned char* pchunk = table + lw.table;
+  unsigned char* nbuf = pchunk + lw.pchunk;
+  const int pool_width = split ? L->d_out : L->m;
+  hipError_t e;
 
-  // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
-  GemmLaunch gq{};
-  gq.A0 = h_in;
-  gq.rowmap = transform_rows;
-  gq.rows_a0 = n_in;
-  gq.lda0 = L->d_in;
-  gq.K0 = L->d_in;
-  gq.A1 = nullptr;
-  gq.lda1 = 0;
-  gq.K1 = 0;
-  gq.B = L->Q;
-  gq.bias = L->q;
-  gq.M = n_transform;
-  gq.N = L->m;
-  gq.C = P;
-  gq.bf16 = bf16;
-  gq.l2norm = false;
-  hipError_t e = launch_gemm(gq, s);
-  if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+  if (!split) {
+    // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
+    e = launch_transform(L, h_in, n_in, transform_rows, 0, n_transform, table, s);
+    if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+  } else {
+    // Per chunk of pins: P = ReLU(h Q^T + q), then R = P W_n^T with W_n the
+    // neighbour columns [d_in, d_in + m) of W (row stride d_in + m).
+    for (int64_t c0 = 0; c0 < n_transform; c0 += kChunkRows) {
+      const int64_t rows = (n_transform - c0) < kChunkRows ? (n_transform - c0) : kChunkRows;
+      e = launch_transform(L, h_in, n_in, transform_rows, c0, rows, pchunk, s);
+      if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+      GemmLaunch gr{};
+      gr.A0 = pchunk;
+      gr.rows_a0 = rows;
+      gr.lda0 = L->m;
+      gr.K0 = L->m;
+      gr.B = static_cast<const unsigned char*>(L->W) + (size_t)L->d_in * es;
+      gr.ldb = (int64_t)L->d_in + L->m;
+      gr.M = rows;
+      gr.N = L->d_out;
+      gr.C = table + (size_t)c0 * L->d_out * es;
+      gr.bf16 = bf16;
+      e = launch_gemm(gr, s);
+      if (e != hipSuccess) return hip_fail(e, "neighbour-half W launch");
+    }
+  }
 
   for (int64_t r0 = 0; r0 < n_out; r0 += kChunkRows) {
     const int64_t rows = (n_out - r0) < kChunkRows ? (n_out - r0) : kChunkRows;
     const int T = nbr->top_t;
     PoolLaunch pl{};
-    pl.P = P;
+    pl.P = table;
     pl.n_transform = n_transform;
-    pl.m = L->m;
+    pl.m = pool_width;
     pl.bf16 = bf16;
     pl.idx = nbr->idx + r0 * T;
     pl.counts = nbr->counts + r0 * T;
@@ -167,7 +232,8 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
     e = launch_pool(pl, s);
     if (e != hipSuccess) return hip_fail(e, "pool launch");
 
-    // Algorithm 1 lines 2-3 on [h_self | n].
+    // Algorithm 1 lines 2-3: on [h_self | n] with all of W, or (split) on
+    // h_self with the self columns of W plus the pooled R rows.
     GemmLaunch gw{};
     if (self_rows) {
       gw.A0 = h_in;
@@ -179,15 +245,21 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
     gw.rows_a0 = self_rows ? n_in : (n_in - r0);
     gw.lda0 = L->d_in;
     gw.K0 = L->d_in;
-    gw.A1 = nbuf;
-    gw.lda1 = L->m;
-    gw.K1 = L->m;
+    if (split) {
+      gw.ldb = (int64_t)L->d_in + L->m;
+      gw.addend = nbuf;
+    } else {
+      gw.A1 = nbuf;
+      gw.lda1 = L->m;
+      gw.K1 = L->m;
+    }
     gw.B = L->W;
     gw.bias = L->w;
     gw.M = rows;
     gw.N = L->d_out;
     gw.C = static_cast<unsigned char*>(h_out) + (size_t)r0 * L->d_out * es;
     gw.bf16 = bf16;
+    gw.relu = true;
     gw.l2norm = true;
     e = launch_gemm(gw, s);
     if (e != hipSuccess) return hip_fail(e, "W transform launch");

@@ -3,7 +3,8 @@
 //   lines 2-3:  h' = normalize(ReLU([h_self | n] W^T + w))
 // as one templated MFMA GEMM  C = epi(A B^T + bias), A [M x K] assembled from
 // two row sources (self rows through an optional row map, then the pooled
-// rows), B [N x K] row-major (the PyTorch Linear layout of Q and W).
+// rows), B [N x K] with a row stride (the PyTorch Linear layout of Q and W,
+// or a column block of W).
 //
 // Work split: a block of WAVES_M x WAVES_N waves owns a BM x BN output tile;
 // each wave owns (BM/WAVES_M) x (BN/WAVES_N), i.e. TM x TN blocks of 32 x 32.
@@ -27,7 +28,9 @@
 // and runs of 4 adjacent output columns, stored as one 8-byte (bf16) or
 // 16-byte (fp32) vector.
 //
-// Epilogue: + bias, ReLU, store in the storage dtype; with L2 the block spans
+// Epilogue: + bias, + an optional addend matrix (the pooled neighbour term
+// when W is split, see run_layer), ReLU (optional without L2), store in the
+// storage dtype; with L2 the block spans
 // all N columns, and a row's sum of squares is added over the lane's own
 // columns, its partner half-wave and then the waves of the row band in a fixed
 // order through LDS; every row is scaled by 1/||z|| (zero rows stay zero).
@@ -134,7 +137,9 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   const int n0 = (tile % tiles_n) * BN;
   const int K = a.K0 + a.K1;
   // Bias slice of the block (zero past N).
-  for (int c = tid; c < BN; c += THREADS) bias_s[c] = n0 + c < a.N ? a.bias[n0 + c] : 0.0f;
+  for (int c = tid; c < BN; c += THREADS)
+    bias_s[c] = (a.bias && n0 + c < a.N) ? a.bias[n0 + c] : 0.0f;
+  const int64_t ldb = a.ldb ? a.ldb : K;
 
   // ---- DMA slots (fixed across the K loop) --------------------------------
   // Slot d of this wave fills group wave*DPW + d of every stage: A groups
@@ -158,13 +163,14 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
                   ? static_cast<const unsigned char*>(a.A0) + src * a.lda0 * ESZ
                   : zrow;
       if constexpr (C::kTwoSources) {
-        const unsigned char* q =
-            in_m ? static_cast<const unsigned char*>(a.A1) + gr * a.lda1 * ESZ : zrow;
+        const unsigned char* q = (in_m && a.A1)
+                                     ? static_cast<const unsigned char*>(a.A1) + gr * a.lda1 * ESZ
+                                     : zrow;
         p1[d] = reinterpret_cast<const unsigned char*>(reinterpret_cast<uintptr_t>(q) - k0b);
       }
     } else {
       const int r = n0 + (grp - C::A_GROUPS) * 16 + rr;
-      p0[d] = r < a.N ? static_cast<const unsigned char*>(a.B) + (int64_t)r * K * ESZ : zrow;
+      p0[d] = r < a.N ? static_cast<const unsigned char*>(a.B) + (int64_t)r * ldb * ESZ : zrow;
       if constexpr (C::kTwoSources) p1[d] = p0[d];
     }
   }
@@ -307,16 +313,38 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   // columns past N have zero weights and zero bias, so they stay zero.
   // Row bands are finished one at a time to keep few accumulators live.
   auto c0 = [&](int j, int g) __attribute__((always_inline)) { return b_base_row + j * 32 + 8 * g + 4 * half; };
+  // + bias (+ addend), then ReLU unless disabled; the L2 epilogue always
+  // follows a ReLU.
+  const bool relu = a.relu || C::L2;
   auto bias_relu = [&](int i) __attribute__((always_inline)) {
+    const int64_t r = m0 + a_base_row + i * 32 + row_in_blk;
+    const bool add = a.addend != nullptr && r < a.M;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const float4 bv = *reinterpret_cast<const float4*>(bias_s + c0(j, g));
-        acc[i][j][4 * g + 0] = fmaxf(acc[i][j][4 * g + 0] + bv.x, 0.0f);
-        acc[i][j][4 * g + 1] = fmaxf(acc[i][j][4 * g + 1] + bv.y, 0.0f);
-        acc[i][j][4 * g + 2] = fmaxf(acc[i][j][4 * g + 2] + bv.z, 0.0f);
-        acc[i][j][4 * g + 3] = fmaxf(acc[i][j][4 * g + 3] + bv.w, 0.0f);
+        float x[4] = {acc[i][j][4 * g + 0] + bv.x, acc[i][j][4 * g + 1] + bv.y,
+                      acc[i][j][4 * g + 2] + bv.z, acc[i][j][4 * g + 3] + bv.w};
+        const int c = n0 + c0(j, g);
+        if (add && c < a.N) {
+          const int64_t o = r * a.N + c;
+          if constexpr (C::kBf16) {
+            const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.addend) + o);
+            x[0] += __uint_as_float(v.x << 16);
+            x[1] += __uint_as_float(v.x & 0xFFFF0000u);
+            x[2] += __uint_as_float(v.y << 16);
+            x[3] += __uint_as_float(v.y & 0xFFFF0000u);
+          } else {
+            const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(a.addend) + o);
+            x[0] += v.x;
+            x[1] += v.y;
+            x[2] += v.z;
+            x[3] += v.w;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][4 * g + e] = relu ? fmaxf(x[e], 0.0f) : x[e];
       }
   };
   auto store_band = [&](int i, float scale) __attribute__((always_inline)) {
@@ -404,7 +432,7 @@ hipError_t launch_cfg(const GemmLaunch& a, hipStream_t s) {
 
 template <bool BF16>
 hipError_t launch_typed(const GemmLaunch& a, hipStream_t s) {
-  if (!a.l2norm) {
+  if (!a.l2norm) {  // Q transform and the neighbour half of W share the tiles
     if constexpr (BF16) return launch_cfg<PINSAGE_CFG_Q_BF16>(a, s);
     else return launch_cfg<PINSAGE_CFG_Q_F32>(a, s);
   }
@@ -426,7 +454,7 @@ hipError_t launch_typed(const GemmLaunch& a, hipStream_t s) {
 
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  ProfileScope prof(a.l2norm ? kKGemmW : kKGemmQ, s);
+  ProfileScope prof(a.l2norm ? kKGemmW : (a.relu ? kKGemmQ : kKGemmR), s);
   return a.bf16 ? launch_typed<true>(a, s) : launch_typed<false>(a, s);
 }
 

@@ -9,7 +9,7 @@ namespace pinsage {
 
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
-                   kKCount = 6 };
+                   kKGemmR = 6, kKCount = 7 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -58,10 +58,12 @@ struct PoolLaunch {
 };
 hipError_t launch_pool(const PoolLaunch& a, hipStream_t s);
 
-// C[r][c] = epilogue(sum_k A[r][k] * B[c][k] + bias[c]) where the A row is the
-// concatenation of A0[rowmap ? rowmap[r] : r][0:K0] and A1[r][0:K1]. B is
-// [N][K0 + K1] row-major. Epilogue: ReLU, optionally followed by row L2
-// normalisation over all N columns.
+// C[r][c] = epilogue(sum_k A[r][k] * B[c][k] + bias[c] + addend[r][c]) where
+// the A row is the concatenation of A0[rowmap ? rowmap[r] : r][0:K0] and
+// A1[r][0:K1]. B is [N][K0 + K1] with row stride ldb. Epilogue: optional
+// ReLU, optionally followed by row L2 normalisation over all N columns (which
+// implies ReLU). Profiled as the Q class (ReLU, no norm), the W class (norm)
+// or the R class (neither).
 struct GemmLaunch {
   const void* A0;
   const int32_t* rowmap;  // nullable; entries outside [0, rows_a0) read as zero rows
@@ -72,11 +74,14 @@ struct GemmLaunch {
   int64_t lda1;
   int K1;
   const void* B;
-  const float* bias;
+  int64_t ldb;        // elements between B rows; 0 means K0 + K1
+  const float* bias;  // nullable: no bias
+  const void* addend; // nullable; [M][N] in the storage dtype
   int64_t M;
   int N;
   void* C;
   bool bf16;
+  bool relu;
   bool l2norm;
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);

@@ -130,43 +130,130 @@ __device__ __forceinline__ float load_elem(const void* base, int64_t i) {
   else return static_cast<const float*>(base)[i];
 }
 
-// Eq. (1) per pair: one wavefront per query b; each lane keeps d/64 entries
-// of z_q in registers; dot products are wave sums in a fixed butterfly order,
-// and the hinge terms are added in negative order.
-template <bool BF16, int PER_LANE>
-__global__ __launch_bounds__(256) void loss_pairs_kernel(LossLaunch a) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int d = a.d;
-  for (int64_t b = (int64_t)blockIdx.x * 4 + wave; b < a.B; b += (int64_t)gridDim.x * 4) {
-    const int64_t qr = a.q_rows ? (int64_t)a.q_rows[b] : b;
-    const int64_t pr = a.pos_rows ? (int64_t)a.pos_rows[b] : b;
-    float zq[PER_LANE];
-    float dp = 0.0f;
-#pragma unroll
-    for (int i = 0; i < PER_LANE; ++i) {
-      const int j = lane + 64 * i;
-      zq[i] = (j < d && qr >= 0) ? load_elem<BF16>(a.zq, qr * d + j) : 0.0f;
-      const float zp = (j < d && pr >= 0) ? load_elem<BF16>(a.zpos, pr * d + j) : 0.0f;
-      dp = fmaf(zq[i], zp, dp);
-    }
-    const float pos = wave_sum_f32(dp);
-    float acc = 0.0f;
-    for (int64_t n = 0; n < a.n_neg; ++n) {
-      const int64_t nr = a.neg_rows ? (int64_t)a.neg_rows[n] : n;
-      float dn = 0.0f;
-#pragma unroll
-      for (int i = 0; i < PER_LANE; ++i) {
-        const int j = lane + 64 * i;
-        const float zn = (j < d && nr >= 0) ? load_elem<BF16>(a.zneg, nr * d + j) : 0.0f;
-        dn = fmaf(zq[i], zn, dn);
-      }
-      const float neg = wave_sum_f32(dn);
-      const float h = neg - pos + a.margin;
-      acc += h > 0.0f ? h : 0.0f;
-    }
-    if (lane == 0) a.per_pair[b] = acc / (float)a.n_neg;
+// Copies one d-wide row of a table (row id `row`, -1 = zero row) into LDS
+// as fp32; TPR threads share the row, thread c of them taking 16-byte vectors
+// c, c + TPR, ... (eight loads in flight before their stores). Rows whose
+// width is not a whole number of vectors go element by element.
+template <bool BF16, int TPR>
+__device__ __forceinline__ void stage_row(float* dst, const void* table, int64_t row, int d,
+                                          int c) {
+  constexpr int VE = BF16 ? 8 : 4;  // elements per 16-byte vector
+  constexpr int U = 8;
+  if (row < 0) {
+    for (int k = c; k < d; k += TPR) dst[k] = 0.0f;
+    return;
   }
+  if (d % VE) {
+    for (int k = c; k < d; k += TPR) dst[k] = load_elem<BF16>(table, row * d + k);
+    return;
+  }
+  const uint4* src = reinterpret_cast<const uint4*>(
+      static_cast<const unsigned char*>(table) + (size_t)row * d * (BF16 ? 2 : 4));
+  const int nv = d / VE;
+  for (int v0 = c; v0 < nv; v0 += TPR * U) {
+    uint4 buf[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + TPR * u;
+      buf[u] = v < nv ? src[v] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + TPR * u;
+      if (v >= nv) break;
+      const uint32_t w[4] = {buf[u].x, buf[u].y, buf[u].z, buf[u].w};
+      float* o = dst + v * VE;
+      if constexpr (BF16) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          o[2 * i] = __uint_as_float(w[i] << 16);
+          o[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = __uint_as_float(w[i]);
+      }
+    }
+  }
+}
+
+// Eq. (1) per pair. A block of THREADS threads scores QB queries against the
+// negatives, NC at a time: the query rows and the chunk's negative rows sit
+// in LDS as fp32 with an odd row stride (rows read by one instruction fall in
+// distinct banks). The TPQ = THREADS / QB threads of query q take negatives
+// c, c + TPQ, ... of the chunk (NP each) and form each dot product over d in
+// index order, so one broadcast read of z_q serves NP products. A thread adds
+// its hinge terms in order, the TPQ threads of a query are summed by a fixed
+// butterfly, and chunk sums are added in chunk order. The positive score is a
+// partial dot per thread (indices c, c + TPQ, ...) summed by the same
+// butterfly.
+template <bool BF16, int THREADS, int QB, int NC, int DMAX>
+__global__ __launch_bounds__(THREADS) void loss_pairs_kernel(LossLaunch a) {
+  constexpr int TPQ = THREADS / QB;
+  constexpr int NP = NC / TPQ;
+  static_assert(TPQ <= 64 && NP * TPQ == NC && THREADS % NC == 0, "pair layout");
+  constexpr int S_MAX = DMAX + 1;
+  __shared__ float zq_s[QB * S_MAX];
+  __shared__ float zn_s[NC * S_MAX];
+  const int d = a.d;
+  const int S = d | 1;  // odd row stride >= d
+  const int t = threadIdx.x;
+  const int q = t / TPQ, c = t % TPQ;
+  const int64_t b0 = (int64_t)blockIdx.x * QB;
+  const int64_t b = b0 + q;
+
+  // Query rows of the block (zero rows for missing pairs or ids).
+  {
+    int64_t row = -1;
+    if (b < a.B) row = a.q_rows ? (int64_t)a.q_rows[b] : b;
+    stage_row<BF16, TPQ>(zq_s + q * S, a.zq, row, d, c);
+  }
+  __syncthreads();
+  // Positive score of query q.
+  float dp = 0.0f;
+  {
+    int64_t pr = -1;
+    if (b < a.B) pr = a.pos_rows ? (int64_t)a.pos_rows[b] : b;
+    if (pr >= 0)
+      for (int k = c; k < d; k += TPQ)
+        dp = fmaf(zq_s[q * S + k], load_elem<BF16>(a.zpos, pr * d + k), dp);
+  }
+#pragma unroll
+  for (int o = TPQ / 2; o >= 1; o >>= 1) dp += __shfl_xor(dp, o);
+  const float pos = dp;
+
+  constexpr int TPR = THREADS / NC;  // threads per staged negative row
+  float acc = 0.0f;
+  for (int64_t c0 = 0; c0 < a.n_neg; c0 += NC) {
+    __syncthreads();  // previous chunk fully read
+    {
+      const int r = t / TPR;
+      const int64_t nn = c0 + r;
+      int64_t row = -1;
+      if (nn < a.n_neg) row = a.neg_rows ? (int64_t)a.neg_rows[nn] : nn;
+      stage_row<BF16, TPR>(zn_s + r * S, a.zneg, row, d, t % TPR);
+    }
+    __syncthreads();
+    const float* zq = zq_s + q * S;
+    float dn[NP];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) dn[j] = 0.0f;
+    for (int k = 0; k < d; ++k) {
+      const float x = zq[k];
+#pragma unroll
+      for (int j = 0; j < NP; ++j) dn[j] = fmaf(x, zn_s[(c + TPQ * j) * S + k], dn[j]);
+    }
+    float hc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      const float h = dn[j] - pos + a.margin;
+      hc += (c0 + c + TPQ * j < a.n_neg && h > 0.0f) ? h : 0.0f;
+    }
+#pragma unroll
+    for (int o = TPQ / 2; o >= 1; o >>= 1) hc += __shfl_xor(hc, o);
+    acc += hc;
+  }
+  if (c == 0 && b < a.B) a.per_pair[b] = acc / (float)a.n_neg;
 }
 
 // Mean over pairs in a fixed order: strided per-thread sums, then a fixed tree.
@@ -261,23 +348,22 @@ hipError_t launch_gather_rows(const void* table, const int32_t* rows, int64_t n,
   return hipGetLastError();
 }
 
+template <int THREADS, int QB, int NC, int DMAX>
+void launch_loss_cfg(const LossLaunch& a, hipStream_t s) {
+  const dim3 grid((unsigned)((a.B + QB - 1) / QB)), block(THREADS);
+  if (a.bf16) hipLaunchKernelGGL((loss_pairs_kernel<true, THREADS, QB, NC, DMAX>), grid, block, 0,
+                                 s, a);
+  else hipLaunchKernelGGL((loss_pairs_kernel<false, THREADS, QB, NC, DMAX>), grid, block, 0, s, a);
+}
+
 hipError_t launch_loss(const LossLaunch& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;
+  if (a.d < 1 || a.d > 1024 || a.B >= (1ll << 32)) return hipErrorInvalidValue;
   ProfileScope prof(kKLoss, s);
-  const int per_lane = (a.d + 63) / 64;
-  int64_t blocks = (a.B + 3) / 4;
-  if (blocks > 65536) blocks = 65536;
-  const dim3 grid((unsigned)blocks), block(256);
-#define PINSAGE_LOSS(PL)                                                                    \
-  if (a.bf16) hipLaunchKernelGGL((loss_pairs_kernel<true, PL>), grid, block, 0, s, a);      \
-  else hipLaunchKernelGGL((loss_pairs_kernel<false, PL>), grid, block, 0, s, a);
-  if (per_lane <= 1) { PINSAGE_LOSS(1) }
-  else if (per_lane <= 2) { PINSAGE_LOSS(2) }
-  else if (per_lane <= 4) { PINSAGE_LOSS(4) }
-  else if (per_lane <= 8) { PINSAGE_LOSS(8) }
-  else if (per_lane <= 16) { PINSAGE_LOSS(16) }
-  else return hipErrorInvalidValue;
-#undef PINSAGE_LOSS
+  // LDS per block: (QB + NC) * (DMAX + 1) * 4 bytes <= 148 KB.
+  if (a.d <= 256) launch_loss_cfg<256, 8, 128, 256>(a, s);
+  else if (a.d <= 512) launch_loss_cfg<256, 8, 64, 512>(a, s);
+  else launch_loss_cfg<128, 4, 32, 1024>(a, s);
   hipLaunchKernelGGL(loss_mean_kernel, dim3(1), dim3(256), 0, s, a.per_pair, a.B, a.loss);
   return hipGetLastError();
 }

@@ -69,9 +69,14 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
        row0 += (int64_t)gridDim.x * kWavesPerBlock) {
     const int64_t row = row0;
     const int32_t* __restrict__ ridx = a.idx + row * T;
+    // Without stored weights, alpha = count / (sum of the row's counts): the
+    // lanes load the counts in parallel and the wave adds them (integers, so
+    // the order does not matter).
     int total = 0;
     if (!a.weights) {
-      for (int t = 0; t < T; ++t) total += a.counts[row * T + t];
+      int part = 0;
+      for (int t = lane; t < T; t += kWave) part += a.counts[row * T + t];
+      total = wave_sum_i32(part);
     }
     float acc[J][VN];
 #pragma unroll

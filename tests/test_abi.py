@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 1
+    assert lib.pinsage_version() == 2
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -95,9 +95,13 @@ def test_layer_validation_and_workspace_sizes(L):
     lyb = _layer(L, dtype=L.PINSAGE_BF16)
     assert lib.pinsage_convolve_workspace_size(ctypes.byref(lyb), 100, 300, ctypes.byref(n)) == 0
     assert n.value == 25600 + 76800
+    # Dense then pool: R (100 x 64 fp32) + P chunk (100 x 128) + pooled rows (300 x 64).
+    lyd = _layer(L, dataflow=L.PINSAGE_DENSE_THEN_POOL)
+    assert lib.pinsage_convolve_workspace_size(ctypes.byref(lyd), 100, 300, ctypes.byref(n)) == 0
+    assert n.value == 25600 + 51200 + 76800
     for bad, code in [(dict(d_in=60), L.PINSAGE_EUNSUPPORTED), (dict(d_out=1024), L.PINSAGE_EUNSUPPORTED),
                       (dict(m=0), L.PINSAGE_EINVAL), (dict(Q=None), L.PINSAGE_EINVAL),
-                      (dict(dtype=5), L.PINSAGE_EINVAL)]:
+                      (dict(dtype=5), L.PINSAGE_EINVAL), (dict(dataflow=2), L.PINSAGE_EINVAL)]:
         b = _layer(L, **bad)
         assert lib.pinsage_convolve_workspace_size(ctypes.byref(b), 1, 1, ctypes.byref(n)) == code
     # Workspace too small: rejected before any launch.

@@ -17,17 +17,21 @@ from helpers import check_embeddings, to_f64, torch_dtype
 pytestmark = pytest.mark.gpu
 
 
-def _dev_layers(layers, dtype):
+DATAFLOWS = ["pool_then_dense", "dense_then_pool"]
+
+
+def _dev_layers(layers, dtype, dataflow="pool_then_dense"):
     import paper_1806_01973_amd as ps
-    return [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=torch_dtype(dtype))
+    return [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=torch_dtype(dtype),
+                           dataflow=dataflow)
             for L in layers]
 
 
-def _embed_all_gpu(wl, data):
+def _embed_all_gpu(wl, data, dataflow="pool_then_dense"):
     import paper_1806_01973_amd as ps
     g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards,
                        offsets64=wl.offsets64)
-    layers = _dev_layers(data["layers"], wl.dtype)
+    layers = _dev_layers(data["layers"], wl.dtype, dataflow)
     x = torch.as_tensor(data["x"]).to(device="cuda", dtype=torch_dtype(wl.dtype))
     job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
     out = job.run(x)
@@ -47,28 +51,30 @@ def _scaled(base, pins, boards, **kw):
     _scaled("medium", 20_011, 4_003, dtype="bf16", name="medium-bf16"),
     _scaled("large", 6_007, 1_201, degree_hi=500, name="large-shape-bf16"),
 ], ids=lambda w: w.name)
-def test_embed_all_full(orc, wl):
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_embed_all_full(orc, wl, dataflow):
     print(f"[case] embed_all {wl.name} N={wl.num_nodes} dims={wl.d_in}/{wl.m}/{wl.d_out} "
-          f"{wl.dtype}", flush=True)
+          f"{wl.dtype} {dataflow}", flush=True)
     data = synth.make_workload(wl)
-    job, out = _embed_all_gpu(wl, data)
+    job, out = _embed_all_gpu(wl, data, dataflow)
     idx, cnt, wts, steps = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
                                                    wl.seed, wl.walks, wl.hops, wl.T)
     np.testing.assert_array_equal(job.nbr.idx.cpu().numpy(), idx)
     assert int(job.steps.item()) == steps
     ref = orc.embed_all(data["x"], wl.num_pins, data["layers"], idx, wts)
-    stats = check_embeddings(to_f64(out), ref, wl.dtype, wl.name)
-    print(f"[ok] {wl.name} {stats}", flush=True)
+    stats = check_embeddings(to_f64(out), ref, wl.dtype, f"{wl.name} {dataflow}")
+    print(f"[ok] {wl.name} {dataflow} {stats}", flush=True)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("dims", [(64, 64, 64), (256, 512, 256), (128, 96, 512), (48, 2048, 128)])
-def test_convolve_layer_self_rows(orc, dtype, dims):
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_convolve_layer_self_rows(orc, dtype, dims, dataflow):
     import paper_1806_01973_amd as ps
     d_in, m, d_out = dims
     rng = np.random.default_rng(11)
     n_in, n_transform, n_out, T = 3_001, 2_203, 1_777, 23
-    print(f"[case] convolve_layer {dtype} dims={dims}", flush=True)
+    print(f"[case] convolve_layer {dtype} dims={dims} {dataflow}", flush=True)
     h = rng.standard_normal((n_in, d_in)).astype(np.float32)
     if dtype == "bf16":
         h = synth.bf16_round(h)
@@ -76,7 +82,8 @@ def test_convolve_layer_self_rows(orc, dtype, dims):
     layer = synth.make_layers(wl)[0]
     idx, counts, weights = synth.random_neighborhoods(n_out, n_transform, T, seed=4)
     self_rows = rng.integers(0, n_in, size=n_out).astype(np.int32)
-    dev = ps.DeviceLayer(layer["Q"], layer["q"], layer["W"], layer["w"], dtype=torch_dtype(dtype))
+    dev = ps.DeviceLayer(layer["Q"], layer["q"], layer["W"], layer["w"], dtype=torch_dtype(dtype),
+                         dataflow=dataflow)
     nb = ps.Neighborhoods(torch.as_tensor(idx).cuda(), torch.as_tensor(counts).cuda(),
                           torch.as_tensor(weights).cuda())
     hin = torch.as_tensor(h).to(device="cuda", dtype=torch_dtype(dtype))
@@ -85,17 +92,18 @@ def test_convolve_layer_self_rows(orc, dtype, dims):
     torch.cuda.synchronize()
     ref = orc.convolve_layer(h, n_transform, layer["Q"], layer["q"], layer["W"], layer["w"], idx,
                              weights, self_rows=self_rows)
-    check_embeddings(to_f64(out), ref, dtype, f"convolve {dtype} {dims}")
+    check_embeddings(to_f64(out), ref, dtype, f"convolve {dtype} {dims} {dataflow}")
 
 
-def test_weights_from_counts_match_stored_weights():
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_weights_from_counts_match_stored_weights(dataflow):
     import paper_1806_01973_amd as ps
     wl = synth.WORKLOADS["tiny"]
     data = synth.make_workload(wl)
     g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
-    print("[case] weights from counts", flush=True)
+    print(f"[case] weights from counts {dataflow}", flush=True)
     nb, _ = ps.build_neighborhoods(g, wl.walks, wl.hops, wl.T, wl.seed)
-    layer = _dev_layers(data["layers"], "f32")[0]
+    layer = _dev_layers(data["layers"], "f32", dataflow)[0]
     x = torch.as_tensor(data["x"]).cuda()
     a = ps.convolve_layer(layer, x, wl.num_pins, nb)
     b = ps.convolve_layer(layer, x, wl.num_pins, ps.Neighborhoods(nb.idx, nb.counts, None))
@@ -103,12 +111,13 @@ def test_weights_from_counts_match_stored_weights():
     assert torch.equal(a, b)
 
 
-def test_empty_sizes():
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_empty_sizes(dataflow):
     import paper_1806_01973_amd as ps
     wl = synth.WORKLOADS["tiny"]
-    layer = _dev_layers(synth.make_layers(wl), "f32")[0]
+    layer = _dev_layers(synth.make_layers(wl), "f32", dataflow)[0]
     x = torch.zeros((10, 64), device="cuda")
-    print("[case] empty sizes", flush=True)
+    print(f"[case] empty sizes {dataflow}", flush=True)
     nb = ps.Neighborhoods.empty(0, 5)
     out = ps.convolve_layer(layer, x, 0, nb)
     assert out.shape == (0, 64)
@@ -120,13 +129,14 @@ def test_empty_sizes():
     assert torch.isfinite(out).all()
 
 
-def test_medium_sampled_rows(orc, medium_bundle):
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_medium_sampled_rows(orc, medium_bundle, dataflow):
     # Full 1.2M-node workload in the benchmark's launch configuration; the oracle
     # evaluates sampled rows through Algorithm 2 on its own neighbourhood table.
     b = medium_bundle
     wl, data, idx, wts = b["wl"], b["data"], b["idx"], b["wts"]
-    print(f"[case] medium full N={wl.num_nodes}", flush=True)
-    job, out = _embed_all_gpu(wl, data)
+    print(f"[case] medium full N={wl.num_nodes} {dataflow}", flush=True)
+    job, out = _embed_all_gpu(wl, data, dataflow)
     np.testing.assert_array_equal(job.nbr.idx.cpu().numpy(), idx)
     np.testing.assert_array_equal(job.nbr.weights.cpu().numpy().view(np.uint32),
                                   wts.view(np.uint32))
@@ -136,21 +146,23 @@ def test_medium_sampled_rows(orc, medium_bundle):
                               [0, wl.num_pins - 1, wl.num_nodes - 1]]).astype(np.int32)
     ref = orc.minibatch_embed(targets, data["x"], data["layers"], idx, wts)
     got = to_f64(out[torch.as_tensor(targets).long().cuda()])
-    stats = check_embeddings(got, ref, wl.dtype, "medium sampled")
+    stats = check_embeddings(got, ref, wl.dtype, f"medium sampled {dataflow}")
     norms = torch.linalg.vector_norm(out.float(), dim=1)
     assert torch.all(((norms - 1).abs() < 1e-5) | (norms == 0))
-    print(f"[ok] medium sampled {stats}", flush=True)
+    print(f"[ok] medium sampled {dataflow} {stats}", flush=True)
 
 
-def test_profile_counts_launches():
+@pytest.mark.parametrize("dataflow", DATAFLOWS)
+def test_profile_counts_launches(dataflow):
     import paper_1806_01973_amd as ps
     wl = synth.WORKLOADS["tiny"]
     data = synth.make_workload(wl)
-    print("[case] profile", flush=True)
+    print(f"[case] profile {dataflow}", flush=True)
     ps.profile_enable(True)
-    _embed_all_gpu(wl, data)
+    _embed_all_gpu(wl, data, dataflow)
     prof = ps.profile_read()
     ps.profile_enable(False)
     assert prof["walk_topt"][0] == 1
     assert prof["gemm_q"][0] == 2 and prof["pool"][0] == 2 and prof["gemm_w"][0] == 2
+    assert prof["gemm_r"][0] == (2 if dataflow == "dense_then_pool" else 0)
     assert all(ms >= 0 for _, ms in prof.values())

@@ -26,16 +26,18 @@ def _unit_rows(rng, n, d):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_loss_kernel(orc, dtype):
+@pytest.mark.parametrize("B,n_neg,d", [(333, 77, 200), (2048, 500, 256), (37, 301, 512),
+                                       (19, 45, 1024), (5, 3, 13)])
+def test_loss_kernel(orc, dtype, B, n_neg, d):
     import paper_1806_01973_amd as ps
     rng = np.random.default_rng(3)
-    B, n_neg, d = 333, 77, 200
     zq, zp, zn = _unit_rows(rng, B, d), _unit_rows(rng, B, d), _unit_rows(rng, n_neg, d)
     # Make some pairs hard so the hinge is active for a mix of negatives.
-    zp[:100] = zq[:100] * 0.3 + zp[:100] * 0.7
+    hard = min(100, B // 3)
+    zp[:hard] = zq[:hard] * 0.3 + zp[:hard] * 0.7
     if dtype == "bf16":
         zq, zp, zn = (synth.bf16_round(a) for a in (zq, zp, zn))
-    print(f"[case] loss kernel {dtype}", flush=True)
+    print(f"[case] loss kernel {dtype} B={B} n_neg={n_neg} d={d}", flush=True)
     dev = lambda a: torch.as_tensor(a).to(device="cuda", dtype=torch_dtype(dtype))
     loss, per = ps.max_margin_loss(dev(zq), dev(zp), dev(zn), 0.1)
     torch.cuda.synchronize()
@@ -58,11 +60,12 @@ def _loss_bound(g, o, B, n_neg):
     return float((neg_term + pos_term).mean())
 
 
-def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0):
+def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0, dataflow="pool_then_dense"):
     import paper_1806_01973_amd as ps
     q, p, n = synth.minibatch_pairs(wl, data["offsets"], data["col"], B, n_neg, seed=seed)
     g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
-    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=torch_dtype(wl.dtype))
+    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=torch_dtype(wl.dtype),
+                             dataflow=dataflow)
               for L in data["layers"]]
     x = torch.as_tensor(data["x"]).to(device="cuda", dtype=torch_dtype(wl.dtype))
     mb = ps.Minibatch(g, layers, wl.walks, wl.hops, wl.T, wl.seed, B, n_neg)
@@ -90,16 +93,18 @@ def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0):
     return sizes
 
 
-def test_minibatch_tiny(orc):
+@pytest.mark.parametrize("dataflow", ["pool_then_dense", "dense_then_pool"])
+def test_minibatch_tiny(orc, dataflow):
     wl = synth.WORKLOADS["tiny"]
     data = synth.make_workload(wl)
     idx, cnt, wts, _ = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
                                                wl.seed, wl.walks, wl.hops, wl.T)
-    print("[case] minibatch tiny", flush=True)
-    _run_minibatch(orc, wl, data, idx, wts, B=64, n_neg=20)
+    print(f"[case] minibatch tiny {dataflow}", flush=True)
+    _run_minibatch(orc, wl, data, idx, wts, B=64, n_neg=20, dataflow=dataflow)
 
 
-def test_minibatch_full(orc, medium_bundle):
+@pytest.mark.parametrize("dataflow", ["pool_then_dense", "dense_then_pool"])
+def test_minibatch_full(orc, medium_bundle, dataflow):
     # The minibatch-shaped workload: the 1.2M-node graph, 2,048 query pins with
     # one positive each and 500 shared negatives, bf16, dims 256 -> 512 -> 256.
     wl = synth.WORKLOADS["minibatch"]
@@ -109,6 +114,7 @@ def test_minibatch_full(orc, medium_bundle):
     data = dict(b["data"])
     data["x"] = synth.make_features(wl, data["offsets"], data["col"])
     data["layers"] = synth.make_layers(wl)
-    print("[case] minibatch full (2048 pairs, 500 negatives, bf16)", flush=True)
-    sizes = _run_minibatch(orc, wl, data, b["idx"], b["wts"], B=2048, n_neg=500)
+    print(f"[case] minibatch full (2048 pairs, 500 negatives, bf16) {dataflow}", flush=True)
+    sizes = _run_minibatch(orc, wl, data, b["idx"], b["wts"], B=2048, n_neg=500,
+                           dataflow=dataflow)
     assert sizes[2] <= 2 * 2048 + 500 and sizes[1] > sizes[2] and sizes[0] > sizes[1]
