@@ -4,7 +4,10 @@ Default (the headline line): all-node embedding of the 1.2M-node pin-board
 workload (1M pins, 200k boards, fp32, dims 256 -> 512 -> 256, 100 walks x 3
 hops, T = 50). One step = importance neighbourhoods of every node, then K = 2
 CONVOLVE layers over every node, layer by layer. Inputs are resident in HBM
-before timing starts.
+before timing starts. The layers run in the dense-then-pool order (the
+neighbour half of W applied per pin before the weighted mean, which is
+linear); the line also carries the time of Algorithm 1's printed order on the
+same inputs (`alt_dataflow`), and both orders are parity-tested.
 
 Other workloads (measurement of the other rows; not the headline):
   --workload tiny | large | shard   all-node embedding of that graph
@@ -258,7 +261,26 @@ def bench_embed_all(args, wl, inp):
     value = N * args.steps / elapsed
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
              "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps}}
+    if compare_dataflow(args, wl):
+        # The other evaluation order of the same layers, timed the same way
+        # (same inputs, same steps), for comparison only.
+        other = "pool_then_dense" if args.dataflow == "dense_then_pool" else "dense_then_pool"
+        alt_layers = [ps.DeviceLayer(L.Q, L.q, L.W, L.w, dtype=L.dtype, dataflow=other)
+                      for L in inp["layers"]]
+        del job
+        torch.cuda.empty_cache()
+        alt = ps.EmbedAll(inp["g"], alt_layers, wl.walks, wl.hops, wl.T, wl.seed,
+                          weights=wl.name != "shard")
+        alt_elapsed, _ = timed(lambda i: alt.run(inp["x"], stream), args.steps, args.warmup)
+        extra["alt_dataflow"] = {"dataflow": other, "value": N * args.steps / alt_elapsed,
+                                 "ms_per_step": 1e3 * alt_elapsed / args.steps}
     return value, "node embeddings/s", METRIC, elapsed, kernels, extra
+
+
+def compare_dataflow(args, wl) -> bool:
+    if args.compare_dataflow == "auto":
+        return wl.name in ("tiny", "medium")
+    return args.compare_dataflow == "on"
 
 
 def bench_minibatch(args, wl, inp):
@@ -327,9 +349,11 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="medium",
                     choices=["tiny", "medium", "minibatch", "large", "shard"])
-    ap.add_argument("--dataflow", default="pool_then_dense",
+    ap.add_argument("--dataflow", default="dense_then_pool",
                     choices=["pool_then_dense", "dense_then_pool"],
                     help="layer evaluation order (same values; see pinsage_dataflow_t)")
+    ap.add_argument("--compare-dataflow", default="auto", choices=["auto", "on", "off"],
+                    help="also time the other evaluation order (auto: small workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
@@ -377,6 +401,7 @@ def main() -> int:
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
         "walk_steps_per_s": extra["walk_steps_per_s"],
+        "alt_dataflow": extra.get("alt_dataflow"),
         "roofline": roofline_of(kernels, wl),
         "kernels": kernels,
         "cpu_baseline": None,

@@ -173,48 +173,60 @@ hipError_t launch_transform(const pinsage_layer_t* L, const void* h_in, int64_t 
   return launch_gemm(g, s);
 }
 
-// Layer body shared by convolve_layer, embed_all and the minibatch forward;
-// arguments already valid.
-int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
-              const int32_t* transform_rows, const pinsage_neighborhoods_t* nbr,
-              const int32_t* self_rows, void* h_out, int64_t n_out, void* ws, hipStream_t s) {
+// Layer bodies shared by convolve_layer, embed_all and the minibatch forward;
+// arguments already valid. Phase 1 fills the per-pin table of the workspace (P,
+// or R = P W_n^T when split); phase 2 pools it and applies W. Phase 1 reads
+// only h_in, so it may run on another stream than phase 2 of the same layer,
+// ordered by an event.
+int run_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
+                  const int32_t* transform_rows, int64_t n_out, void* ws, hipStream_t s) {
   const bool bf16 = L->dtype == PINSAGE_BF16;
-  const bool split = L->dataflow == PINSAGE_DENSE_THEN_POOL;
   const size_t es = elem_size(L->dtype);
   const LayerWs lw = layer_ws(L, n_transform, n_out);
   unsigned char* table = static_cast<unsigned char*>(ws);  // P, or R when split
   unsigned char* pchunk = table + lw.table;
-  unsigned char* nbuf = pchunk + lw.pchunk;
-  const int pool_width = split ? L->d_out : L->m;
   hipError_t e;
-
-  if (!split) {
+  if (L->dataflow != PINSAGE_DENSE_THEN_POOL) {
     // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
     e = launch_transform(L, h_in, n_in, transform_rows, 0, n_transform, table, s);
     if (e != hipSuccess) return hip_fail(e, "Q transform launch");
-  } else {
-    // Per chunk of pins: P = ReLU(h Q^T + q), then R = P W_n^T with W_n the
-    // neighbour columns [d_in, d_in + m) of W (row stride d_in + m).
-    for (int64_t c0 = 0; c0 < n_transform; c0 += kChunkRows) {
-      const int64_t rows = (n_transform - c0) < kChunkRows ? (n_transform - c0) : kChunkRows;
-      e = launch_transform(L, h_in, n_in, transform_rows, c0, rows, pchunk, s);
-      if (e != hipSuccess) return hip_fail(e, "Q transform launch");
-      GemmLaunch gr{};
-      gr.A0 = pchunk;
-      gr.rows_a0 = rows;
-      gr.lda0 = L->m;
-      gr.K0 = L->m;
-      gr.B = static_cast<const unsigned char*>(L->W) + (size_t)L->d_in * es;
-      gr.ldb = (int64_t)L->d_in + L->m;
-      gr.M = rows;
-      gr.N = L->d_out;
-      gr.C = table + (size_t)c0 * L->d_out * es;
-      gr.bf16 = bf16;
-      e = launch_gemm(gr, s);
-      if (e != hipSuccess) return hip_fail(e, "neighbour-half W launch");
-    }
+    return PINSAGE_OK;
   }
+  // Per chunk of pins: P = ReLU(h Q^T + q), then R = P W_n^T with W_n the
+  // neighbour columns [d_in, d_in + m) of W (row stride d_in + m).
+  for (int64_t c0 = 0; c0 < n_transform; c0 += kChunkRows) {
+    const int64_t rows = (n_transform - c0) < kChunkRows ? (n_transform - c0) : kChunkRows;
+    e = launch_transform(L, h_in, n_in, transform_rows, c0, rows, pchunk, s);
+    if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+    GemmLaunch gr{};
+    gr.A0 = pchunk;
+    gr.rows_a0 = rows;
+    gr.lda0 = L->m;
+    gr.K0 = L->m;
+    gr.B = static_cast<const unsigned char*>(L->W) + (size_t)L->d_in * es;
+    gr.ldb = (int64_t)L->d_in + L->m;
+    gr.M = rows;
+    gr.N = L->d_out;
+    gr.C = table + (size_t)c0 * L->d_out * es;
+    gr.bf16 = bf16;
+    e = launch_gemm(gr, s);
+    if (e != hipSuccess) return hip_fail(e, "neighbour-half W launch");
+  }
+  return PINSAGE_OK;
+}
 
+int run_pool_dense(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
+                   int64_t n_transform, const pinsage_neighborhoods_t* nbr,
+                   const int32_t* self_rows, void* h_out, int64_t n_out, void* ws,
+                   hipStream_t s) {
+  const bool bf16 = L->dtype == PINSAGE_BF16;
+  const bool split = L->dataflow == PINSAGE_DENSE_THEN_POOL;
+  const size_t es = elem_size(L->dtype);
+  const LayerWs lw = layer_ws(L, n_transform, n_out);
+  unsigned char* table = static_cast<unsigned char*>(ws);
+  unsigned char* nbuf = table + lw.table + lw.pchunk;
+  const int pool_width = split ? L->d_out : L->m;
+  hipError_t e;
   for (int64_t r0 = 0; r0 < n_out; r0 += kChunkRows) {
     const int64_t rows = (n_out - r0) < kChunkRows ? (n_out - r0) : kChunkRows;
     const int T = nbr->top_t;
@@ -265,6 +277,51 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
     if (e != hipSuccess) return hip_fail(e, "W transform launch");
   }
   return PINSAGE_OK;
+}
+
+int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
+              const int32_t* transform_rows, const pinsage_neighborhoods_t* nbr,
+              const int32_t* self_rows, void* h_out, int64_t n_out, void* ws, hipStream_t s) {
+  int st = run_transform(L, h_in, n_in, n_transform, transform_rows, n_out, ws, s);
+  if (st) return st;
+  return run_pool_dense(L, h_in, n_in, n_transform, nbr, self_rows, h_out, n_out, ws, s);
+}
+
+// A second stream per device (default priority, non-blocking) for work that
+// overlaps the caller's stream; created on first use and kept for the
+// process. Work on it is ordered against the caller's stream by events only.
+hipError_t side_stream(hipStream_t caller, hipStream_t* out) {
+  static std::mutex mu;
+  static std::vector<hipStream_t> streams;
+  int dev = 0;
+  hipError_t e = caller ? hipStreamGetDevice(caller, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)streams.size() <= dev) streams.resize(dev + 1, nullptr);
+  if (!streams[dev]) {
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess) {
+      streams[dev] = nullptr;
+      return e;
+    }
+  }
+  *out = streams[dev];
+  return hipSuccess;
+}
+
+// Makes `waiter` wait for the work enqueued on `signaller` so far.
+hipError_t stream_wait(hipStream_t waiter, hipStream_t signaller) {
+  hipEvent_t ev;
+  hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(ev, signaller);
+  if (e == hipSuccess) e = hipStreamWaitEvent(waiter, ev, 0);
+  (void)hipEventDestroy(ev);  // released once the recorded work completes
+  return e;
 }
 
 }  // namespace
@@ -447,10 +504,16 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
-  if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
-    return st;
-
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // The first layer's per-pin table (P, or R) depends on x only, so it is
+  // built on a side stream while the walks run on the caller's stream
+  // (memory-latency-bound walks beside MFMA-bound GEMMs); the pool waits for
+  // both.
+  hipStream_t side = nullptr;
+  hipError_t e = side_stream(s, &side);
+  if (e != hipSuccess) return hip_fail(e, "side stream");
+  if ((e = stream_wait(side, s)) != hipSuccess) return hip_fail(e, "stream fork");
+
   size_t conv = 0, h = 0;
   for (int k = 0; k < num_layers; ++k) {
     const size_t c = convolve_ws(&layers[k], graph->num_pins, n);
@@ -462,10 +525,21 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   }
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   unsigned char* hbuf[2] = {ws + conv, ws + conv + h};
+  // The GEMMs go first: each of their blocks takes most of a CU's LDS, and
+  // the walk blocks (small LDS and register footprint) fill in beside them.
+  st = run_transform(&layers[0], x, n, graph->num_pins, nullptr, n, ws, side);
+  if (!st) st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream);
+  // Joined even after a failed launch, so nothing of this call is left
+  // running on the side stream once the caller's stream is done.
+  if ((e = stream_wait(s, side)) != hipSuccess && !st) return hip_fail(e, "stream join");
+  if (st) return st;
   const void* cur = x;
   for (int k = 0; k < num_layers; ++k) {
     void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
-    st = run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n, ws, s);
+    st = k == 0 ? run_pool_dense(&layers[k], cur, n, graph->num_pins, nbr_out, nullptr, dst, n,
+                                 ws, s)
+                : run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n,
+                            ws, s);
     if (st) return st;
     cur = dst;
   }
@@ -594,6 +668,7 @@ int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
     conv = c > conv ? c : conv;
   }
   p->conv = take(conv);
+
   p->total = cur;
   return PINSAGE_OK;
 }

@@ -38,6 +38,8 @@
 // Tile order is XCD-aware: hardware hands block b to XCD b % 8; blocks are
 // renumbered so that each XCD gets a contiguous run of tiles, keeping the
 // column tiles of one row block on one XCD's L2.
+#include <type_traits>
+
 #include "device_util.h"
 #include "kernels.h"
 
@@ -179,7 +181,12 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   // Tiles start their K sweep at different chunks (rotation by tile index):
   // rows of A and B sit at power-of-two strides, and blocks that all read the
   // same K columns at once would pile onto a few L2 channels.
-  const int kshift = tile % nchunks;
+#ifndef PINSAGE_GEMM_KSHIFT
+#define PINSAGE_GEMM_KSHIFT 0
+#endif
+  const int kshift = PINSAGE_GEMM_KSHIFT == 0 ? tile % nchunks
+                     : PINSAGE_GEMM_KSHIFT == 1 ? 0
+                     : (tile / tiles_n) % nchunks;
   // Issues the DMAs of the chunk-th chunk of this tile's sweep into its
   // stage. Sweep positions past the end read the zero row, which keeps the
   // in-flight count uniform for wait_vmcnt.
@@ -401,6 +408,216 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 GEMM with register-staged loads, for one A source without a row map
+// and without the L2 epilogue (the Q transform and the neighbour half of W).
+//
+// A 256 x 256 tile per block of 4 waves (2 x 2, 128 x 128 each). K runs in
+// chunks of 64 columns, i.e. 128 bytes per row: each load instruction of a
+// wave reads 8 whole rows of a chunk (8 lanes x 16 B per row), so every
+// request is a full 128-byte line. Chunks travel global -> VGPR -> LDS: two
+// register buffers keep chunks c + 2 and c + 3 in flight while chunk c is
+// multiplied from one LDS stage and chunk c + 1 waits in the other. In a row
+// of a stage, 16-byte vector v sits in slot v ^ (row & 7): the 8 lanes that
+// write one row and the rows read by one fragment instruction both fall on
+// distinct banks. Missing rows and the K tail load from the zero row.
+// ---------------------------------------------------------------------------
+namespace rs {
+constexpr int BM = 256, BN = 256, BK = 64, THREADS = 256;
+constexpr int ROWS = BM + BN;            // rows of a stage (A rows, then B rows)
+constexpr int ROW_BYTES = BK * 2;        // 128
+constexpr int STAGE_BYTES = ROWS * ROW_BYTES;  // 64 KB
+constexpr int LOADS = ROWS * (ROW_BYTES / 16) / THREADS;  // 16 vectors per thread per chunk
+constexpr int TM = 4, TN = 4;            // 32 x 32 blocks per wave
+}  // namespace rs
+
+__global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
+  using namespace rs;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE_BYTES + BN * 4];
+  float* bias_s = reinterpret_cast<float*>(smem + 2 * STAGE_BYTES);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // Tile coordinates are wave-uniform; readfirstlane keeps them (and the
+  // buffer descriptors built from them) in scalar registers.
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int tile = __builtin_amdgcn_readfirstlane(xcd_tile(blockIdx.x, gridDim.x));
+  const int tm = __builtin_amdgcn_readfirstlane(tile / tiles_n);
+  const int n0 = __builtin_amdgcn_readfirstlane((tile - tm * tiles_n) * BN);
+  const int64_t m0 = (int64_t)tm * BM;
+  const int K = a.K0;
+  for (int c = tid; c < BN; c += THREADS)
+    bias_s[c] = (a.bias && n0 + c < a.N) ? a.bias[n0 + c] : 0.0f;
+
+  // Load slot i of this thread: stage row (tid >> 3) + 32 i (A rows for
+  // i < 8, B rows after), 16-byte vector tid & 7 of the row's chunk. Loads go
+  // through buffer descriptors spanning the rows of this tile that exist, so
+  // missing rows read zeros; the K tail takes an offset past every
+  // descriptor's range (also zeros). No load is behind a branch.
+  const int r0 = tid >> 3, v = tid & 7;
+  const int64_t a_rows = a.M < a.rows_a0 ? a.M : a.rows_a0;  // rows of A that exist
+  const int64_t a_have = a_rows - m0 < 0 ? 0 : (a_rows - m0 > BM ? BM : a_rows - m0);
+  const int64_t b_have = a.N - n0 < 0 ? 0 : (a.N - n0 > BN ? BN : a.N - n0);
+  const int a_bytes = __builtin_amdgcn_readfirstlane((int)(a_have * a.lda0 * 2));
+  const int b_bytes = __builtin_amdgcn_readfirstlane((int)(b_have * a.ldb * 2));
+  const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<unsigned char*>(static_cast<const unsigned char*>(a.A0)) + m0 * a.lda0 * 2,
+      (short)0, a_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<unsigned char*>(static_cast<const unsigned char*>(a.B)) + (int64_t)n0 * a.ldb * 2,
+      (short)0, b_bytes, 0x00020000);
+  const int a_off0 = r0 * (int)a.lda0 * 2 + v * 16, a_step = 32 * (int)a.lda0 * 2;
+  const int b_off0 = r0 * (int)a.ldb * 2 + v * 16, b_step = 32 * (int)a.ldb * 2;
+  const int nchunks = (K + BK - 1) / BK;
+
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 stage_regs[2][LOADS];
+  auto load_chunk = [&](int chunk, u32x4 (&r)[LOADS]) __attribute__((always_inline)) {
+    // Bit 31 set (arithmetically, not by a select) sends the K tail past the
+    // descriptors' ranges.
+    const int oob = (int)((uint32_t)(K - 1 - (chunk * BK + v * 8)) & 0x80000000u);
+    const int koff = chunk * ROW_BYTES;
+#pragma unroll
+    for (int i = 0; i < LOADS / 2; ++i)
+      r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           a_rsrc, (a_off0 + i * a_step + koff) | oob, 0, 0));
+#pragma unroll
+    for (int i = 0; i < LOADS / 2; ++i)
+      r[LOADS / 2 + i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                       b_rsrc, (b_off0 + i * b_step + koff) | oob,
+                                                       0, 0));
+  };
+  // Row (r0 + 32 i) & 7 == r0 & 7: one slot for all of this thread's rows.
+  const int wslot = (v ^ (r0 & 7)) * 16;
+  auto store_chunk = [&](int stage, const u32x4 (&r)[LOADS]) __attribute__((always_inline)) {
+    unsigned char* base = smem + stage * STAGE_BYTES + r0 * ROW_BYTES + wslot;
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i)
+      *reinterpret_cast<u32x4*>(base + i * 32 * ROW_BYTES) = r[i];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  // Fragment reads: lane l takes row (l & 31) of a 32-row block and vector
+  // 2 ks + (l >> 5) of k-step ks; rows of a block start at multiples of 8.
+  const int frow = lane & 31, half = lane >> 5;
+  const int fa = (wm * 128 + frow) * ROW_BYTES;
+  const int fb = (BM + wn * 128 + frow) * ROW_BYTES;
+  auto read_a = [&](int stage, int ks, int i) __attribute__((always_inline)) {
+    const int slot = ((2 * ks + half) ^ (frow & 7)) * 16;
+    return *reinterpret_cast<const u32x4*>(smem + stage * STAGE_BYTES + fa + i * 32 * ROW_BYTES +
+                                            slot);
+  };
+  auto read_b = [&](int stage, int ks, u32x4 (&b)[TN]) __attribute__((always_inline)) {
+    const int slot = ((2 * ks + half) ^ (frow & 7)) * 16;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      b[j] = *reinterpret_cast<const u32x4*>(smem + stage * STAGE_BYTES + fb + j * 32 * ROW_BYTES +
+                                              slot);
+  };
+
+  // Prologue: chunk 0 into stage 0; chunks 1 and 2 in flight. (The compiler
+  // places the vmcnt waits before each store from the loaded registers.)
+  load_chunk(0, stage_regs[0]);
+  load_chunk(1, stage_regs[1]);
+  store_chunk(0, stage_regs[0]);
+  load_chunk(2, stage_regs[0]);
+  lds_barrier();
+
+  // One chunk: chunk c + 1 (the oldest loads in flight) goes into the other
+  // stage, whose last readers passed the barrier that ended the previous
+  // step; its registers then take chunk c + 3; chunk c is multiplied. The
+  // stage and register-buffer indices are compile-time (two steps per loop
+  // trip), so the buffers stay in registers.
+  auto step = [&](int c, auto CUR) __attribute__((always_inline)) {
+    constexpr int cur = decltype(CUR)::value, nxt = cur ^ 1;
+    store_chunk(nxt, stage_regs[nxt]);
+    load_chunk(c + 3, stage_regs[nxt]);
+    // k-steps ks = 0..3: the B fragments of k-step ks + 1 are read while the
+    // MFMAs of k-step ks run; A fragments are read one row block ahead.
+    u32x4 bf[2][TN], af[2];
+    read_b(cur, 0, bf[0]);
+    af[0] = read_a(cur, 0, 0);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) read_b(cur, ks + 1, bf[(ks + 1) & 1]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int nks = i + 1 < TM ? ks : ks + 1, ni = i + 1 < TM ? i + 1 : 0;
+        if (nks < 4) af[(i + 1) & 1] = read_a(cur, nks, ni);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, bf[ks & 1][j]), __builtin_bit_cast(bf16x8, af[i & 1]),
+              acc[i][j], 0, 0, 0);
+      }
+    }
+    lds_barrier();
+  };
+  // An odd chunk count runs one more chunk, read entirely out of range (all
+  // zeros), so the loop body has no exit in the middle.
+  for (int c = 0; c < nchunks; c += 2) {
+    step(c, std::integral_constant<int, 0>{});
+    step(c + 1, std::integral_constant<int, 1>{});
+  }
+
+  // ---- epilogue: bias (+ ReLU), bf16 stores ---------------------------------
+  // Lane l: output row m0 + 128 wm + 32 i + (l & 31); for group g of block j,
+  // columns n0 + 128 wn + 32 j + 8 g + 4 (l >> 5) + 0..3.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t r = m0 + wm * 128 + i * 32 + frow;
+    if (r >= a.M) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cb = wn * 128 + j * 32 + 8 * g + 4 * half;
+        const int c = n0 + cb;
+        if (c >= a.N) continue;
+        const float4 bv = *reinterpret_cast<const float4*>(bias_s + cb);
+        float x0 = acc[i][j][4 * g] + bv.x, x1 = acc[i][j][4 * g + 1] + bv.y;
+        float x2 = acc[i][j][4 * g + 2] + bv.z, x3 = acc[i][j][4 * g + 3] + bv.w;
+        if (a.relu) {
+          x0 = fmaxf(x0, 0.0f);
+          x1 = fmaxf(x1, 0.0f);
+          x2 = fmaxf(x2, 0.0f);
+          x3 = fmaxf(x3, 0.0f);
+        }
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + r * a.N + c) =
+            make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3));
+      }
+  }
+}
+
+// The register-staged kernel covers bf16 launches with one A source, no row
+// map, no addend and no L2 epilogue, and rows whose byte strides keep 16-byte
+// vectors aligned.
+bool use_rs(const GemmLaunch& a) {
+  const int64_t ldb = a.ldb ? a.ldb : a.K0;
+  // Buffer offsets are 32-bit: a tile's 256 rows must span < 2^31 bytes.
+  return a.bf16 && !a.l2norm && a.K1 == 0 && !a.rowmap && !a.addend && a.K0 % 8 == 0 &&
+         a.lda0 % 8 == 0 && ldb % 8 == 0 && a.lda0 <= (1 << 20) && ldb <= (1 << 20) &&
+         reinterpret_cast<uintptr_t>(a.A0) % 16 == 0 && reinterpret_cast<uintptr_t>(a.B) % 16 == 0;
+}
+
+hipError_t launch_rs(GemmLaunch a, hipStream_t s) {
+  if (!a.ldb) a.ldb = a.K0;
+  const int64_t tiles = ((a.M + rs::BM - 1) / rs::BM) * (int64_t)((a.N + rs::BN - 1) / rs::BN);
+  if (tiles <= 0) return hipSuccess;
+  if (tiles > 0x7FFFFFFFll) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gemm_rs_kernel, dim3((unsigned)tiles), dim3(rs::THREADS), 0, s, a);
+  return hipGetLastError();
+}
+
 template <typename C>
 hipError_t launch_cfg(const GemmLaunch& a, hipStream_t s) {
   const int64_t tiles = ((a.M + C::BM - 1) / C::BM) * (int64_t)((a.N + C::BN - 1) / C::BN);
@@ -455,6 +672,9 @@ hipError_t launch_typed(const GemmLaunch& a, hipStream_t s) {
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   ProfileScope prof(a.l2norm ? kKGemmW : (a.relu ? kKGemmQ : kKGemmR), s);
+#ifndef PINSAGE_GEMM_NO_RS
+  if (use_rs(a)) return launch_rs(a, s);
+#endif
   return a.bf16 ? launch_typed<true>(a, s) : launch_typed<false>(a, s);
 }
 

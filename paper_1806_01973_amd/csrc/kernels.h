@@ -42,6 +42,7 @@ struct WalkLaunch {
 };
 hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
 
+
 // n[r] = sum_t alpha[r][t] * P[idx[r][t]] for rows [0, rows) of the given
 // neighbourhood slice; storage dtype bf16 when bf16 is true.
 struct PoolLaunch {

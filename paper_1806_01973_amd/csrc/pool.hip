@@ -124,6 +124,70 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
   }
 }
 
+// Rows narrower than one wave slab (at most 64 / RG vectors): the wave splits
+// into RG lane groups of 64 / RG lanes, group g gathering neighbours
+// t = g, g + RG, ... of the row, so one load instruction reads RG rows. Each
+// group sums its neighbours in rank order; the RG partial sums are then added
+// by a fixed butterfly over the groups (the same order on every lane).
+template <bool BF16, int RG, int U = 8>
+__global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
+  using V = Vec<BF16>;
+  using Raw = typename V::Raw;
+  constexpr int VN = V::kN;
+  constexpr int GL = kWave / RG;  // lanes per group
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int grp = lane / GL, c = lane % GL;
+  const int T = a.T;
+  const Raw* __restrict__ P = static_cast<const Raw*>(a.P);
+  Raw* __restrict__ out = static_cast<Raw*>(a.out);
+  const int vec_per_row = a.m / VN;
+  const bool col_ok = c < vec_per_row;
+
+  for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < a.rows;
+       row += (int64_t)gridDim.x * kWavesPerBlock) {
+    const int32_t* __restrict__ ridx = a.idx + row * T;
+    int total = 0;
+    if (!a.weights) {
+      int part = 0;
+      for (int t = lane; t < T; t += kWave) part += a.counts[row * T + t];
+      total = wave_sum_i32(part);
+    }
+    float acc[VN];
+#pragma unroll
+    for (int v = 0; v < VN; ++v) acc[v] = 0.0f;
+    for (int t0 = 0; t0 < T; t0 += U * RG) {
+      Raw buf[U];
+      float alpha[U];
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        const int t = t0 + i * RG + grp;
+        int32_t v = t < T ? ridx[t] : -1;
+        if ((uint64_t)(int64_t)v >= (uint64_t)a.n_transform) v = -1;
+        float al = 0.0f;
+        if (v >= 0) {
+          if (a.weights) al = a.weights[row * T + t];
+          else al = (float)a.counts[row * T + t] / (float)total;
+        }
+        alpha[i] = al;
+        buf[i] = (v >= 0 && col_ok) ? P[(int64_t)v * vec_per_row + c] : Raw{};
+      }
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        float f[VN];
+        V::to_f32(buf[i], f);
+#pragma unroll
+        for (int v = 0; v < VN; ++v) acc[v] = fmaf(alpha[i], f[v], acc[v]);
+      }
+    }
+#pragma unroll
+    for (int o = GL; o < kWave; o <<= 1)
+#pragma unroll
+      for (int v = 0; v < VN; ++v) acc[v] += __shfl_xor(acc[v], o);
+    if (grp == 0 && col_ok) out[row * vec_per_row + c] = V::from_f32(acc);
+  }
+}
+
 template <bool BF16>
 hipError_t launch_typed(const PoolLaunch& a, hipStream_t s) {
   constexpr int VN = BF16 ? 8 : 4;
@@ -132,7 +196,12 @@ hipError_t launch_typed(const PoolLaunch& a, hipStream_t s) {
   const int64_t cap = 1ll << 22;
   const dim3 grid((unsigned)(blocks_needed < cap ? blocks_needed : cap));
   const dim3 block(256);
-  if (slabs <= 1) hipLaunchKernelGGL((pool_kernel<BF16, 1>), grid, block, 0, s, a);
+  const int vec_per_row = a.m / VN;
+  if (vec_per_row <= kWave / 4)
+    hipLaunchKernelGGL((pool_narrow_kernel<BF16, 4>), grid, block, 0, s, a);
+  else if (vec_per_row <= kWave / 2)
+    hipLaunchKernelGGL((pool_narrow_kernel<BF16, 2>), grid, block, 0, s, a);
+  else if (slabs <= 1) hipLaunchKernelGGL((pool_kernel<BF16, 1>), grid, block, 0, s, a);
   else if (slabs <= 2) hipLaunchKernelGGL((pool_kernel<BF16, 2>), grid, block, 0, s, a);
   else if (slabs <= 4) hipLaunchKernelGGL((pool_kernel<BF16, 4>), grid, block, 0, s, a);
   else if (slabs <= 8) hipLaunchKernelGGL((pool_kernel<BF16, 8>), grid, block, 0, s, a);

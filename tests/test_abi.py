@@ -185,3 +185,4 @@ def test_minibatch_validation_and_workspace(L):
     st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, 2048, L.PINSAGE_F32, 0.1, FAKE, FAKE,
                                      None)
     assert st == L.PINSAGE_EUNSUPPORTED
+
