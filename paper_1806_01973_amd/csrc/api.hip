@@ -175,9 +175,7 @@ hipError_t launch_transform(const pinsage_layer_t* L, const void* h_in, int64_t 
 
 // Layer bodies shared by convolve_layer, embed_all and the minibatch forward;
 // arguments already valid. Phase 1 fills the per-pin table of the workspace (P,
-// or R = P W_n^T when split); phase 2 pools it and applies W. Phase 1 reads
-// only h_in, so it may run on another stream than phase 2 of the same layer,
-// ordered by an event.
+// or R = P W_n^T when split); phase 2 pools it and applies W.
 int run_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
                   const int32_t* transform_rows, int64_t n_out, void* ws, hipStream_t s) {
   const bool bf16 = L->dtype == PINSAGE_BF16;
@@ -285,43 +283,6 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
   int st = run_transform(L, h_in, n_in, n_transform, transform_rows, n_out, ws, s);
   if (st) return st;
   return run_pool_dense(L, h_in, n_in, n_transform, nbr, self_rows, h_out, n_out, ws, s);
-}
-
-// A second stream per device (default priority, non-blocking) for work that
-// overlaps the caller's stream; created on first use and kept for the
-// process. Work on it is ordered against the caller's stream by events only.
-hipError_t side_stream(hipStream_t caller, hipStream_t* out) {
-  static std::mutex mu;
-  static std::vector<hipStream_t> streams;
-  int dev = 0;
-  hipError_t e = caller ? hipStreamGetDevice(caller, &dev) : hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  std::lock_guard<std::mutex> lk(mu);
-  if ((int)streams.size() <= dev) streams.resize(dev + 1, nullptr);
-  if (!streams[dev]) {
-    int cur = 0;
-    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
-    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
-    e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
-    if (cur != dev) (void)hipSetDevice(cur);
-    if (e != hipSuccess) {
-      streams[dev] = nullptr;
-      return e;
-    }
-  }
-  *out = streams[dev];
-  return hipSuccess;
-}
-
-// Makes `waiter` wait for the work enqueued on `signaller` so far.
-hipError_t stream_wait(hipStream_t waiter, hipStream_t signaller) {
-  hipEvent_t ev;
-  hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-  if (e != hipSuccess) return e;
-  e = hipEventRecord(ev, signaller);
-  if (e == hipSuccess) e = hipStreamWaitEvent(waiter, ev, 0);
-  (void)hipEventDestroy(ev);  // released once the recorded work completes
-  return e;
 }
 
 }  // namespace
@@ -504,16 +465,10 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  // The first layer's per-pin table (P, or R) depends on x only, so it is
-  // built on a side stream while the walks run on the caller's stream
-  // (memory-latency-bound walks beside MFMA-bound GEMMs); the pool waits for
-  // both.
-  hipStream_t side = nullptr;
-  hipError_t e = side_stream(s, &side);
-  if (e != hipSuccess) return hip_fail(e, "side stream");
-  if ((e = stream_wait(side, s)) != hipSuccess) return hip_fail(e, "stream fork");
+  if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
+    return st;
 
+  hipStream_t s = static_cast<hipStream_t>(stream);
   size_t conv = 0, h = 0;
   for (int k = 0; k < num_layers; ++k) {
     const size_t c = convolve_ws(&layers[k], graph->num_pins, n);
@@ -525,21 +480,10 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   }
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   unsigned char* hbuf[2] = {ws + conv, ws + conv + h};
-  // The GEMMs go first: each of their blocks takes most of a CU's LDS, and
-  // the walk blocks (small LDS and register footprint) fill in beside them.
-  st = run_transform(&layers[0], x, n, graph->num_pins, nullptr, n, ws, side);
-  if (!st) st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream);
-  // Joined even after a failed launch, so nothing of this call is left
-  // running on the side stream once the caller's stream is done.
-  if ((e = stream_wait(s, side)) != hipSuccess && !st) return hip_fail(e, "stream join");
-  if (st) return st;
   const void* cur = x;
   for (int k = 0; k < num_layers; ++k) {
     void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
-    st = k == 0 ? run_pool_dense(&layers[k], cur, n, graph->num_pins, nbr_out, nullptr, dst, n,
-                                 ws, s)
-                : run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n,
-                            ws, s);
+    st = run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n, ws, s);
     if (st) return st;
     cur = dst;
   }

@@ -489,6 +489,22 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
                                                        b_rsrc, (b_off0 + i * b_step + koff) | oob,
                                                        0, 0));
   };
+  // Quarter q of a chunk: load slots 4q .. 4q + 3 (A rows for q < 2).
+  auto load_slice = [&](int chunk, u32x4 (&r)[LOADS], int q) __attribute__((always_inline)) {
+    const int oob = (int)((uint32_t)(K - 1 - (chunk * BK + v * 8)) & 0x80000000u);
+    const int koff = chunk * ROW_BYTES;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * q + u;
+      if (i < LOADS / 2)
+        r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             a_rsrc, (a_off0 + i * a_step + koff) | oob, 0, 0));
+      else
+        r[i] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       b_rsrc, (b_off0 + (i - LOADS / 2) * b_step + koff) | oob, 0, 0));
+    }
+  };
   // Row (r0 + 32 i) & 7 == r0 & 7: one slot for all of this thread's rows.
   const int wslot = (v ^ (r0 & 7)) * 16;
   auto store_chunk = [&](int stage, const u32x4 (&r)[LOADS]) __attribute__((always_inline)) {
@@ -496,6 +512,12 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i)
       *reinterpret_cast<u32x4*>(base + i * 32 * ROW_BYTES) = r[i];
+  };
+  auto store_slice = [&](int stage, const u32x4 (&r)[LOADS], int q) __attribute__((always_inline)) {
+    unsigned char* base = smem + stage * STAGE_BYTES + r0 * ROW_BYTES + wslot;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      *reinterpret_cast<u32x4*>(base + (4 * q + u) * 32 * ROW_BYTES) = r[4 * q + u];
   };
 
   f32x16 acc[TM][TN];
@@ -511,17 +533,27 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   const int frow = lane & 31, half = lane >> 5;
   const int fa = (wm * 128 + frow) * ROW_BYTES;
   const int fb = (BM + wn * 128 + frow) * ROW_BYTES;
-  auto read_a = [&](int stage, int ks, int i) __attribute__((always_inline)) {
-    const int slot = ((2 * ks + half) ^ (frow & 7)) * 16;
-    return *reinterpret_cast<const u32x4*>(smem + stage * STAGE_BYTES + fa + i * 32 * ROW_BYTES +
-                                            slot);
+  struct Frags {
+    u32x4 a[TM], b[TN];
   };
-  auto read_b = [&](int stage, int ks, u32x4 (&b)[TN]) __attribute__((always_inline)) {
+  auto read_frags = [&](int stage, int ks, Frags& f) __attribute__((always_inline)) {
+    const unsigned char* st = smem + stage * STAGE_BYTES;
     const int slot = ((2 * ks + half) ^ (frow & 7)) * 16;
 #pragma unroll
+    for (int i = 0; i < TM; ++i)
+      f.a[i] = *reinterpret_cast<const u32x4*>(st + fa + i * 32 * ROW_BYTES + slot);
+#pragma unroll
     for (int j = 0; j < TN; ++j)
-      b[j] = *reinterpret_cast<const u32x4*>(smem + stage * STAGE_BYTES + fb + j * 32 * ROW_BYTES +
-                                              slot);
+      f.b[j] = *reinterpret_cast<const u32x4*>(st + fb + j * 32 * ROW_BYTES + slot);
+  };
+  auto mfma = [&](const Frags& f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, f.b[j]), __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j],
+            0, 0, 0);
   };
 
   // Prologue: chunk 0 into stage 0; chunks 1 and 2 in flight. (The compiler
@@ -539,25 +571,36 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   // trip), so the buffers stay in registers.
   auto step = [&](int c, auto CUR) __attribute__((always_inline)) {
     constexpr int cur = decltype(CUR)::value, nxt = cur ^ 1;
-    store_chunk(nxt, stage_regs[nxt]);
-    load_chunk(c + 3, stage_regs[nxt]);
-    // k-steps ks = 0..3: the B fragments of k-step ks + 1 are read while the
-    // MFMAs of k-step ks run; A fragments are read one row block ahead.
-    u32x4 bf[2][TN], af[2];
-    read_b(cur, 0, bf[0]);
-    af[0] = read_a(cur, 0, 0);
+    Frags f[2];
+    read_frags(cur, 0, f[0]);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      if (ks < 3) read_b(cur, ks + 1, bf[(ks + 1) & 1]);
+      // A quarter of chunk c + 1's LDS writes and of chunk c + 3's loads per
+      // k-step, the next k-step's fragment reads, and the 16 MFMAs of this
+      // k-step, interleaved one for one so that LDS and memory traffic run
+      // under the matrix work.
+      if (ks < 3) read_frags(cur, ks + 1, f[(ks + 1) & 1]);
+      store_slice(nxt, stage_regs[nxt], ks);
+      load_slice(c + 3, stage_regs[nxt], ks);
+      mfma(f[ks & 1]);
+      if (ks < 3) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int nks = i + 1 < TM ? ks : ks + 1, ni = i + 1 < TM ? i + 1 : 0;
-        if (nks < 4) af[(i + 1) & 1] = read_a(cur, nks, ni);
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        }
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      }
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8, bf[ks & 1][j]), __builtin_bit_cast(bf16x8, af[i & 1]),
-              acc[i][j], 0, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
       }
     }
     lds_barrier();
