@@ -22,6 +22,7 @@ of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--workload medium] [--no-cpu-baseline]
   python bench.py --copy-calibration   # plain copy of a known size, for counter scaling
+  python bench.py --layer 1024,2048,512 --rows 4000000 --dtype bf16   # one layer, for counters
 """
 
 from __future__ import annotations
@@ -342,6 +343,48 @@ def cpu_baseline_minibatch(inp, wl, threads):
                        f"gather excluded)")}
 
 
+def layer_probe(args) -> int:
+    """One CONVOLVE layer on seeded random inputs, for kernel-level measurement
+    (rocprofv3 counters, GEMM tile studies): rows x (d_in, m, d_out) in the
+    given dtype and dataflow, T random neighbours per row. Prints per-kernel
+    times and rates; not the headline metric."""
+    import torch
+
+    import paper_1806_01973_amd as ps
+    d_in, m, d_out = (int(v) for v in args.layer.split(","))
+    n, T = args.rows, 8
+    dt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
+    g = torch.Generator(device="cuda").manual_seed(0)
+    Q = (torch.randn(m, d_in, device="cuda", generator=g) * 0.05).to(dt)
+    W = (torch.randn(d_out, d_in + m, device="cuda", generator=g) * 0.05).to(dt)
+    q = torch.zeros(m, device="cuda")
+    w = torch.zeros(d_out, device="cuda")
+    h = torch.randn(n, d_in, device="cuda", generator=g).to(dt)
+    idx = torch.randint(0, n, (n, T), device="cuda", dtype=torch.int32, generator=g)
+    cnt = torch.ones((n, T), device="cuda", dtype=torch.int16).view(torch.uint16)
+    nb = ps.Neighborhoods(idx, cnt, None)
+    L = ps.DeviceLayer(Q, q, W, w, dtype=dt, dataflow=args.dataflow)
+    ws = torch.empty(ps.convolve_workspace_size(L, n, n), dtype=torch.uint8, device="cuda")
+    out = torch.empty((n, d_out), dtype=dt, device="cuda")
+    steps = args.steps if args.steps is not None else 3
+    _, prof = timed(lambda i: ps.convolve_layer(L, h, n, nb, out=out, workspace=ws),
+                    steps, args.warmup if args.warmup is not None else 1)
+    peak = MFMA_PEAK_TFLOPS[args.dtype]
+    split = args.dataflow == "dense_then_pool"
+    flops = {"gemm_q": 2.0 * n * d_in * m, "gemm_r": 2.0 * n * m * d_out if split else 0.0,
+             "gemm_w": 2.0 * n * (d_in + (0 if split else m)) * d_out}
+    res = {"layer": [d_in, m, d_out], "rows": n, "dtype": args.dtype, "dataflow": args.dataflow}
+    for name, (launches, ms) in prof.items():
+        if launches and name in flops:
+            per_call = ms / steps
+            res[name] = {"ms": per_call, "TFLOP/s": flops[name] / (per_call * 1e-3) / 1e12,
+                         "frac_mfma": flops[name] / (per_call * 1e-3) / 1e12 / peak}
+        elif launches:
+            res[name] = {"ms": ms / steps}
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,6 +398,10 @@ def main() -> int:
     ap.add_argument("--compare-dataflow", default="auto", choices=["auto", "on", "off"],
                     help="also time the other evaluation order (auto: small workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layer", default=None,
+                    help="d_in,m,d_out: time one layer on random inputs instead of a workload")
+    ap.add_argument("--rows", type=int, default=4_000_000, help="rows for --layer")
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"], help="dtype for --layer")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
@@ -368,6 +415,8 @@ def main() -> int:
     if args.copy_calibration:
         copy_calibration()
         return 0
+    if args.layer:
+        return layer_probe(args)
 
     import synth
 
