@@ -3,7 +3,9 @@
 A plain, slow CPU statement of the PinSage hot path (Ying et al., KDD 2018),
 written from the paper: random-walk importance neighbourhoods (Sec. 3.2),
 CONVOLVE (Algorithm 1), stacked layers evaluated layer-wise (Secs. 3.2, 3.4),
-MINIBATCH (Algorithm 2) and the max-margin loss (Sec. 3.3, Eq. 1). The
+MINIBATCH (Algorithm 2) with its output dense layers, the aggregators gamma
+(importance pooling, and the mean and max of Sec. 4's variants) and the
+max-margin loss (Sec. 3.3, Eq. 1). The
 arithmetic lives in ``oracle.cpp`` (fp64; importance weights fp32); this module
 only loads that library and marshals numpy arrays.
 
@@ -57,12 +59,12 @@ def _load():
                                             P, P, P, P, i32]
     lib.orc_build_neighborhoods.restype = None
     lib.orc_convolve_layer.argtypes = [P, i64, i32, i64, P, P, i32, P, P, i32, P, P, i32,
-                                       P, i64, P, i32]
+                                       P, i64, P, i32, i32]
     lib.orc_convolve_layer.restype = None
     lib.orc_minibatch_sets.argtypes = [P, i64, i32, P, i32, P, P, i64]
     lib.orc_minibatch_sets.restype = i64
     lib.orc_minibatch_embed.argtypes = [P, i64, i32, P, i32, P, P, i32, P, P, P, P, P, P, P,
-                                        i32]
+                                        i32, P]
     lib.orc_minibatch_embed.restype = None
     lib.orc_minibatch_sample.argtypes = [P, i64, i32, P, P, i64, i64, u64, i32, i32, i32, i32]
     lib.orc_minibatch_sample.restype = ctypes.c_void_p
@@ -73,8 +75,10 @@ def _load():
     lib.orc_sample_free.argtypes = [P]
     lib.orc_sample_free.restype = None
     lib.orc_minibatch_embed_sampled.argtypes = [P, i64, i32, P, i64, P, i32, P, i64, P, P, i32,
-                                                P, P, P, P, P, P, P, i32]
+                                                P, P, P, P, P, P, P, i32, P]
     lib.orc_minibatch_embed_sampled.restype = None
+    lib.orc_output_mlp.argtypes = [P, i64, i32, P, P, i32, P, i32, P, i32]
+    lib.orc_output_mlp.restype = None
     lib.orc_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_double, P]
     lib.orc_max_margin_loss.restype = ctypes.c_double
     _lib = lib
@@ -138,8 +142,13 @@ def build_neighborhoods(offsets, col, num_pins, seed, walks, hops, T, sources=No
     return idx, cnt, wts, int(steps[0])
 
 
-def convolve_layer(h_in, n_transform, Q, q, W, w, idx, wts, self_rows=None, nthreads=None):
-    """One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow of Sec. 3.4, fp64."""
+POOLS = {"importance": 0, "mean": 1, "max": 2}
+
+
+def convolve_layer(h_in, n_transform, Q, q, W, w, idx, wts, self_rows=None, nthreads=None,
+                   pool="importance"):
+    """One CONVOLVE layer (Algorithm 1) in the layer-wise dataflow of Sec. 3.4, fp64;
+    `pool` is the aggregator gamma (importance, mean or max)."""
     lib = _load()
     h = _c(h_in, np.float64)
     Qd, qd, Wd, wd = _c(Q, np.float64), _c(q, np.float64), _c(W, np.float64), _c(w, np.float64)
@@ -153,7 +162,7 @@ def convolve_layer(h_in, n_transform, Q, q, W, w, idx, wts, self_rows=None, nthr
     out = np.empty((n_out, d_out), np.float64)
     lib.orc_convolve_layer(_ptr(h), h.shape[0], d_in, n_transform, _ptr(Qd), _ptr(qd), m,
                            _ptr(Wd), _ptr(wd), d_out, _ptr(ix), _ptr(wt), T, _ptr(sr), n_out,
-                           _ptr(out), nthreads or default_threads())
+                           _ptr(out), nthreads or default_threads(), POOLS[pool])
     return out
 
 
@@ -163,7 +172,7 @@ def embed_all(x, num_pins, layers, idx, wts, nthreads=None):
     h = _c(x, np.float64)
     for L in layers:
         h = convolve_layer(h, num_pins, L["Q"], L["q"], L["W"], L["w"], idx, wts,
-                           nthreads=nthreads)
+                           nthreads=nthreads, pool=L.get("pool", "importance"))
     return h
 
 
@@ -206,10 +215,15 @@ def minibatch_embed(targets, x, layers, nbr_idx, nbr_w, nthreads=None):
         ms[k] = Q.shape[0]
         ds[k] = W.shape[0]
     out = np.empty((len(tg), int(ds[-1])), np.float64)
+    pools = _pools(layers)
     lib.orc_minibatch_embed(_ptr(tg), len(tg), K, _ptr(xd), xd.shape[1], _ptr(ix), _ptr(wt),
                             ix.shape[1], Qp, qp, _ptr(ms), Wp, wp, _ptr(ds), _ptr(out),
-                            nthreads or default_threads())
+                            nthreads or default_threads(), _ptr(pools))
     return out
+
+
+def _pools(layers):
+    return np.array([POOLS[L.get("pool", "importance")] for L in layers], np.int32)
 
 
 def _layer_ptrs(layers):
@@ -270,8 +284,22 @@ def minibatch_embed_sampled(targets, x_ids, x_rows, sample, layers, nthreads=Non
     lib.orc_minibatch_embed_sampled(_ptr(tg), len(tg), len(layers), _ptr(xi), len(xi), _ptr(xr),
                                     xr.shape[1], _ptr(ri), len(ri), _ptr(ix), _ptr(wt),
                                     ix.shape[1], Qp, qp, _ptr(ms), Wp, wp, _ptr(ds), _ptr(out),
-                                    nthreads or default_threads())
+                                    nthreads or default_threads(), _ptr(_pools(layers)))
     return out
+
+
+def output_mlp(h, G1, g, G2, nthreads=None):
+    """Algorithm 2's final dense layers, z = G2 ReLU(G1 h + g), per row (fp64)."""
+    lib = _load()
+    hd = _c(h, np.float64)
+    A, b, B = _c(G1, np.float64), _c(g, np.float64), _c(G2, np.float64)
+    d_hidden, d_in = A.shape
+    d_out = B.shape[0]
+    assert hd.shape[1] == d_in and B.shape[1] == d_hidden and b.shape == (d_hidden,)
+    z = np.empty((hd.shape[0], d_out), np.float64)
+    lib.orc_output_mlp(_ptr(hd), hd.shape[0], d_in, _ptr(A), _ptr(b), d_hidden, _ptr(B), d_out,
+                       _ptr(z), nthreads or default_threads())
+    return z
 
 
 def max_margin_loss(zq, zpos, zneg, margin):

@@ -16,6 +16,9 @@
 //   * layer-wise inference ... Sec. 3.4 (project every pin once, then pool).
 //   * MINIBATCH sets + loop .. Sec. 3.2, Algorithm 2 (sampling and embedding).
 //   * max-margin loss ........ Sec. 3.3, Eq. (1).
+//   * aggregators gamma ...... importance pooling (Sec. 3.2), and the element-wise
+//                              mean and max of the compared variants (Sec. 4).
+//   * output dense layers .... Algorithm 2, final loop: z = G2 ReLU(G1 h + g).
 //
 // Readings of points the paper leaves open are listed in the repository's
 // design notes; the ones that change arithmetic are restated at each function.
@@ -200,11 +203,45 @@ void combine_row(const double* h_self, int d_in, const double* n_u, int m, const
   for (int o = 0; o < d_out; ++o) out[o] = norm > 0.0 ? out[o] / norm : 0.0;
 }
 
+// The aggregator gamma of Algorithm 1, line 1, over the transformed
+// neighbours of one node, taken in rank order t = 0, 1, ... (ids < 0 are
+// padding and are skipped):
+//   mode 0, importance pooling (Sec. 3.2): sum_t alpha_t * P_t, alpha the
+//           node's normalised visit counts;
+//   mode 1, mean (Sec. 4, gamma = mean): (1 / #neighbours) * sum_t P_t;
+//   mode 2, max (Sec. 4, gamma = max): element-wise max over the P_t.
+// An empty neighbourhood gives the zero vector in every mode.
+template <typename RowOf>
+void pool_row(int mode, const int32_t* ids, const float* alpha, int T, RowOf row_of, int m,
+              double* n_u) {
+  int count = 0;
+  for (int t = 0; t < T; ++t)
+    if (ids[t] >= 0) ++count;
+  for (int i = 0; i < m; ++i) n_u[i] = 0.0;
+  if (count == 0) return;
+  if (mode == 2) {
+    bool first = true;
+    for (int t = 0; t < T; ++t) {
+      if (ids[t] < 0) continue;
+      const double* pv = row_of(ids[t]);
+      for (int i = 0; i < m; ++i) n_u[i] = first ? pv[i] : std::max(n_u[i], pv[i]);
+      first = false;
+    }
+    return;
+  }
+  for (int t = 0; t < T; ++t) {
+    if (ids[t] < 0) continue;
+    const double a = mode == 1 ? 1.0 / (double)count : (double)alpha[t];
+    const double* pv = row_of(ids[t]);
+    for (int i = 0; i < m; ++i) n_u[i] += a * pv[i];
+  }
+}
+
 }  // namespace
 
 extern "C" {
 
-int orc_version(void) { return 1; }
+int orc_version(void) { return 2; }
 
 // Philox4x32-10 block function, exposed for known-answer tests.
 void orc_philox4x32_10(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
@@ -273,7 +310,8 @@ void orc_build_neighborhoods(const int64_t* off, const int32_t* col, int64_t num
 void orc_convolve_layer(const double* h_in, int64_t n_in, int d_in, int64_t n_transform,
                         const double* Q, const double* q, int m, const double* W,
                         const double* w, int d_out, const int32_t* idx, const float* wts, int T,
-                        const int64_t* self_rows, int64_t n_out, double* h_out, int nthreads) {
+                        const int64_t* self_rows, int64_t n_out, double* h_out, int nthreads,
+                        int pool) {
   (void)n_in;
   std::vector<double> P((size_t)n_transform * (size_t)m);
   parallel_rows(n_transform, nthreads, [&](int64_t lo, int64_t hi) {
@@ -283,14 +321,8 @@ void orc_convolve_layer(const double* h_in, int64_t n_in, int d_in, int64_t n_tr
   parallel_rows(n_out, nthreads, [&](int64_t lo, int64_t hi) {
     std::vector<double> n_u((size_t)m);
     for (int64_t r = lo; r < hi; ++r) {
-      std::fill(n_u.begin(), n_u.end(), 0.0);
-      for (int t = 0; t < T; ++t) {
-        int32_t v = idx[r * T + t];
-        if (v < 0) continue;
-        double a = (double)wts[r * T + t];
-        const double* pv = P.data() + (int64_t)v * m;
-        for (int i = 0; i < m; ++i) n_u[i] += a * pv[i];
-      }
+      pool_row(pool, idx + r * T, wts + r * T, T,
+               [&](int32_t v) { return P.data() + (int64_t)v * m; }, m, n_u.data());
       int64_t self = self_rows ? self_rows[r] : r;
       combine_row(h_in + self * d_in, d_in, n_u.data(), m, W, w, d_out, h_out + r * d_out);
     }
@@ -341,7 +373,7 @@ void minibatch_embed_impl(const int32_t* targets, int64_t num_targets, int K,
                           const std::vector<std::vector<int32_t>>& S, XRow x_row, int d0,
                           NbrRow nbr_row, int T, const double* const* Qs, const double* const* qs,
                           const int* ms, const double* const* Ws, const double* const* ws,
-                          const int* d_outs, double* out, int nthreads) {
+                          const int* d_outs, const int* pools, double* out, int nthreads) {
   std::map<int32_t, int64_t> pos_prev;  // node -> row in h_prev
   std::vector<double> h_prev((size_t)S[0].size() * d0);
   for (size_t i = 0; i < S[0].size(); ++i) {
@@ -378,15 +410,9 @@ void minibatch_embed_impl(const int32_t* targets, int64_t num_targets, int K,
       std::vector<double> n_u((size_t)m);
       for (int64_t i = lo; i < hi; ++i) {
         int32_t u = S[k][i];
-        std::fill(n_u.begin(), n_u.end(), 0.0);
         const auto row = nbr_row(u);
-        for (int t = 0; t < T; ++t) {
-          int32_t v = row.first[t];
-          if (v < 0) continue;
-          double a = (double)row.second[t];
-          const double* pv = Pn.data() + pos_need.at(v) * m;
-          for (int j = 0; j < m; ++j) n_u[j] += a * pv[j];
-        }
+        pool_row(pools ? pools[k - 1] : 0, row.first, row.second, T,
+                 [&](int32_t v) { return Pn.data() + pos_need.at(v) * m; }, m, n_u.data());
         combine_row(h_prev.data() + pos_prev.at(u) * d_prev, d_prev, n_u.data(), m, W, w,
                     d_out, h_next.data() + i * d_out);
       }
@@ -442,7 +468,7 @@ void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, con
                          int d0, const int32_t* nbr_idx, const float* nbr_w, int T,
                          const double* const* Qs, const double* const* qs, const int* ms,
                          const double* const* Ws, const double* const* ws, const int* d_outs,
-                         double* out, int nthreads) {
+                         double* out, int nthreads, const int* pools) {
   auto ids_of = [&](int32_t u) { return nbr_idx + (int64_t)u * T; };
   auto S = minibatch_sets_impl(targets, num_targets, K, T, ids_of);
   minibatch_embed_impl(
@@ -450,7 +476,7 @@ void orc_minibatch_embed(const int32_t* targets, int64_t num_targets, int K, con
       [&](int32_t u) {
         return std::make_pair(nbr_idx + (int64_t)u * T, nbr_w + (int64_t)u * T);
       },
-      T, Qs, qs, ms, Ws, ws, d_outs, out, nthreads);
+      T, Qs, qs, ms, Ws, ws, d_outs, pools, out, nthreads);
 }
 
 // Sampling part of Algorithm 2 with neighbourhoods computed on demand, for
@@ -548,7 +574,8 @@ void orc_minibatch_embed_sampled(const int32_t* targets, int64_t num_targets, in
                                  const float* wts, int T, const double* const* Qs,
                                  const double* const* qs, const int* ms,
                                  const double* const* Ws, const double* const* ws,
-                                 const int* d_outs, double* out, int nthreads) {
+                                 const int* d_outs, double* out, int nthreads,
+                                 const int* pools) {
   auto find = [](const int32_t* ids, int64_t n, int32_t v) -> int64_t {
     const int32_t* p = std::lower_bound(ids, ids + n, v);
     return (p != ids + n && *p == v) ? (int64_t)(p - ids) : -1;
@@ -562,7 +589,30 @@ void orc_minibatch_embed_sampled(const int32_t* targets, int64_t num_targets, in
         const int64_t r = find(row_ids, n_rows, u);
         return std::make_pair(idx + r * T, wts + r * T);
       },
-      T, Qs, qs, ms, Ws, ws, d_outs, out, nthreads);
+      T, Qs, qs, ms, Ws, ws, d_outs, pools, out, nthreads);
+}
+
+// Algorithm 2, final loop: the output embedding z_u = G2 ReLU(G1 h_u + g) of
+// each row, with G1 [d_hidden x d_in], g [d_hidden], G2 [d_out x d_hidden]
+// (no bias and no activation after G2).
+void orc_output_mlp(const double* h, int64_t n, int d_in, const double* G1, const double* g,
+                    int d_hidden, const double* G2, int d_out, double* z, int nthreads) {
+  parallel_rows(n, nthreads, [&](int64_t lo, int64_t hi) {
+    std::vector<double> a((size_t)d_hidden);
+    for (int64_t r = lo; r < hi; ++r) {
+      for (int i = 0; i < d_hidden; ++i) {
+        double acc = 0.0;
+        for (int j = 0; j < d_in; ++j) acc += G1[(int64_t)i * d_in + j] * h[r * d_in + j];
+        acc += g[i];
+        a[i] = acc > 0.0 ? acc : 0.0;
+      }
+      for (int o = 0; o < d_out; ++o) {
+        double acc = 0.0;
+        for (int i = 0; i < d_hidden; ++i) acc += G2[(int64_t)o * d_hidden + i] * a[i];
+        z[r * d_out + o] = acc;
+      }
+    }
+  });
 }
 
 // Eq. (1), Sec. 3.3: for each pair (q, i), the expectation over negatives of
