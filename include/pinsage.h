@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 2
+#define PINSAGE_ABI_VERSION 3
 
 enum {
   PINSAGE_OK = 0,
@@ -107,6 +107,18 @@ typedef struct {
  *                    The gather reads d_out instead of m values per neighbour. */
 typedef enum { PINSAGE_POOL_THEN_DENSE = 0, PINSAGE_DENSE_THEN_POOL = 1 } pinsage_dataflow_t;
 
+/* The aggregator gamma of Algorithm 1, line 1, over a node's neighbourhood
+ * (rank order, padding skipped; an empty neighbourhood gives zero):
+ *   IMPORTANCE  sum_t alpha_t P_t, alpha the normalised visit counts (Sec. 3.2)
+ *   MEAN        element-wise mean of the neighbours' rows (gamma = mean, Sec. 4)
+ *   MAX         element-wise max of the neighbours' rows (gamma = max, Sec. 4)
+ * MAX is not linear, so it requires PINSAGE_POOL_THEN_DENSE. */
+typedef enum {
+  PINSAGE_POOL_IMPORTANCE = 0,
+  PINSAGE_POOL_MEAN = 1,
+  PINSAGE_POOL_MAX = 2
+} pinsage_pool_t;
+
 /* One CONVOLVE layer's parameters (Algorithm 1; Sec. 3.2 "Stacking
  * convolutions": shared by all nodes, distinct per layer).
  *   Q device [m][d_in]            (storage dtype)
@@ -116,6 +128,7 @@ typedef enum { PINSAGE_POOL_THEN_DENSE = 0, PINSAGE_DENSE_THEN_POOL = 1 } pinsag
  *                                 pooled neighbourhood vector
  *   w device fp32 [d_out]
  *   dataflow                      evaluation order (above)
+ *   pool                          the aggregator gamma (above)
  * Limits: d_in, m, d_out multiples of 16; d_in, m <= 8192; d_out <= 512. */
 typedef struct {
   int32_t d_in;
@@ -127,7 +140,25 @@ typedef struct {
   const void* W;
   const float* w;
   pinsage_dataflow_t dataflow;
+  pinsage_pool_t pool;
 } pinsage_layer_t;
+
+/* The output dense layers of Algorithm 2 (its final loop), applied after the
+ * last CONVOLVE layer: z_u = G2 ReLU(G1 h_u + g).
+ *   G1 device [d_hidden][d_in]   (storage dtype)
+ *   g  device fp32 [d_hidden]
+ *   G2 device [d_out][d_hidden]  (storage dtype); no bias, no activation
+ * Accumulation fp32; the hidden activations are stored in the storage dtype.
+ * Limits: d_in, d_hidden, d_out multiples of 16 and <= 8192. */
+typedef struct {
+  int32_t d_in;
+  int32_t d_hidden;
+  int32_t d_out;
+  pinsage_dtype_t dtype;
+  const void* G1;
+  const float* g;
+  const void* G2;
+} pinsage_mlp_t;
 
 /* Version of this ABI (PINSAGE_ABI_VERSION). */
 int pinsage_version(void);
@@ -192,6 +223,15 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
                       unsigned long long* total_steps, void* workspace,
                       size_t workspace_bytes, void* stream);
 
+/* Workspace bytes needed by pinsage_output_mlp for n rows. */
+int pinsage_output_mlp_workspace_size(const pinsage_mlp_t* mlp, int64_t n, size_t* bytes);
+
+/* z[r] = G2 ReLU(G1 h[r] + g) for r in [0, n) (Algorithm 2, final loop).
+ * h: device [n][d_in], z: device [n][d_out], storage dtype; workspace: device,
+ * >= pinsage_output_mlp_workspace_size bytes, 256-aligned. */
+int pinsage_output_mlp(const pinsage_mlp_t* mlp, const void* h, int64_t n, void* z,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
 /* Max-margin loss, Eq. (1) (Sec. 3.3), with the expectation over negatives
  * taken as the mean over the shared negative set (500 per minibatch in the
  * paper):
@@ -222,7 +262,8 @@ typedef struct {
 int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_walk_params_t* walk,
                                      const pinsage_layer_t* layers, int32_t num_layers,
-                                     int64_t num_pairs, int64_t num_negatives, size_t* bytes);
+                                     const pinsage_mlp_t* mlp, int64_t num_pairs,
+                                     int64_t num_negatives, size_t* bytes);
 
 /* Minibatch forward of Algorithm 2 plus the loss of Eq. (1):
  *   S^(K) = queries u positives u negatives; S^(k-1) = S^(k) u N(S^(k))
@@ -230,16 +271,19 @@ int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
  *   each equals the node's row of the all-node table); every set is sorted
  *   and de-duplicated on the device and neighbour ids are re-indexed into the
  *   compact sets (Sec. 3.3); then h^(k) = CONVOLVE^(k) for u in S^(k),
- *   k = 1..K, with h^(0) = x (read in place through a row map), and the loss
- *   over the pairs on h^(K).
- * x: device [num_nodes][layers[0].d_in]; loss: device fp32 scalar;
- * per_pair: device fp32 [B] or NULL; z_out: device [2B + n_neg][d_out] or
- * NULL -- h^(K) of queries, then positives, then negatives; set_sizes: host
- * int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|.
+ *   k = 1..K, with h^(0) = x (read in place through a row map); then, when
+ *   mlp is non-NULL, z = G2 ReLU(G1 h^(K) + g) (Algorithm 2, final loop),
+ *   else z = h^(K); and the loss over the pairs on z.
+ * x: device [num_nodes][layers[0].d_in]; mlp: NULL or d_in = the last
+ * layer's d_out, same dtype; loss: device fp32 scalar; per_pair: device fp32
+ * [B] or NULL; z_out: device [2B + n_neg][d] or NULL (d = mlp->d_out, or the
+ * last layer's d_out) -- z of queries, then positives, then negatives;
+ * set_sizes: host int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|.
  * This call synchronises `stream` K + 1 times to size the frontiers.
- * Limits: as for the layers, plus d_out of the last layer <= 1024. */
+ * Limits: as for the layers, plus d <= 1024. */
 int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
-                              const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                              const pinsage_layer_t* layers, int32_t num_layers,
+                              const pinsage_mlp_t* mlp, const void* x,
                               const pinsage_pairs_t* pairs, float* loss, float* per_pair,
                               void* z_out, int64_t* set_sizes, void* workspace,
                               size_t workspace_bytes, void* stream);
@@ -257,7 +301,8 @@ enum {
   PINSAGE_KERNEL_MINIBATCH = 4,
   PINSAGE_KERNEL_LOSS = 5,
   PINSAGE_KERNEL_GEMM_R = 6, /* neighbour half of W per pin (DENSE_THEN_POOL) */
-  PINSAGE_KERNEL_COUNT = 7
+  PINSAGE_KERNEL_MLP = 7,    /* output dense layers */
+  PINSAGE_KERNEL_COUNT = 8
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

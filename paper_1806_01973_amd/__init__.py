@@ -10,6 +10,7 @@ from ._lib import PinsageError, lib  # noqa: F401
 from .api import (  # noqa: F401
     DeviceGraph,
     DeviceLayer,
+    DeviceMLP,
     EmbedAll,
     Minibatch,
     Neighborhoods,
@@ -19,6 +20,7 @@ from .api import (  # noqa: F401
     embed_all,
     embed_all_workspace_size,
     max_margin_loss,
+    output_mlp,
     profile_enable,
     profile_read,
 )

@@ -18,15 +18,17 @@ PINSAGE_I32, PINSAGE_I64 = 0, 1
 PINSAGE_F32, PINSAGE_BF16 = 0, 1
 PINSAGE_POOL_THEN_DENSE, PINSAGE_DENSE_THEN_POOL = 0, 1
 DATAFLOWS = {"pool_then_dense": PINSAGE_POOL_THEN_DENSE, "dense_then_pool": PINSAGE_DENSE_THEN_POOL}
+POOLS = {"importance": 0, "mean": 1, "max": 2}
 
 (KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
- KERNEL_GEMM_R) = range(7)
-KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r"]
+ KERNEL_GEMM_R, KERNEL_MLP) = range(8)
+KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
     "pinsage_build_neighborhoods", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
-    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_max_margin_loss",
+    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_output_mlp_workspace_size",
+    "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
     "pinsage_profile_enable", "pinsage_profile_read",
 ]
@@ -52,7 +54,14 @@ class Neighborhoods(ctypes.Structure):
 class Layer(ctypes.Structure):
     _fields_ = [("d_in", ctypes.c_int32), ("m", ctypes.c_int32), ("d_out", ctypes.c_int32),
                 ("dtype", ctypes.c_int), ("Q", ctypes.c_void_p), ("q", ctypes.c_void_p),
-                ("W", ctypes.c_void_p), ("w", ctypes.c_void_p), ("dataflow", ctypes.c_int)]
+                ("W", ctypes.c_void_p), ("w", ctypes.c_void_p), ("dataflow", ctypes.c_int),
+                ("pool", ctypes.c_int)]
+
+
+class MLP(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int32), ("d_hidden", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("dtype", ctypes.c_int), ("G1", ctypes.c_void_p), ("g", ctypes.c_void_p),
+                ("G2", ctypes.c_void_p)]
 
 
 class Pairs(ctypes.Structure):
@@ -96,14 +105,18 @@ def lib():
     L.pinsage_embed_all.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                     ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Neighborhoods),
                                     P, P, P, ctypes.c_size_t, P]
+    L.pinsage_output_mlp_workspace_size.argtypes = [ctypes.POINTER(MLP), i64,
+                                                    ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_output_mlp.argtypes = [ctypes.POINTER(MLP), P, i64, P, P, ctypes.c_size_t, P]
     L.pinsage_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_int, ctypes.c_float,
                                           P, P, P]
     L.pinsage_minibatch_workspace_size.argtypes = [ctypes.POINTER(Graph),
                                                    ctypes.POINTER(WalkParams),
-                                                   ctypes.POINTER(Layer), i32, i64, i64,
-                                                   ctypes.POINTER(ctypes.c_size_t)]
+                                                   ctypes.POINTER(Layer), i32, ctypes.POINTER(MLP),
+                                                   i64, i64, ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_minibatch_forward.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
-                                            ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Pairs),
+                                            ctypes.POINTER(Layer), i32, ctypes.POINTER(MLP), P,
+                                            ctypes.POINTER(Pairs),
                                             P, P, P, ctypes.POINTER(ctypes.c_int64), P,
                                             ctypes.c_size_t, P]
     L.pinsage_profile_enable.argtypes = [ctypes.c_int]

@@ -107,13 +107,17 @@ class DeviceLayer:
     dataflow: "pool_then_dense" (Algorithm 1 as written: pool m-wide
     transformed rows, then W) or "dense_then_pool" (the neighbour half of W is
     applied per pin first, so the pool gathers d_out-wide rows); both compute
-    the same layer."""
+    the same layer. pool: the aggregator gamma, "importance" (Sec. 3.2), "mean"
+    or "max" (Sec. 4); "max" needs "pool_then_dense"."""
 
     def __init__(self, Q, q, W, w, dtype: torch.dtype = torch.float32, device="cuda",
-                 dataflow: str = "pool_then_dense"):
+                 dataflow: str = "pool_then_dense", pool: str = "importance"):
         if dataflow not in L.DATAFLOWS:
             raise ValueError(f"dataflow must be one of {sorted(L.DATAFLOWS)}, got {dataflow!r}")
+        if pool not in L.POOLS:
+            raise ValueError(f"pool must be one of {sorted(L.POOLS)}, got {pool!r}")
         self.dataflow = dataflow
+        self.pool = pool
         self.dtype = dtype
         self.Q = torch.as_tensor(Q).to(device=device, dtype=dtype).contiguous()
         self.W = torch.as_tensor(W).to(device=device, dtype=dtype).contiguous()
@@ -127,7 +131,46 @@ class DeviceLayer:
     def struct(self) -> L.Layer:
         return L.Layer(self.d_in, self.m, self.d_out, _dtype_code(self.dtype), self.Q.data_ptr(),
                        self.q.data_ptr(), self.W.data_ptr(), self.w.data_ptr(),
-                       L.DATAFLOWS[self.dataflow])
+                       L.DATAFLOWS[self.dataflow], L.POOLS[self.pool])
+
+
+class DeviceMLP:
+    """Output dense layers of Algorithm 2 on the GPU: z = G2 ReLU(G1 h + g);
+    G1 [d_hidden, d_in], g [d_hidden] fp32, G2 [d_out, d_hidden]."""
+
+    def __init__(self, G1, g, G2, dtype: torch.dtype = torch.float32, device="cuda"):
+        self.dtype = dtype
+        self.G1 = torch.as_tensor(G1).to(device=device, dtype=dtype).contiguous()
+        self.G2 = torch.as_tensor(G2).to(device=device, dtype=dtype).contiguous()
+        self.g = torch.as_tensor(g).to(device=device, dtype=torch.float32).contiguous()
+        self.d_hidden, self.d_in = self.G1.shape
+        self.d_out = self.G2.shape[0]
+        if self.G2.shape[1] != self.d_hidden or self.g.numel() != self.d_hidden:
+            raise ValueError("G2 must be [d_out, d_hidden] and g [d_hidden]")
+
+    def struct(self) -> L.MLP:
+        return L.MLP(self.d_in, self.d_hidden, self.d_out, _dtype_code(self.dtype),
+                     self.G1.data_ptr(), self.g.data_ptr(), self.G2.data_ptr())
+
+
+def output_mlp(mlp: DeviceMLP, h: torch.Tensor, out: Optional[torch.Tensor] = None,
+               workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """z = G2 ReLU(G1 h + g) for every row of h (Algorithm 2, final loop)."""
+    h = _dev(h, "h", mlp.dtype)
+    n = int(h.shape[0])
+    if out is None:
+        out = torch.empty((n, mlp.d_out), dtype=mlp.dtype, device=h.device)
+    _dev(out, "out", mlp.dtype)
+    m = mlp.struct()
+    need = ctypes.c_size_t(0)
+    L.check(L.lib().pinsage_output_mlp_workspace_size(ctypes.byref(m), n, ctypes.byref(need)),
+            "pinsage_output_mlp_workspace_size")
+    if workspace is None:
+        workspace = torch.empty(max(1, int(need.value)), dtype=torch.uint8, device=h.device)
+    L.check(L.lib().pinsage_output_mlp(ctypes.byref(m), _ptr(h), n, _ptr(out), _ptr(workspace),
+                                       workspace.numel(), _stream(stream)),
+            "pinsage_output_mlp")
+    return out
 
 
 def build_neighborhoods(graph: DeviceGraph, walks: int, hops: int, T: int, seed: int,
@@ -258,22 +301,26 @@ class Minibatch:
     negatives."""
 
     def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
-                 T: int, seed: int, num_pairs: int, num_negatives: int):
+                 T: int, seed: int, num_pairs: int, num_negatives: int,
+                 mlp: Optional[DeviceMLP] = None):
         self.graph, self.layers = graph, list(layers)
+        self.mlp = mlp
+        self._mlp = mlp.struct() if mlp is not None else None
         self.walk = L.WalkParams(seed, walks, hops, T)
         self.B, self.n_neg = int(num_pairs), int(num_negatives)
         self._g = graph.struct()
         self._layers = _layer_array(self.layers)
         n = ctypes.c_size_t(0)
         st = L.lib().pinsage_minibatch_workspace_size(ctypes.byref(self._g), ctypes.byref(self.walk),
-                                                      self._layers, len(self.layers), self.B,
-                                                      self.n_neg, ctypes.byref(n))
+                                                      self._layers, len(self.layers),
+                                                      self._mlp_ref(), self.B, self.n_neg,
+                                                      ctypes.byref(n))
         L.check(st, "pinsage_minibatch_workspace_size")
         dev = graph.col.device
         self.workspace = torch.empty(max(1, int(n.value)), dtype=torch.uint8, device=dev)
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)
         self.per_pair = torch.empty(self.B, dtype=torch.float32, device=dev)
-        d = self.layers[-1].d_out
+        d = mlp.d_out if mlp is not None else self.layers[-1].d_out
         self.z = torch.empty((2 * self.B + self.n_neg, d), dtype=self.layers[-1].dtype, device=dev)
         self.set_sizes = (ctypes.c_int64 * (len(self.layers) + 1))()
 
@@ -287,7 +334,8 @@ class Minibatch:
             raise ValueError("pair counts differ from the sizes this workspace was made for")
         pairs = L.Pairs(self.B, self.n_neg, q.data_ptr(), p.data_ptr(), ng.data_ptr(), margin)
         st = L.lib().pinsage_minibatch_forward(ctypes.byref(self._g), ctypes.byref(self.walk),
-                                               self._layers, len(self.layers), _ptr(x),
+                                               self._layers, len(self.layers), self._mlp_ref(),
+                                               _ptr(x),
                                                ctypes.byref(pairs), _ptr(self.loss),
                                                _ptr(self.per_pair),
                                                _ptr(self.z) if want_z else None, self.set_sizes,
@@ -298,6 +346,9 @@ class Minibatch:
 
     def sizes(self) -> list:
         return [int(v) for v in self.set_sizes]
+
+    def _mlp_ref(self):
+        return ctypes.byref(self._mlp) if self._mlp is not None else None
 
 
 def profile_enable(on: bool = True) -> None:

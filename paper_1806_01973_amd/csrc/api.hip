@@ -102,6 +102,77 @@ int check_layer(const pinsage_layer_t* L, int k) {
     return fail(PINSAGE_EINVAL, "layer %d: a parameter pointer is NULL", k);
   if (L->dataflow != PINSAGE_POOL_THEN_DENSE && L->dataflow != PINSAGE_DENSE_THEN_POOL)
     return fail(PINSAGE_EINVAL, "layer %d: unknown dataflow %d", k, (int)L->dataflow);
+  if (L->pool != PINSAGE_POOL_IMPORTANCE && L->pool != PINSAGE_POOL_MEAN &&
+      L->pool != PINSAGE_POOL_MAX)
+    return fail(PINSAGE_EINVAL, "layer %d: unknown pool %d", k, (int)L->pool);
+  if (L->pool == PINSAGE_POOL_MAX && L->dataflow == PINSAGE_DENSE_THEN_POOL)
+    return fail(PINSAGE_EUNSUPPORTED,
+                "layer %d: max pooling is not linear and needs PINSAGE_POOL_THEN_DENSE", k);
+  return PINSAGE_OK;
+}
+
+int check_mlp(const pinsage_mlp_t* M) {
+  if (!M) return fail(PINSAGE_EINVAL, "mlp is NULL");
+  if (M->dtype != PINSAGE_F32 && M->dtype != PINSAGE_BF16)
+    return fail(PINSAGE_EINVAL, "mlp: unknown dtype %d", (int)M->dtype);
+  if (M->d_in <= 0 || M->d_hidden <= 0 || M->d_out <= 0)
+    return fail(PINSAGE_EINVAL, "mlp: dims must be positive (%d, %d, %d)", M->d_in, M->d_hidden,
+                M->d_out);
+  if (M->d_in % 16 || M->d_hidden % 16 || M->d_out % 16)
+    return fail(PINSAGE_EUNSUPPORTED, "mlp: d_in, d_hidden, d_out must be multiples of 16");
+  if (M->d_in > 8192 || M->d_hidden > 8192 || M->d_out > 8192)
+    return fail(PINSAGE_EUNSUPPORTED, "mlp: dims above 8192");
+  if (!M->G1 || !M->g || !M->G2) return fail(PINSAGE_EINVAL, "mlp: a parameter pointer is NULL");
+  return PINSAGE_OK;
+}
+
+size_t mlp_ws(const pinsage_mlp_t* M, int64_t n) {
+  const int64_t chunk = n < kChunkRows ? n : kChunkRows;
+  return align_up((size_t)chunk * M->d_hidden * elem_size(M->dtype));
+}
+
+// z = G2 ReLU(G1 h + g) in row chunks (hidden activations in the workspace).
+int run_mlp(const pinsage_mlp_t* M, const void* h, const int32_t* rowmap, int64_t n_h,
+            int64_t n, void* z, void* ws, hipStream_t s) {
+  const size_t es = elem_size(M->dtype);
+  const bool bf16 = M->dtype == PINSAGE_BF16;
+  for (int64_t r0 = 0; r0 < n; r0 += kChunkRows) {
+    const int64_t rows = (n - r0) < kChunkRows ? (n - r0) : kChunkRows;
+    GemmLaunch g1{};
+    if (rowmap) {
+      g1.A0 = h;
+      g1.rowmap = rowmap + r0;
+      g1.rows_a0 = n_h;
+    } else {
+      g1.A0 = static_cast<const unsigned char*>(h) + (size_t)r0 * M->d_in * es;
+      g1.rows_a0 = n_h - r0;
+    }
+    g1.lda0 = M->d_in;
+    g1.K0 = M->d_in;
+    g1.B = M->G1;
+    g1.bias = M->g;
+    g1.M = rows;
+    g1.N = M->d_hidden;
+    g1.C = ws;
+    g1.bf16 = bf16;
+    g1.relu = true;
+    g1.prof_class = kKMlp;
+    hipError_t e = launch_gemm(g1, s);
+    if (e != hipSuccess) return hip_fail(e, "output layer G1 launch");
+    GemmLaunch g2{};
+    g2.A0 = ws;
+    g2.rows_a0 = rows;
+    g2.lda0 = M->d_hidden;
+    g2.K0 = M->d_hidden;
+    g2.B = M->G2;
+    g2.M = rows;
+    g2.N = M->d_out;
+    g2.C = static_cast<unsigned char*>(z) + (size_t)r0 * M->d_out * es;
+    g2.bf16 = bf16;
+    g2.prof_class = kKMlp;
+    e = launch_gemm(g2, s);
+    if (e != hipSuccess) return hip_fail(e, "output layer G2 launch");
+  }
   return PINSAGE_OK;
 }
 
@@ -239,6 +310,7 @@ int run_pool_dense(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
     pl.T = T;
     pl.rows = rows;
     pl.out = nbuf;
+    pl.mode = (int)L->pool;
     e = launch_pool(pl, s);
     if (e != hipSuccess) return hip_fail(e, "pool launch");
 
@@ -527,6 +599,32 @@ int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms) {
   return PINSAGE_OK;
 }
 
+int pinsage_output_mlp_workspace_size(const pinsage_mlp_t* mlp, int64_t n, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_mlp(mlp);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  if (n < 0) return fail(PINSAGE_EINVAL, "negative row count");
+  *bytes = mlp_ws(mlp, n);
+  return PINSAGE_OK;
+}
+
+int pinsage_output_mlp(const pinsage_mlp_t* mlp, const void* h, int64_t n, void* z,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int st = check_mlp(mlp);
+  if (st) return st;
+  if (n < 0) return fail(PINSAGE_EINVAL, "negative row count");
+  if (n == 0) return PINSAGE_OK;
+  if (!h || !z) return fail(PINSAGE_EINVAL, "h or z is NULL");
+  const size_t need = mlp_ws(mlp, n);
+  if (!workspace || workspace_bytes < need)
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
+  return run_mlp(mlp, h, nullptr, n, n, z, workspace, static_cast<hipStream_t>(stream));
+}
+
 int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
                             int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
                             float* loss, float* per_pair, void* stream) {
@@ -565,7 +663,7 @@ struct MbPlan {
   int K = 0, T = 0;
   int64_t N = 0;
   int64_t U[kMaxMinibatchLayers + 1] = {};  // frontier capacity per level
-  size_t flags = 0, pos = 0, tiles = 0, ctr = 0, rows = 0, pp = 0, conv = 0;
+  size_t flags = 0, pos = 0, tiles = 0, ctr = 0, rows = 0, pp = 0, conv = 0, z = 0, mlp = 0;
   size_t set[kMaxMinibatchLayers + 1] = {};
   size_t nidx[kMaxMinibatchLayers + 1] = {}, ncnt[kMaxMinibatchLayers + 1] = {},
          nw[kMaxMinibatchLayers + 1] = {}, self[kMaxMinibatchLayers + 1] = {},
@@ -574,7 +672,8 @@ struct MbPlan {
 };
 
 int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
-              const pinsage_layer_t* layers, int K, int64_t B, int64_t n_neg, MbPlan* p) {
+              const pinsage_layer_t* layers, int K, const pinsage_mlp_t* mlp, int64_t B,
+              int64_t n_neg, MbPlan* p) {
   const int64_t N = g->num_pins + g->num_boards;
   p->K = K;
   p->T = w->top_t;
@@ -612,13 +711,17 @@ int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
     conv = c > conv ? c : conv;
   }
   p->conv = take(conv);
-
+  if (mlp) {  // z of the targets' set, and the hidden activations of the output layers
+    p->z = take((size_t)p->U[K] * mlp->d_out * elem_size(mlp->dtype));
+    p->mlp = take(mlp_ws(mlp, p->U[K]));
+  }
   p->total = cur;
   return PINSAGE_OK;
 }
 
 int check_minibatch(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
-                    const pinsage_layer_t* layers, int32_t K, int64_t B, int64_t n_neg) {
+                    const pinsage_layer_t* layers, int32_t K, const pinsage_mlp_t* mlp,
+                    int64_t B, int64_t n_neg) {
   int st = check_graph(graph);
   if (st) return st;
   if ((st = check_walk(walk))) return st;
@@ -632,8 +735,15 @@ int check_minibatch(const pinsage_graph_t* graph, const pinsage_walk_params_t* w
       return fail(PINSAGE_EINVAL, "layer %d d_in %d != layer %d d_out %d", k, layers[k].d_in,
                   k - 1, layers[k - 1].d_out);
   }
-  if (layers[K - 1].d_out > 1024)
-    return fail(PINSAGE_EUNSUPPORTED, "last layer d_out %d > 1024", layers[K - 1].d_out);
+  if (mlp) {
+    if ((st = check_mlp(mlp))) return st;
+    if (mlp->d_in != layers[K - 1].d_out)
+      return fail(PINSAGE_EINVAL, "mlp d_in %d != last layer d_out %d", mlp->d_in,
+                  layers[K - 1].d_out);
+    if (mlp->dtype != layers[0].dtype) return fail(PINSAGE_EINVAL, "mlp dtype differs from layers");
+  }
+  const int d = mlp ? mlp->d_out : layers[K - 1].d_out;
+  if (d > 1024) return fail(PINSAGE_EUNSUPPORTED, "output dim %d > 1024", d);
   if (B < 1 || n_neg < 1) return fail(PINSAGE_EINVAL, "need num_pairs >= 1 and num_negatives >= 1");
   return PINSAGE_OK;
 }
@@ -654,19 +764,21 @@ extern "C" {
 int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_walk_params_t* walk,
                                      const pinsage_layer_t* layers, int32_t num_layers,
-                                     int64_t num_pairs, int64_t num_negatives, size_t* bytes) {
+                                     const pinsage_mlp_t* mlp, int64_t num_pairs,
+                                     int64_t num_negatives, size_t* bytes) {
   g_last_error.clear();
-  int st = check_minibatch(graph, walk, layers, num_layers, num_pairs, num_negatives);
+  int st = check_minibatch(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives);
   if (st) return st;
   if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
   MbPlan p;
-  make_plan(graph, walk, layers, num_layers, num_pairs, num_negatives, &p);
+  make_plan(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives, &p);
   *bytes = p.total;
   return PINSAGE_OK;
 }
 
 int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
-                              const pinsage_layer_t* layers, int32_t num_layers, const void* x,
+                              const pinsage_layer_t* layers, int32_t num_layers,
+                              const pinsage_mlp_t* mlp, const void* x,
                               const pinsage_pairs_t* pairs, float* loss, float* per_pair,
                               void* z_out, int64_t* set_sizes, void* workspace,
                               size_t workspace_bytes, void* stream) {
@@ -674,13 +786,13 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
   if (!pairs) return fail(PINSAGE_EINVAL, "pairs is NULL");
   const int64_t B = pairs->num_pairs, n_neg = pairs->num_negatives;
   const int K = num_layers;
-  int st = check_minibatch(graph, walk, layers, K, B, n_neg);
+  int st = check_minibatch(graph, walk, layers, K, mlp, B, n_neg);
   if (st) return st;
   if (!pairs->queries || !pairs->positives || !pairs->negatives)
     return fail(PINSAGE_EINVAL, "pair id arrays must not be NULL");
   if (!x || !loss) return fail(PINSAGE_EINVAL, "x or loss is NULL");
   MbPlan p;
-  make_plan(graph, walk, layers, K, B, n_neg, &p);
+  make_plan(graph, walk, layers, K, mlp, B, n_neg, &p);
   if (!workspace || workspace_bytes < p.total)
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes,
                 p.total);
@@ -783,26 +895,35 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
     if (st) return st;
   }
 
-  // Eq. (1) on h^(K), rows looked up through the level-K positions.
+  // Output dense layers (Algorithm 2, final loop) on every row of S^(K).
   const pinsage_layer_t* LK = &layers[K - 1];
+  const unsigned char* zsrc = ws + p.h[K];
+  int d = LK->d_out;
+  if (mlp) {
+    if ((st = run_mlp(mlp, ws + p.h[K], nullptr, size[K], size[K], ws + p.z, ws + p.mlp, s)))
+      return st;
+    zsrc = ws + p.z;
+    d = mlp->d_out;
+  }
+  // Eq. (1) on z, rows looked up through the level-K positions.
   LossLaunch la{};
-  la.zq = ws + p.h[K];
+  la.zq = zsrc;
   la.q_rows = rows;
-  la.zpos = ws + p.h[K];
+  la.zpos = zsrc;
   la.pos_rows = rows + B;
-  la.zneg = ws + p.h[K];
+  la.zneg = zsrc;
   la.neg_rows = rows + 2 * B;
   la.B = B;
   la.n_neg = n_neg;
-  la.d = LK->d_out;
+  la.d = d;
   la.bf16 = LK->dtype == PINSAGE_BF16;
   la.margin = pairs->margin;
   la.per_pair = per_pair ? per_pair : reinterpret_cast<float*>(ws + p.pp);
   la.loss = loss;
   PINSAGE_TRY(launch_loss(la, s), "loss launch");
   if (z_out)
-    PINSAGE_TRY(launch_gather_rows(ws + p.h[K], rows, 2 * B + n_neg,
-                                   (int64_t)LK->d_out * elem_size(LK->dtype), z_out, s),
+    PINSAGE_TRY(launch_gather_rows(zsrc, rows, 2 * B + n_neg,
+                                   (int64_t)d * elem_size(LK->dtype), z_out, s),
                 "target gather");
   if (set_sizes)
     for (int k = 0; k <= K; ++k) set_sizes[k] = size[k];

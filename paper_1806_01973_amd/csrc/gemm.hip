@@ -714,7 +714,7 @@ hipError_t launch_typed(const GemmLaunch& a, hipStream_t s) {
 
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  ProfileScope prof(a.l2norm ? kKGemmW : (a.relu ? kKGemmQ : kKGemmR), s);
+  ProfileScope prof(a.prof_class >= 0 ? a.prof_class : (a.l2norm ? kKGemmW : (a.relu ? kKGemmQ : kKGemmR)), s);
 #ifndef PINSAGE_GEMM_NO_RS
   if (use_rs(a)) return launch_rs(a, s);
 #endif

@@ -9,7 +9,7 @@ namespace pinsage {
 
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
-                   kKGemmR = 6, kKCount = 7 };
+                   kKGemmR = 6, kKMlp = 7, kKCount = 8 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -43,8 +43,12 @@ struct WalkLaunch {
 hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
 
 
-// n[r] = sum_t alpha[r][t] * P[idx[r][t]] for rows [0, rows) of the given
-// neighbourhood slice; storage dtype bf16 when bf16 is true.
+// Pooling modes (values match pinsage_pool_t).
+enum PoolMode { kPoolImportance = 0, kPoolMean = 1, kPoolMax = 2 };
+
+// n[r] = sum_t alpha[r][t] * P[idx[r][t]] (importance), the mean, or the
+// element-wise max of the P rows of rows [0, rows) of the given neighbourhood
+// slice; storage dtype bf16 when bf16 is true.
 struct PoolLaunch {
   const void* P;
   int64_t n_transform;
@@ -56,6 +60,7 @@ struct PoolLaunch {
   int T;
   int64_t rows;
   void* out;
+  int mode;  // PoolMode
 };
 hipError_t launch_pool(const PoolLaunch& a, hipStream_t s);
 
@@ -84,6 +89,7 @@ struct GemmLaunch {
   bool bf16;
   bool relu;
   bool l2norm;
+  int prof_class = -1;  // KernelClass for timing; -1: inferred from the epilogue
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
 

@@ -1,7 +1,9 @@
-// Importance pooling on gfx950 (Sec. 3.2: gamma is the weighted mean of the
-// transformed neighbour vectors, weighted by the L1-normalised visit counts;
-// Algorithm 1, line 1 applied as a gather over the once-per-node projections
-// of Sec. 3.4):  n[r] = sum_t alpha[r][t] * P[idx[r][t]].
+// Neighbourhood pooling on gfx950 (Algorithm 1, line 1 applied as a gather
+// over the once-per-node projections of Sec. 3.4). Importance pooling
+// (Sec. 3.2: gamma is the weighted mean of the transformed neighbour vectors,
+// weighted by the L1-normalised visit counts):
+//   n[r] = sum_t alpha[r][t] * P[idx[r][t]];
+// and the gamma = mean and gamma = max variants compared in Sec. 4.
 //
 // One wavefront per output row (grid-stride). The row's idx/weights are
 // wave-uniform and come through the scalar cache; each lane owns VEC
@@ -50,9 +52,39 @@ struct Vec<true> {  // 8 x bf16 = 16 B per lane
   }
 };
 
+// Per-row setup shared by both kernels: the weight sum S of a row without
+// stored weights (importance pooling derives alpha = count / S) or the number
+// of neighbours (mean pooling), counted by the lanes in parallel; integers, so
+// the order does not matter.
+__device__ __forceinline__ int row_total(const PoolLaunch& a, int64_t row, int lane) {
+  const int T = a.T;
+  int part = 0;
+  if (a.mode == kPoolMean) {
+    for (int t = lane; t < T; t += kWave) {
+      const int32_t v = a.idx[row * T + t];
+      part += ((uint64_t)(int64_t)v < (uint64_t)a.n_transform) ? 1 : 0;
+    }
+  } else if (a.mode == kPoolImportance && !a.weights) {
+    for (int t = lane; t < T; t += kWave) part += a.counts[row * T + t];
+  } else {
+    return 0;
+  }
+  return wave_sum_i32(part);
+}
+
+// Weight of neighbour slot t of a row (importance or mean pooling).
+template <int MODE>
+__device__ __forceinline__ float slot_alpha(const PoolLaunch& a, int64_t row, int t, int total) {
+  if constexpr (MODE == kPoolMean) return 1.0f / (float)total;
+  if (a.weights) return a.weights[row * a.T + t];
+  return (float)a.counts[row * a.T + t] / (float)total;
+}
+
 // J = number of 64*VEC-column slabs per row (compile time); U neighbour rows
-// are in flight per wave (U*J 16-byte loads per lane).
-template <bool BF16, int J, int U = (J <= 2 ? 8 : (J <= 4 ? 4 : (J <= 8 ? 2 : 1)))>
+// are in flight per wave (U*J 16-byte loads per lane). MODE: importance
+// (weighted sum), mean (uniform weights 1/#neighbours) or max (element-wise,
+// skipped slots do not take part; an empty row gives zeros).
+template <bool BF16, int MODE, int J, int U = (J <= 2 ? 8 : (J <= 4 ? 4 : (J <= 8 ? 2 : 1)))>
 __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
   using V = Vec<BF16>;
   using Raw = typename V::Raw;
@@ -69,35 +101,27 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
        row0 += (int64_t)gridDim.x * kWavesPerBlock) {
     const int64_t row = row0;
     const int32_t* __restrict__ ridx = a.idx + row * T;
-    // Without stored weights, alpha = count / (sum of the row's counts): the
-    // lanes load the counts in parallel and the wave adds them (integers, so
-    // the order does not matter).
-    int total = 0;
-    if (!a.weights) {
-      int part = 0;
-      for (int t = lane; t < T; t += kWave) part += a.counts[row * T + t];
-      total = wave_sum_i32(part);
-    }
+    const int total = row_total(a, row, lane);
     float acc[J][VN];
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
-      for (int v = 0; v < VN; ++v) acc[j][v] = 0.0f;
+      for (int v = 0; v < VN; ++v) acc[j][v] = MODE == kPoolMax ? -INFINITY : 0.0f;
+    bool any = false;
 
     for (int t0 = 0; t0 < T; t0 += U) {
       Raw buf[U][J];
       float alpha[U];
+      bool ok[U];
 #pragma unroll
       for (int i = 0; i < U; ++i) {
         const int t = t0 + i;
         int32_t v = t < T ? ridx[t] : -1;
         if ((uint64_t)(int64_t)v >= (uint64_t)a.n_transform) v = -1;
-        float al = 0.0f;
-        if (v >= 0) {
-          if (a.weights) al = a.weights[row * T + t];
-          else al = (float)a.counts[row * T + t] / (float)total;
-        }
-        alpha[i] = (v >= 0) ? al : 0.0f;
+        ok[i] = v >= 0;
+        alpha[i] = 0.0f;
+        if constexpr (MODE != kPoolMax)
+          if (v >= 0) alpha[i] = slot_alpha<MODE>(a, row, t, total);
 #pragma unroll
         for (int j = 0; j < J; ++j) {
           const int c = j * kWave + lane;
@@ -107,18 +131,25 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
       }
 #pragma unroll
       for (int i = 0; i < U; ++i) {
+        any = any || ok[i];
 #pragma unroll
         for (int j = 0; j < J; ++j) {
           float f[VN];
           V::to_f32(buf[i][j], f);
 #pragma unroll
-          for (int v = 0; v < VN; ++v) acc[j][v] = fmaf(alpha[i], f[v], acc[j][v]);
+          for (int v = 0; v < VN; ++v) {
+            if constexpr (MODE == kPoolMax) acc[j][v] = ok[i] ? fmaxf(acc[j][v], f[v]) : acc[j][v];
+            else acc[j][v] = fmaf(alpha[i], f[v], acc[j][v]);
+          }
         }
       }
     }
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int c = j * kWave + lane;
+      if constexpr (MODE == kPoolMax)
+#pragma unroll
+        for (int v = 0; v < VN; ++v) acc[j][v] = any ? acc[j][v] : 0.0f;
       if (c < vec_per_row) out[row * vec_per_row + c] = V::from_f32(acc[j]);
     }
   }
@@ -127,11 +158,11 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
 // Rows narrower than one wave slab (at most 64 / RG vectors): the wave splits
 // into RG lane groups of 64 / RG lanes, group g gathering neighbours
 // t = g, g + RG, ... of the row, so one load instruction reads RG rows. Each
-// group sums its neighbours in rank order; the RG partial sums are then added
-// by a fixed butterfly over the groups (the same order on every lane). U = 4
-// loads in flight per lane: on 512-byte rows, 8 and 16 measured 5% and 40%
-// slower (fewer resident waves).
-template <bool BF16, int RG, int U = 4>
+// group reduces its neighbours in rank order; the RG partial results are then
+// combined by a fixed butterfly over the groups (the same order on every
+// lane). U = 4 loads in flight per lane: on 512-byte rows, 8 and 16 measured
+// 5% and 40% slower (fewer resident waves).
+template <bool BF16, int MODE, int RG, int U = 4>
 __global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
   using V = Vec<BF16>;
   using Raw = typename V::Raw;
@@ -149,49 +180,57 @@ __global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
   for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < a.rows;
        row += (int64_t)gridDim.x * kWavesPerBlock) {
     const int32_t* __restrict__ ridx = a.idx + row * T;
-    int total = 0;
-    if (!a.weights) {
-      int part = 0;
-      for (int t = lane; t < T; t += kWave) part += a.counts[row * T + t];
-      total = wave_sum_i32(part);
-    }
+    const int total = row_total(a, row, lane);
     float acc[VN];
 #pragma unroll
-    for (int v = 0; v < VN; ++v) acc[v] = 0.0f;
+    for (int v = 0; v < VN; ++v) acc[v] = MODE == kPoolMax ? -INFINITY : 0.0f;
+    bool any = false;
     for (int t0 = 0; t0 < T; t0 += U * RG) {
       Raw buf[U];
       float alpha[U];
+      bool ok[U];
 #pragma unroll
       for (int i = 0; i < U; ++i) {
         const int t = t0 + i * RG + grp;
         int32_t v = t < T ? ridx[t] : -1;
         if ((uint64_t)(int64_t)v >= (uint64_t)a.n_transform) v = -1;
-        float al = 0.0f;
-        if (v >= 0) {
-          if (a.weights) al = a.weights[row * T + t];
-          else al = (float)a.counts[row * T + t] / (float)total;
-        }
-        alpha[i] = al;
+        ok[i] = v >= 0;
+        alpha[i] = 0.0f;
+        if constexpr (MODE != kPoolMax)
+          if (v >= 0) alpha[i] = slot_alpha<MODE>(a, row, t, total);
         buf[i] = (v >= 0 && col_ok) ? P[(int64_t)v * vec_per_row + c] : Raw{};
       }
 #pragma unroll
       for (int i = 0; i < U; ++i) {
+        any = any || ok[i];
         float f[VN];
         V::to_f32(buf[i], f);
 #pragma unroll
-        for (int v = 0; v < VN; ++v) acc[v] = fmaf(alpha[i], f[v], acc[v]);
+        for (int v = 0; v < VN; ++v) {
+          if constexpr (MODE == kPoolMax) acc[v] = ok[i] ? fmaxf(acc[v], f[v]) : acc[v];
+          else acc[v] = fmaf(alpha[i], f[v], acc[v]);
+        }
       }
     }
 #pragma unroll
     for (int o = GL; o < kWave; o <<= 1)
 #pragma unroll
-      for (int v = 0; v < VN; ++v) acc[v] += __shfl_xor(acc[v], o);
+      for (int v = 0; v < VN; ++v) {
+        const float other = __shfl_xor(acc[v], o);
+        acc[v] = MODE == kPoolMax ? fmaxf(acc[v], other) : acc[v] + other;
+      }
+    if constexpr (MODE == kPoolMax) {
+      // `any` of the whole row: some group saw a neighbour.
+      const bool row_any = __builtin_amdgcn_readfirstlane(wave_sum_i32(any ? 1 : 0)) > 0;
+#pragma unroll
+      for (int v = 0; v < VN; ++v) acc[v] = row_any ? acc[v] : 0.0f;
+    }
     if (grp == 0 && col_ok) out[row * vec_per_row + c] = V::from_f32(acc);
   }
 }
 
-template <bool BF16>
-hipError_t launch_typed(const PoolLaunch& a, hipStream_t s) {
+template <bool BF16, int MODE>
+hipError_t launch_mode(const PoolLaunch& a, hipStream_t s) {
   constexpr int VN = BF16 ? 8 : 4;
   const int slabs = (a.m / VN + kWave - 1) / kWave;
   const int64_t blocks_needed = (a.rows + kWavesPerBlock - 1) / kWavesPerBlock;
@@ -200,17 +239,27 @@ hipError_t launch_typed(const PoolLaunch& a, hipStream_t s) {
   const dim3 block(256);
   const int vec_per_row = a.m / VN;
   if (vec_per_row <= kWave / 4)
-    hipLaunchKernelGGL((pool_narrow_kernel<BF16, 4>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((pool_narrow_kernel<BF16, MODE, 4>), grid, block, 0, s, a);
   else if (vec_per_row <= kWave / 2)
-    hipLaunchKernelGGL((pool_narrow_kernel<BF16, 2>), grid, block, 0, s, a);
-  else if (slabs <= 1) hipLaunchKernelGGL((pool_kernel<BF16, 1>), grid, block, 0, s, a);
-  else if (slabs <= 2) hipLaunchKernelGGL((pool_kernel<BF16, 2>), grid, block, 0, s, a);
-  else if (slabs <= 4) hipLaunchKernelGGL((pool_kernel<BF16, 4>), grid, block, 0, s, a);
-  else if (slabs <= 8) hipLaunchKernelGGL((pool_kernel<BF16, 8>), grid, block, 0, s, a);
-  else if (slabs <= 16) hipLaunchKernelGGL((pool_kernel<BF16, 16>), grid, block, 0, s, a);
-  else if (slabs <= 32) hipLaunchKernelGGL((pool_kernel<BF16, 32>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((pool_narrow_kernel<BF16, MODE, 2>), grid, block, 0, s, a);
+  else if (slabs <= 1) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 1>), grid, block, 0, s, a);
+  else if (slabs <= 2) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 2>), grid, block, 0, s, a);
+  else if (slabs <= 4) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 4>), grid, block, 0, s, a);
+  else if (slabs <= 8) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 8>), grid, block, 0, s, a);
+  else if (slabs <= 16) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 16>), grid, block, 0, s, a);
+  else if (slabs <= 32) hipLaunchKernelGGL((pool_kernel<BF16, MODE, 32>), grid, block, 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t launch_typed(const PoolLaunch& a, hipStream_t s) {
+  switch (a.mode) {
+    case kPoolImportance: return launch_mode<BF16, kPoolImportance>(a, s);
+    case kPoolMean: return launch_mode<BF16, kPoolMean>(a, s);
+    case kPoolMax: return launch_mode<BF16, kPoolMax>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace

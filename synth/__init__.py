@@ -1,7 +1,7 @@
 """Seeded synthetic inputs for the PinSage hot path.
 
 This module only draws inputs: a bipartite pin-board graph in CSR form, node
-features and layer parameters. It holds none of the method's arithmetic
+features and layer (and output-layer) parameters. It holds none of the method's arithmetic
 (no walks, no pooling, no layers), so both the GPU library's tests and the CPU
 oracle can consume the same inputs without sharing any computation.
 
@@ -14,6 +14,7 @@ from .graphs import (  # noqa: F401
     WORKLOADS,
     make_graph,
     make_layers,
+    make_mlp,
     make_features,
     make_workload,
     bf16_round,

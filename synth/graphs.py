@@ -201,6 +201,21 @@ def make_layers(wl: Workload, seed_offset: int = 0) -> List[dict]:
     return layers
 
 
+def make_mlp(d_in: int, d_hidden: int, d_out: int, seed: int, dtype: str = "f32") -> dict:
+    """Output dense layers (G1 [d_hidden, d_in], g [d_hidden], G2 [d_out, d_hidden])
+    as fp32 numpy: Glorot-uniform matrices, g ~ U(-0.1, 0.1); G1 and G2 rounded to
+    bf16 for bf16 storage."""
+    rng = np.random.default_rng([seed, 5])
+    a1 = math.sqrt(6.0 / (d_in + d_hidden))
+    a2 = math.sqrt(6.0 / (d_hidden + d_out))
+    G1 = rng.uniform(-a1, a1, size=(d_hidden, d_in)).astype(np.float32)
+    g = rng.uniform(-0.1, 0.1, size=d_hidden).astype(np.float32)
+    G2 = rng.uniform(-a2, a2, size=(d_out, d_hidden)).astype(np.float32)
+    if dtype == "bf16":
+        G1, G2 = bf16_round(G1), bf16_round(G2)
+    return {"G1": G1, "g": g, "G2": G2}
+
+
 def make_workload(wl: Workload):
     """Full input bundle: dict with offsets, col, num_edges, x, layers."""
     offsets, col, E = make_graph(wl)

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 2
+    assert lib.pinsage_version() == 3
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -101,7 +101,9 @@ def test_layer_validation_and_workspace_sizes(L):
     assert n.value == 25600 + 51200 + 76800
     for bad, code in [(dict(d_in=60), L.PINSAGE_EUNSUPPORTED), (dict(d_out=1024), L.PINSAGE_EUNSUPPORTED),
                       (dict(m=0), L.PINSAGE_EINVAL), (dict(Q=None), L.PINSAGE_EINVAL),
-                      (dict(dtype=5), L.PINSAGE_EINVAL), (dict(dataflow=2), L.PINSAGE_EINVAL)]:
+                      (dict(dtype=5), L.PINSAGE_EINVAL), (dict(dataflow=2), L.PINSAGE_EINVAL),
+                      (dict(pool=3), L.PINSAGE_EINVAL),
+                      (dict(pool=2, dataflow=1), L.PINSAGE_EUNSUPPORTED)]:
         b = _layer(L, **bad)
         assert lib.pinsage_convolve_workspace_size(ctypes.byref(b), 1, 1, ctypes.byref(n)) == code
     # Workspace too small: rejected before any launch.
@@ -154,7 +156,7 @@ def test_minibatch_validation_and_workspace(L):
     walk = L.WalkParams(1, 10, 2, 4)
     layers = (L.Layer * 2)(_layer(L), _layer(L))
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                3, 2, ctypes.byref(n)) == 0
+                                                None, 3, 2, ctypes.byref(n)) == 0
     # Frontier capacities: U2 = min(15, 2*3+2) = 8, U1 = U0 = 15 (capped by N).
     a = lambda b: (b + 255) // 256 * 256
     U = [15, 15, 8]
@@ -166,16 +168,16 @@ def test_minibatch_validation_and_workspace(L):
     want += a(conv)
     assert n.value == want
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                0, 2, ctypes.byref(n)) == L.PINSAGE_EINVAL
+                                                None, 0, 2, ctypes.byref(n)) == L.PINSAGE_EINVAL
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 9,
-                                                3, 2, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
+                                                None, 3, 2, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
     pairs = L.Pairs(3, 2, FAKE, None, FAKE, 0.1)
-    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
+    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
                                        ctypes.byref(pairs), FAKE, None, None, None, FAKE,
                                        1 << 30, None)
     assert st == L.PINSAGE_EINVAL
     pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1)
-    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
+    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
                                        ctypes.byref(pairs), FAKE, None, None, None, FAKE, 16, None)
     assert st == L.PINSAGE_EWORKSPACE
     # Standalone loss: per_pair is required, d is bounded.
@@ -186,3 +188,42 @@ def test_minibatch_validation_and_workspace(L):
                                      None)
     assert st == L.PINSAGE_EUNSUPPORTED
 
+
+def _mlp(L, **kw):
+    d = dict(d_in=64, d_hidden=96, d_out=32, dtype=L.PINSAGE_F32, G1=FAKE, g=FAKE, G2=FAKE)
+    d.update(kw)
+    return L.MLP(**d)
+
+
+def test_output_mlp_validation(L):
+    lib = L.lib()
+    n = ctypes.c_size_t(0)
+    m = _mlp(L)
+    assert lib.pinsage_output_mlp_workspace_size(ctypes.byref(m), 300, ctypes.byref(n)) == 0
+    assert n.value == 300 * 96 * 4 // 256 * 256 + (256 if 300 * 96 * 4 % 256 else 0)
+    for bad, code in [(dict(d_in=60), L.PINSAGE_EUNSUPPORTED), (dict(d_hidden=0), L.PINSAGE_EINVAL),
+                      (dict(G2=None), L.PINSAGE_EINVAL), (dict(dtype=9), L.PINSAGE_EINVAL),
+                      (dict(d_out=16384), L.PINSAGE_EUNSUPPORTED)]:
+        b = _mlp(L, **bad)
+        assert lib.pinsage_output_mlp_workspace_size(ctypes.byref(b), 1, ctypes.byref(n)) == code
+    assert lib.pinsage_output_mlp(ctypes.byref(m), FAKE, 300, FAKE, FAKE, 1024, None) == \
+        L.PINSAGE_EWORKSPACE
+    assert lib.pinsage_output_mlp(ctypes.byref(m), FAKE, 300, FAKE, FAKE + 8, 1 << 30, None) == \
+        L.PINSAGE_EINVAL
+    assert lib.pinsage_output_mlp(ctypes.byref(m), FAKE, 0, FAKE, None, 0, None) == 0
+    # Minibatch with output layers: d_in must match the last layer, dtype must match.
+    g = _graph(L)
+    walk = L.WalkParams(1, 10, 2, 4)
+    layers = (L.Layer * 2)(_layer(L), _layer(L))
+    bad = _mlp(L, d_in=32)
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                ctypes.byref(bad), 3, 2, ctypes.byref(n)) == \
+        L.PINSAGE_EINVAL
+    ok = _mlp(L, d_in=64)
+    n0 = ctypes.c_size_t(0)
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                None, 3, 2, ctypes.byref(n0)) == 0
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                ctypes.byref(ok), 3, 2, ctypes.byref(n)) == 0
+    a = lambda b: (b + 255) // 256 * 256
+    assert n.value == n0.value + a(8 * 32 * 4) + a(8 * 96 * 4)  # z and hidden rows of S^(2)

@@ -166,3 +166,84 @@ def test_profile_counts_launches(dataflow):
     assert prof["gemm_q"][0] == 2 and prof["pool"][0] == 2 and prof["gemm_w"][0] == 2
     assert prof["gemm_r"][0] == (2 if dataflow == "dense_then_pool" else 0)
     assert all(ms >= 0 for _, ms in prof.values())
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dims", [(64, 64, 64), (256, 512, 256), (128, 96, 512)])
+@pytest.mark.parametrize("pool,dataflow", [("mean", "pool_then_dense"), ("mean", "dense_then_pool"),
+                                           ("max", "pool_then_dense")])
+def test_convolve_layer_pool_modes(orc, dtype, dims, pool, dataflow):
+    # The gamma = mean / max aggregators of Sec. 4 (narrow- and wide-row pools).
+    import paper_1806_01973_amd as ps
+    d_in, m, d_out = dims
+    rng = np.random.default_rng(12)
+    n_in, n_transform, n_out, T = 2_501, 1_903, 1_401, 19
+    print(f"[case] convolve_layer pool={pool} {dataflow} {dtype} dims={dims}", flush=True)
+    h = rng.standard_normal((n_in, d_in)).astype(np.float32)
+    if dtype == "bf16":
+        h = synth.bf16_round(h)
+    wl = synth.Workload("layer", 1, 1, "uniform8", 0, 8, None, d_in, m, d_out, 1, 1, 1, T, dtype, 13)
+    layer = synth.make_layers(wl)[0]
+    idx, counts, weights = synth.random_neighborhoods(n_out, n_transform, T, seed=14)
+    self_rows = rng.integers(0, n_in, size=n_out).astype(np.int32)
+    dev = ps.DeviceLayer(layer["Q"], layer["q"], layer["W"], layer["w"], dtype=torch_dtype(dtype),
+                         dataflow=dataflow, pool=pool)
+    nb = ps.Neighborhoods(torch.as_tensor(idx).cuda(), torch.as_tensor(counts).cuda(),
+                          torch.as_tensor(weights).cuda())
+    hin = torch.as_tensor(h).to(device="cuda", dtype=torch_dtype(dtype))
+    out = ps.convolve_layer(dev, hin, n_transform, nb, self_rows=torch.as_tensor(self_rows).cuda())
+    torch.cuda.synchronize()
+    ref = orc.convolve_layer(h, n_transform, layer["Q"], layer["q"], layer["W"], layer["w"], idx,
+                             weights, self_rows=self_rows, pool=pool)
+    check_embeddings(to_f64(out), ref, dtype, f"pool={pool} {dataflow} {dtype} {dims}")
+
+
+def test_max_pool_rejects_dense_then_pool():
+    import paper_1806_01973_amd as ps
+    wl = synth.WORKLOADS["tiny"]
+    L = synth.make_layers(wl)[0]
+    dev = ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dataflow="dense_then_pool", pool="max")
+    nb = ps.Neighborhoods.empty(4, 3)
+    print("[case] max pool + dense_then_pool rejected", flush=True)
+    with pytest.raises(ps.PinsageError) as e:
+        ps.convolve_layer(dev, torch.zeros((10, 64), device="cuda"), 10, nb)
+    assert e.value.status == -2
+
+
+@pytest.mark.parametrize("pool", ["mean", "max"])
+def test_embed_all_pool_modes(orc, pool):
+    wl = synth.WORKLOADS["tiny"]
+    data = synth.make_workload(wl)
+    layers = [dict(L, pool=pool) for L in data["layers"]]
+    import paper_1806_01973_amd as ps
+    print(f"[case] embed_all tiny pool={pool}", flush=True)
+    g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
+    dl = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], pool=pool) for L in layers]
+    job = ps.EmbedAll(g, dl, wl.walks, wl.hops, wl.T, wl.seed)
+    out = job.run(torch.as_tensor(data["x"]).cuda())
+    torch.cuda.synchronize()
+    idx, cnt, wts, _ = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
+                                               wl.seed, wl.walks, wl.hops, wl.T)
+    ref = orc.embed_all(data["x"], wl.num_pins, layers, idx, wts)
+    check_embeddings(to_f64(out), ref, "f32", f"embed_all pool={pool}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dims,n", [((64, 96, 32), 777), ((256, 512, 256), 70_001),
+                                    ((512, 1024, 512), 9_999), ((16, 16, 16), 1)])
+def test_output_mlp(orc, dtype, dims, n):
+    # Algorithm 2's output layers, z = G2 ReLU(G1 h + g), several tiles and a ragged tail.
+    import paper_1806_01973_amd as ps
+    d_in, d_hidden, d_out = dims
+    print(f"[case] output mlp {dtype} dims={dims} n={n}", flush=True)
+    rng = np.random.default_rng(15)
+    h = rng.standard_normal((n, d_in)).astype(np.float32)
+    h /= np.linalg.norm(h, axis=1, keepdims=True)
+    if dtype == "bf16":
+        h = synth.bf16_round(h)
+    P = synth.make_mlp(d_in, d_hidden, d_out, seed=16, dtype=dtype)
+    mlp = ps.DeviceMLP(P["G1"], P["g"], P["G2"], dtype=torch_dtype(dtype))
+    z = ps.output_mlp(mlp, torch.as_tensor(h).to(device="cuda", dtype=torch_dtype(dtype)))
+    torch.cuda.synchronize()
+    ref = orc.output_mlp(h, P["G1"], P["g"], P["G2"])
+    check_embeddings(to_f64(z), ref, dtype, f"mlp {dtype} {dims}")

@@ -60,7 +60,8 @@ def _loss_bound(g, o, B, n_neg):
     return float((neg_term + pos_term).mean())
 
 
-def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0, dataflow="pool_then_dense"):
+def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0, dataflow="pool_then_dense",
+                   mlp=None):
     import paper_1806_01973_amd as ps
     q, p, n = synth.minibatch_pairs(wl, data["offsets"], data["col"], B, n_neg, seed=seed)
     g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
@@ -68,7 +69,9 @@ def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0, dataflow="pool_the
                              dataflow=dataflow)
               for L in data["layers"]]
     x = torch.as_tensor(data["x"]).to(device="cuda", dtype=torch_dtype(wl.dtype))
-    mb = ps.Minibatch(g, layers, wl.walks, wl.hops, wl.T, wl.seed, B, n_neg)
+    dmlp = None if mlp is None else ps.DeviceMLP(mlp["G1"], mlp["g"], mlp["G2"],
+                                                 dtype=torch_dtype(wl.dtype))
+    mb = ps.Minibatch(g, layers, wl.walks, wl.hops, wl.T, wl.seed, B, n_neg, mlp=dmlp)
     dq, dp, dn = (torch.as_tensor(a).cuda() for a in (q, p, n))
     mb.run(x, dq, dp, dn, 0.1)
     torch.cuda.synchronize()
@@ -83,6 +86,8 @@ def _run_minibatch(orc, wl, data, idx, wts, B, n_neg, seed=0, dataflow="pool_the
     ref_sets = orc.minibatch_sets(targets, wl.K, idx)
     assert sizes == [len(s) for s in ref_sets], (sizes, [len(s) for s in ref_sets])
     ref_z = orc.minibatch_embed(targets, data["x"], data["layers"], idx, wts)
+    if mlp is not None:
+        ref_z = orc.output_mlp(ref_z, mlp["G1"], mlp["g"], mlp["G2"])
     stats = check_embeddings(z, ref_z, wl.dtype, f"minibatch {wl.name}")
     ref_loss, ref_per = orc.max_margin_loss(ref_z[:B], ref_z[B:2 * B], ref_z[2 * B:], 0.1)
     bound = _loss_bound(z, ref_z, B, n_neg) + 1e-5
@@ -118,3 +123,16 @@ def test_minibatch_full(orc, medium_bundle, dataflow):
     sizes = _run_minibatch(orc, wl, data, b["idx"], b["wts"], B=2048, n_neg=500,
                            dataflow=dataflow)
     assert sizes[2] <= 2 * 2048 + 500 and sizes[1] > sizes[2] and sizes[0] > sizes[1]
+
+
+@pytest.mark.parametrize("dataflow", ["pool_then_dense", "dense_then_pool"])
+def test_minibatch_with_output_layers(orc, dataflow):
+    # Algorithm 2 in full: the K layers, then z = G2 ReLU(G1 h + g), and the
+    # loss of Eq. 1 on z.
+    wl = synth.WORKLOADS["tiny"]
+    data = synth.make_workload(wl)
+    idx, cnt, wts, _ = orc.build_neighborhoods(data["offsets"], data["col"], wl.num_pins,
+                                               wl.seed, wl.walks, wl.hops, wl.T)
+    mlp = synth.make_mlp(wl.d_out, 96, 48, seed=17)
+    print(f"[case] minibatch tiny with output layers {dataflow}", flush=True)
+    _run_minibatch(orc, wl, data, idx, wts, B=64, n_neg=20, dataflow=dataflow, mlp=mlp)
