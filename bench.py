@@ -81,7 +81,7 @@ def copy_calibration(gib: float = 1.0, reps: int = 5) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
 
 
-def load_inputs(wl, dataflow="pool_then_dense"):
+def load_inputs(wl, dataflow="pool_then_dense", pool="importance"):
     """Inputs on the GPU plus host views the CPU baseline needs."""
     import numpy as np
     import torch
@@ -105,8 +105,8 @@ def load_inputs(wl, dataflow="pool_then_dense"):
         x_rows = lambda n: data["x"][:n]
     layers_np = synth.make_layers(wl)
     g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards, offsets64=wl.offsets64)
-    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt, dataflow=dataflow)
-              for L in layers_np]
+    layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=tdt, dataflow=dataflow,
+                             pool=pool) for L in layers_np]
     torch.cuda.synchronize()
     log(f"inputs for {wl.name}: {wl.num_nodes} nodes, {E} edges in "
         f"{time.perf_counter() - t0:.1f}s")
@@ -251,7 +251,18 @@ def bench_embed_all(args, wl, inp):
     job = ps.EmbedAll(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed,
                       weights=wl.name != "shard")
     stream = torch.cuda.current_stream()
-    elapsed, prof = timed(lambda i: job.run(inp["x"], stream), args.steps, args.warmup)
+    mlp = inp.get("mlp")
+    if mlp is not None:
+        z = torch.empty((wl.num_nodes, mlp.d_out), dtype=mlp.dtype, device="cuda")
+        mws = torch.empty(max(1, mlp_workspace(mlp, wl.num_nodes)), dtype=torch.uint8,
+                          device="cuda")
+
+    def step(i):
+        h = job.run(inp["x"], stream)
+        if mlp is not None:
+            ps.output_mlp(mlp, h, out=z, workspace=mws, stream=stream)
+
+    elapsed, prof = timed(step, args.steps, args.warmup)
     N = wl.num_nodes
     walk_steps = int(job.steps.item())
     kernels = kernel_table(prof, args.steps)
@@ -266,8 +277,8 @@ def bench_embed_all(args, wl, inp):
         # The other evaluation order of the same layers, timed the same way
         # (same inputs, same steps), for comparison only.
         other = "pool_then_dense" if args.dataflow == "dense_then_pool" else "dense_then_pool"
-        alt_layers = [ps.DeviceLayer(L.Q, L.q, L.W, L.w, dtype=L.dtype, dataflow=other)
-                      for L in inp["layers"]]
+        alt_layers = [ps.DeviceLayer(L.Q, L.q, L.W, L.w, dtype=L.dtype, dataflow=other,
+                                     pool=L.pool) for L in inp["layers"]]
         del job
         torch.cuda.empty_cache()
         alt = ps.EmbedAll(inp["g"], alt_layers, wl.walks, wl.hops, wl.T, wl.seed,
@@ -278,7 +289,28 @@ def bench_embed_all(args, wl, inp):
     return value, "node embeddings/s", METRIC, elapsed, kernels, extra
 
 
+def mlp_workspace(mlp, n):
+    import ctypes
+
+    from paper_1806_01973_amd import _lib
+    need = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().pinsage_output_mlp_workspace_size(ctypes.byref(mlp.struct()), n,
+                                                            ctypes.byref(need)),
+               "pinsage_output_mlp_workspace_size")
+    return int(need.value)
+
+
+def ps_mlp(P, wl):
+    import torch
+
+    import paper_1806_01973_amd as ps
+    return ps.DeviceMLP(P["G1"], P["g"], P["G2"],
+                        dtype=torch.bfloat16 if wl.dtype == "bf16" else torch.float32)
+
+
 def compare_dataflow(args, wl) -> bool:
+    if args.pool == "max":
+        return False  # max pooling has one order only
     if args.compare_dataflow == "auto":
         return wl.name in ("tiny", "medium")
     return args.compare_dataflow == "on"
@@ -295,7 +327,8 @@ def bench_minibatch(args, wl, inp):
     sets = [synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], B, n_neg,
                                   seed=i) for i in range(total)]
     dev = [[torch.as_tensor(a).cuda() for a in s] for s in sets]
-    mb = ps.Minibatch(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed, B, n_neg)
+    mb = ps.Minibatch(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed, B, n_neg,
+                      mlp=inp.get("mlp"))
     stream = torch.cuda.current_stream()
     sizes = []
 
@@ -397,6 +430,10 @@ def main() -> int:
                     help="layer evaluation order (same values; see pinsage_dataflow_t)")
     ap.add_argument("--compare-dataflow", default="auto", choices=["auto", "on", "off"],
                     help="also time the other evaluation order (auto: small workloads)")
+    ap.add_argument("--pool", default="importance", choices=["importance", "mean", "max"],
+                    help="aggregator of every layer (max implies the pool-then-dense order)")
+    ap.add_argument("--mlp", type=int, default=0, metavar="D_HIDDEN",
+                    help="append the output dense layers z = G2 ReLU(G1 h + g) to the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layer", default=None,
                     help="d_in,m,d_out: time one layer on random inputs instead of a workload")
@@ -423,7 +460,13 @@ def main() -> int:
     wl = synth.WORKLOADS[args.workload]
     args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[wl.name]
     args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[wl.name]
-    inp = load_inputs(wl, args.dataflow)
+    if args.pool == "max" and args.dataflow == "dense_then_pool":
+        args.dataflow = "pool_then_dense"  # max pooling is not linear
+    inp = load_inputs(wl, args.dataflow, args.pool)
+    if args.mlp:
+        import synth as _s
+        P = _s.make_mlp(wl.d_out, args.mlp, wl.d_out, seed=wl.seed, dtype=wl.dtype)
+        inp["mlp"] = ps_mlp(P, wl)
     if wl.name == "minibatch":
         value, unit, metric, elapsed, kernels, extra = bench_minibatch(args, wl, inp)
     else:
@@ -445,8 +488,11 @@ def main() -> int:
         "config": {"workload": f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
                                f"{inp['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
                                f"T={wl.T}, K={wl.K}, dims {wl.d_in}->{wl.m}->{wl.d_out} "
-                               f"{wl.dtype}, layer dataflow {args.dataflow}",
-                   "dataflow": args.dataflow,
+                               f"{wl.dtype}, layer dataflow {args.dataflow}"
+                               + (f", pool {args.pool}" if args.pool != "importance" else "")
+                               + (f", output layers {wl.d_out}->{args.mlp}->{wl.d_out}"
+                                  if args.mlp else ""),
+                   "dataflow": args.dataflow, "pool": args.pool, "output_layers": args.mlp or None,
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
         "walk_steps_per_s": extra["walk_steps_per_s"],
