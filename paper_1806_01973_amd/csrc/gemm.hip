@@ -422,23 +422,33 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
 // write one row and the rows read by one fragment instruction both fall on
 // distinct banks. Missing rows and the K tail load from the zero row.
 // ---------------------------------------------------------------------------
-namespace rs {
-constexpr int BM = 256, BN = 256, BK = 64, THREADS = 256;
-constexpr int ROWS = BM + BN;            // rows of a stage (A rows, then B rows)
-constexpr int ROW_BYTES = BK * 2;        // 128
-constexpr int STAGE_BYTES = ROWS * ROW_BYTES;  // 64 KB
-constexpr int LOADS = ROWS * (ROW_BYTES / 16) / THREADS;  // 16 vectors per thread per chunk
-constexpr int TM = 4, TN = 4;            // 32 x 32 blocks per wave
-}  // namespace rs
+template <int WAVES_M_, int WAVES_N_>
+struct RsCfg {
+  static constexpr int BM = 256, BN = 256, BK = 64;
+  static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, NW = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int ROWS = BM + BN;                 // rows of a stage (A rows, then B rows)
+  static constexpr int ROW_BYTES = BK * 2;             // 128
+  static constexpr int STAGE_BYTES = ROWS * ROW_BYTES; // 64 KB
+  static constexpr int RSTEP = THREADS / 8;            // stage rows per block load instruction
+  static constexpr int LOADS = ROWS / RSTEP;           // 16-byte vectors per thread per chunk
+  static constexpr int SLICE = LOADS / 4;              // loads (and stores) per k-step
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  static constexpr int TM = WM / 32, TN = WN / 32;     // 32 x 32 blocks per wave
+  static_assert(LOADS % 4 == 0 && TM * TN >= TM + TN + 2, "k-step interleave pattern");
+};
 
-__global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
-  using namespace rs;
+template <typename C>
+__global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, THREADS = C::THREADS;
+  constexpr int ROW_BYTES = C::ROW_BYTES, STAGE_BYTES = C::STAGE_BYTES, RSTEP = C::RSTEP;
+  constexpr int LOADS = C::LOADS, SLICE = C::SLICE, TM = C::TM, TN = C::TN;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE_BYTES + BN * 4];
   float* bias_s = reinterpret_cast<float*>(smem + 2 * STAGE_BYTES);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
 
   // Tile coordinates are wave-uniform; readfirstlane keeps them (and the
   // buffer descriptors built from them) in scalar registers.
@@ -451,8 +461,9 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   for (int c = tid; c < BN; c += THREADS)
     bias_s[c] = (a.bias && n0 + c < a.N) ? a.bias[n0 + c] : 0.0f;
 
-  // Load slot i of this thread: stage row (tid >> 3) + 32 i (A rows for
-  // i < 8, B rows after), 16-byte vector tid & 7 of the row's chunk. Loads go
+  // Load slot i of this thread: stage row (tid >> 3) + RSTEP i (A rows for
+  // i < LOADS / 2, B rows after), 16-byte vector tid & 7 of the row's chunk.
+  // Loads go
   // through buffer descriptors spanning the rows of this tile that exist, so
   // missing rows read zeros; the K tail takes an offset past every
   // descriptor's range (also zeros). No load is behind a branch.
@@ -468,8 +479,8 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<unsigned char*>(static_cast<const unsigned char*>(a.B)) + (int64_t)n0 * a.ldb * 2,
       (short)0, b_bytes, 0x00020000);
-  const int a_off0 = r0 * (int)a.lda0 * 2 + v * 16, a_step = 32 * (int)a.lda0 * 2;
-  const int b_off0 = r0 * (int)a.ldb * 2 + v * 16, b_step = 32 * (int)a.ldb * 2;
+  const int a_off0 = r0 * (int)a.lda0 * 2 + v * 16, a_step = RSTEP * (int)a.lda0 * 2;
+  const int b_off0 = r0 * (int)a.ldb * 2 + v * 16, b_step = RSTEP * (int)a.ldb * 2;
   const int nchunks = (K + BK - 1) / BK;
 
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -489,13 +500,13 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
                                                        b_rsrc, (b_off0 + i * b_step + koff) | oob,
                                                        0, 0));
   };
-  // Quarter q of a chunk: load slots 4q .. 4q + 3 (A rows for q < 2).
+  // Quarter q of a chunk: load slots SLICE q .. SLICE (q + 1) - 1 (A rows for q < 2).
   auto load_slice = [&](int chunk, u32x4 (&r)[LOADS], int q) __attribute__((always_inline)) {
     const int oob = (int)((uint32_t)(K - 1 - (chunk * BK + v * 8)) & 0x80000000u);
     const int koff = chunk * ROW_BYTES;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = 4 * q + u;
+    for (int u = 0; u < SLICE; ++u) {
+      const int i = SLICE * q + u;
       if (i < LOADS / 2)
         r[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                              a_rsrc, (a_off0 + i * a_step + koff) | oob, 0, 0));
@@ -505,19 +516,19 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
                        b_rsrc, (b_off0 + (i - LOADS / 2) * b_step + koff) | oob, 0, 0));
     }
   };
-  // Row (r0 + 32 i) & 7 == r0 & 7: one slot for all of this thread's rows.
+  // Row (r0 + RSTEP i) & 7 == r0 & 7: one slot for all of this thread's rows.
   const int wslot = (v ^ (r0 & 7)) * 16;
   auto store_chunk = [&](int stage, const u32x4 (&r)[LOADS]) __attribute__((always_inline)) {
     unsigned char* base = smem + stage * STAGE_BYTES + r0 * ROW_BYTES + wslot;
 #pragma unroll
     for (int i = 0; i < LOADS; ++i)
-      *reinterpret_cast<u32x4*>(base + i * 32 * ROW_BYTES) = r[i];
+      *reinterpret_cast<u32x4*>(base + i * RSTEP * ROW_BYTES) = r[i];
   };
   auto store_slice = [&](int stage, const u32x4 (&r)[LOADS], int q) __attribute__((always_inline)) {
     unsigned char* base = smem + stage * STAGE_BYTES + r0 * ROW_BYTES + wslot;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      *reinterpret_cast<u32x4*>(base + (4 * q + u) * 32 * ROW_BYTES) = r[4 * q + u];
+    for (int u = 0; u < SLICE; ++u)
+      *reinterpret_cast<u32x4*>(base + (SLICE * q + u) * RSTEP * ROW_BYTES) = r[SLICE * q + u];
   };
 
   f32x16 acc[TM][TN];
@@ -531,8 +542,8 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   // Fragment reads: lane l takes row (l & 31) of a 32-row block and vector
   // 2 ks + (l >> 5) of k-step ks; rows of a block start at multiples of 8.
   const int frow = lane & 31, half = lane >> 5;
-  const int fa = (wm * 128 + frow) * ROW_BYTES;
-  const int fb = (BM + wn * 128 + frow) * ROW_BYTES;
+  const int fa = (wm * C::WM + frow) * ROW_BYTES;
+  const int fb = (BM + wn * C::WN + frow) * ROW_BYTES;
   struct Frags {
     u32x4 a[TM], b[TN];
   };
@@ -583,24 +594,27 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
       store_slice(nxt, stage_regs[nxt], ks);
       load_slice(c + 3, stage_regs[nxt], ks);
       mfma(f[ks & 1]);
+      constexpr int NR = TM + TN;              // fragment reads of a k-step
       if (ks < 3) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < NR; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         }
       } else {
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NR, 0);
+      }
+      constexpr int REST = TM * TN - NR;       // MFMAs left for the writes and loads
+      constexpr int PER = SLICE < REST / 2 ? 1 : (SLICE + REST / 2 - 1) / (REST / 2);
+#pragma unroll
+      for (int i = 0; i < SLICE; i += PER) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x200, PER, 0);  // DS write
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+      for (int i = 0; i < SLICE; i += PER) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, PER, 0);  // VMEM read
       }
     }
     lds_barrier();
@@ -613,17 +627,17 @@ __global__ __launch_bounds__(rs::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   }
 
   // ---- epilogue: bias (+ ReLU), bf16 stores ---------------------------------
-  // Lane l: output row m0 + 128 wm + 32 i + (l & 31); for group g of block j,
-  // columns n0 + 128 wn + 32 j + 8 g + 4 (l >> 5) + 0..3.
+  // Lane l: output row m0 + WM wm + 32 i + (l & 31); for group g of block j,
+  // columns n0 + WN wn + 32 j + 8 g + 4 (l >> 5) + 0..3.
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int64_t r = m0 + wm * 128 + i * 32 + frow;
+    const int64_t r = m0 + wm * C::WM + i * 32 + frow;
     if (r >= a.M) continue;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int cb = wn * 128 + j * 32 + 8 * g + 4 * half;
+        const int cb = wn * C::WN + j * 32 + 8 * g + 4 * half;
         const int c = n0 + cb;
         if (c >= a.N) continue;
         const float4 bv = *reinterpret_cast<const float4*>(bias_s + cb);
@@ -652,12 +666,16 @@ bool use_rs(const GemmLaunch& a) {
          reinterpret_cast<uintptr_t>(a.A0) % 16 == 0 && reinterpret_cast<uintptr_t>(a.B) % 16 == 0;
 }
 
+#ifndef PINSAGE_RS_CFG
+#define PINSAGE_RS_CFG RsCfg<2, 2>
+#endif
 hipError_t launch_rs(GemmLaunch a, hipStream_t s) {
+  using C = PINSAGE_RS_CFG;
   if (!a.ldb) a.ldb = a.K0;
-  const int64_t tiles = ((a.M + rs::BM - 1) / rs::BM) * (int64_t)((a.N + rs::BN - 1) / rs::BN);
+  const int64_t tiles = ((a.M + C::BM - 1) / C::BM) * (int64_t)((a.N + C::BN - 1) / C::BN);
   if (tiles <= 0) return hipSuccess;
   if (tiles > 0x7FFFFFFFll) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gemm_rs_kernel, dim3((unsigned)tiles), dim3(rs::THREADS), 0, s, a);
+  hipLaunchKernelGGL(gemm_rs_kernel<C>, dim3((unsigned)tiles), dim3(C::THREADS), 0, s, a);
   return hipGetLastError();
 }
 
