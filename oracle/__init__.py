@@ -4,8 +4,8 @@ A plain, slow CPU statement of the PinSage hot path (Ying et al., KDD 2018),
 written from the paper: random-walk importance neighbourhoods (Sec. 3.2),
 CONVOLVE (Algorithm 1), stacked layers evaluated layer-wise (Secs. 3.2, 3.4),
 MINIBATCH (Algorithm 2) with its output dense layers, the aggregators gamma
-(importance pooling, and the mean and max of Sec. 4's variants) and the
-max-margin loss (Sec. 3.3, Eq. 1). The
+(importance pooling, and the mean and max of Sec. 4's variants), the hard
+negative items of Sec. 3.3 and the max-margin loss (Sec. 3.3, Eq. 1). The
 arithmetic lives in ``oracle.cpp`` (fp64; importance weights fp32); this module
 only loads that library and marshals numpy arrays.
 
@@ -77,6 +77,9 @@ def _load():
     lib.orc_minibatch_embed_sampled.argtypes = [P, i64, i32, P, i64, P, i32, P, i64, P, P, i32,
                                                 P, P, P, P, P, P, P, i32, P]
     lib.orc_minibatch_embed_sampled.restype = None
+    lib.orc_hard_negatives.argtypes = [P, P, i64, i64, u64, i32, i32, P, i64, i32, i32, i32, P,
+                                       i32]
+    lib.orc_hard_negatives.restype = None
     lib.orc_output_mlp.argtypes = [P, i64, i32, P, P, i32, P, i32, P, i32]
     lib.orc_output_mlp.restype = None
     lib.orc_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_double, P]
@@ -311,3 +314,19 @@ def max_margin_loss(zq, zpos, zneg, margin):
     loss = lib.orc_max_margin_loss(_ptr(a), _ptr(b), a.shape[0], _ptr(c), c.shape[0],
                                    a.shape[1], margin, _ptr(per))
     return float(loss), per
+
+
+def hard_negatives(offsets, col, num_pins, seed, walks, hops, queries, rank_lo, rank_hi, k,
+                   nthreads=None):
+    """Sec. 3.3 hard negatives: k pins per query drawn from the PPR rank window
+    [rank_lo, rank_hi) (visit-count ranking of the query's own walks); -1 where
+    the window is empty."""
+    lib = _load()
+    off = _c(offsets, np.int64)
+    cl = _c(col, np.int32)
+    q = _c(queries, np.int32)
+    out = np.empty((len(q), k), np.int32)
+    lib.orc_hard_negatives(_ptr(off), _ptr(cl), num_pins, len(off) - 1, seed, walks, hops,
+                           _ptr(q), len(q), rank_lo, rank_hi, k, _ptr(out),
+                           nthreads or default_threads())
+    return out

@@ -19,6 +19,7 @@
 //   * aggregators gamma ...... importance pooling (Sec. 3.2), and the element-wise
 //                              mean and max of the compared variants (Sec. 4).
 //   * output dense layers .... Algorithm 2, final loop: z = G2 ReLU(G1 h + g).
+//   * hard negative items .... Sec. 3.3 (PPR rank window, sampled).
 //
 // Readings of points the paper leaves open are listed in the repository's
 // design notes; the ones that change arithmetic are restated at each function.
@@ -125,8 +126,9 @@ int64_t walk_from(const Graph& g, uint64_t seed, int64_t u, int walks, int hops,
 // kept T counts, so the weights of a row sum to one (the weighted mean is the
 // same under either normalisation). Rows with fewer than T distinct pins are
 // padded with (-1, 0, 0.0f).
-void select_top_t(const std::vector<int32_t>& visits, int T, int32_t* idx, uint16_t* cnt,
-                  float* wts) {
+// The distinct visited pins as (count, id), in rank order: more visits
+// first, ties to the lower id.
+std::vector<std::pair<int64_t, int32_t>> ranked_pins(const std::vector<int32_t>& visits) {
   std::map<int32_t, int64_t> counts;
   for (int32_t v : visits) counts[v] += 1;
   std::vector<std::pair<int64_t, int32_t>> order;  // (count, id)
@@ -136,6 +138,12 @@ void select_top_t(const std::vector<int32_t>& visits, int T, int32_t* idx, uint1
               if (a.first != b.first) return a.first > b.first;  // more visits first
               return a.second < b.second;                        // then lower id
             });
+  return order;
+}
+
+void select_top_t(const std::vector<int32_t>& visits, int T, int32_t* idx, uint16_t* cnt,
+                  float* wts) {
+  const std::vector<std::pair<int64_t, int32_t>> order = ranked_pins(visits);
   int keep = (int)std::min<size_t>((size_t)T, order.size());
   int64_t total = 0;
   for (int t = 0; t < keep; ++t) total += order[t].first;
@@ -325,6 +333,46 @@ void orc_convolve_layer(const double* h_in, int64_t n_in, int d_in, int64_t n_tr
                [&](int32_t v) { return P.data() + (int64_t)v * m; }, m, n_u.data());
       int64_t self = self_rows ? self_rows[r] : r;
       combine_row(h_in + self * d_in, d_in, n_u.data(), m, W, w, d_out, h_out + r * d_out);
+    }
+  });
+}
+
+// Sec. 3.3, hard negative items: the pins are ranked by their Personalized
+// PageRank score with respect to the query, and items at ranks in a window
+// (the paper: 2000-5000) are sampled at random. Readings: the scores are the
+// visit counts of the Sec. 3.2 walks from the query (walks, hops and seed of
+// their own), ranked like the neighbourhoods (count descending, ties to the
+// lower id, the query itself excluded); the window is [rank_lo, rank_hi),
+// 0-based, cut at the number of ranked pins n_r; draw j for query q is word 0
+// of Philox4x32-10 at counter (q, j, 0, 1) under the walk key, mapped to
+// window position floor(r * n / 2^32), n = min(rank_hi, n_r) - rank_lo
+// (independent draws, with replacement). Without a window (n <= 0), or for a
+// query id outside the graph, the k entries are -1.
+void orc_hard_negatives(const int64_t* off, const int32_t* col, int64_t num_pins,
+                        int64_t num_nodes, uint64_t seed, int walks, int hops,
+                        const int32_t* queries, int64_t num_queries, int rank_lo, int rank_hi,
+                        int k, int32_t* out, int nthreads) {
+  Graph g{off, col, num_pins, num_nodes};
+  const uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+  parallel_rows(num_queries, nthreads, [&](int64_t lo, int64_t hi) {
+    std::vector<int32_t> visits;
+    for (int64_t i = lo; i < hi; ++i) {
+      const int64_t q = queries[i];
+      for (int j = 0; j < k; ++j) out[i * k + j] = -1;
+      if (q < 0 || q >= num_nodes) continue;
+      visits.clear();
+      walk_from(g, seed, q, walks, hops, visits);
+      const auto order = ranked_pins(visits);
+      const int64_t top = std::min<int64_t>(rank_hi, (int64_t)order.size());
+      const int64_t n = top - rank_lo;
+      if (n <= 0) continue;
+      for (int j = 0; j < k; ++j) {
+        const uint32_t ctr[4] = {(uint32_t)q, (uint32_t)j, 0u, 1u};
+        uint32_t r[4];
+        philox4x32_10(ctr, key, r);
+        const int64_t pos = (int64_t)(((uint64_t)r[0] * (uint64_t)n) >> 32);
+        out[i * k + j] = order[rank_lo + pos].second;
+      }
     }
   });
 }
