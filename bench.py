@@ -14,6 +14,10 @@ Other workloads (measurement of the other rows; not the headline):
   --workload minibatch              one step = the minibatch forward of
                                     Algorithm 2 (2,048 pairs, 500 shared
                                     negatives) plus the loss of Eq. 1
+  --workload hardneg                one step = hard negative items (Sec. 3.3)
+                                    for 2,048 query pins of the 1.2M-node
+                                    graph: 4096 walks x 4 landings each, ranks
+                                    2000-5000, --hard-neg draws per query
 
 Prints one JSON line: throughput of the whole step, walk steps/s, per-kernel
 times from hipEvents recorded around every launch in the timed region, the
@@ -41,8 +45,11 @@ METRIC = "node embeddings/sec (K=2 layerwise, all nodes) + walk steps/sec, 1 MI3
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2}
-DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1}
+DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2, "hardneg": 20}
+DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1, "hardneg": 3}
+# Hard negative workload: queries per step, walks and landings per query, the
+# rank window [lo, hi) (ranks 2000-5000 counted from 1).
+HN_QUERIES, HN_WALKS, HN_HOPS, HN_LO, HN_HI = 2048, 4096, 4, 1999, 5000
 DEVICE_GENERATED = ("large", "shard")
 
 
@@ -215,7 +222,8 @@ def roofline_of(kernels, wl):
         return {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
                 "peak": MFMA_PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s", "frac": kd["frac_mfma"],
                 "traffic": None}
-    src_file = {"pool": "pool.hip", "walk_topt": "walk.hip"}.get(dominant, "")
+    src_file = {"pool": "pool.hip", "walk_topt": "walk.hip",
+                "hard_neg": "hardneg.hip"}.get(dominant, "")
     tr = load_traffic(src_file, wl.name) if src_file else None
     return {"kernel": dominant, "bound": "hbm", "achieved": kd.get("achieved_GBs"),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -376,6 +384,56 @@ def cpu_baseline_minibatch(inp, wl, threads):
                        f"gather excluded)")}
 
 
+def bench_hard_negatives(args, wl, inp):
+    import numpy as np
+    import torch
+
+    import paper_1806_01973_amd as ps
+    k = args.hard_neg
+    total = args.steps + args.warmup
+    rng = np.random.default_rng(wl.seed)
+    qs = [torch.as_tensor(rng.integers(0, wl.num_pins, HN_QUERIES).astype(np.int32)).cuda()
+          for _ in range(total)]
+    out = torch.empty((HN_QUERIES, k), dtype=torch.int32, device="cuda")
+    steps_dev = []
+
+    def run(i):
+        _, st = ps.hard_negatives(inp["g"], qs[i], k, wl.seed + 1, HN_WALKS, HN_HOPS, HN_LO,
+                                  HN_HI, out=out, count_steps=True)
+        steps_dev.append(st)
+
+    elapsed, prof = timed(run, args.steps, args.warmup)
+    kernels = kernel_table(prof, args.steps)
+    edge_steps = sum(int(t.item()) for t in steps_dev[args.warmup:]) / args.steps
+    kd = kernels["hard_neg"]
+    off_b = 8 if wl.offsets64 else 4
+    kd["edge_steps_per_launch"] = edge_steps
+    kd["algo_bytes_per_launch"] = edge_steps * (2 * off_b + 4)
+    kd["achieved_GBs"] = kd["algo_bytes_per_launch"] / (kd["avg_ms"] * 1e-3) / 1e9
+    kd["edge_steps_per_s"] = edge_steps / (kd["avg_ms"] * 1e-3)
+    value = HN_QUERIES * args.steps / elapsed
+    extra = {"walk_steps_per_s": edge_steps * args.steps / elapsed,
+             "config_extra": {"queries": HN_QUERIES, "walks": HN_WALKS, "hops": HN_HOPS,
+                              "rank_window": [HN_LO, HN_HI], "per_query": k,
+                              "empty_rows_last": int((out[:, 0] < 0).sum().item())}}
+    metric = "hard negative items (Sec. 3.3, PPR rank window), queries/sec, 1 MI355X"
+    return value, "queries/s", metric, elapsed, kernels, extra
+
+
+def cpu_baseline_hard_negatives(inp, wl, threads, k):
+    """The oracle's hard negatives for a sample of 512 query pins."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(10_000)
+    q = rng.integers(0, wl.num_pins, 512).astype(np.int32)
+    t0 = time.perf_counter()
+    oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins, wl.seed + 1,
+                          HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k, nthreads=threads)
+    secs = time.perf_counter() - t0
+    return {"value": len(q) / secs, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(q)} query pins, {secs:.1f}s"}
+
+
 def layer_probe(args) -> int:
     """One CONVOLVE layer on seeded random inputs, for kernel-level measurement
     (rocprofv3 counters, GEMM tile studies): rows x (d_in, m, d_out) in the
@@ -424,7 +482,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="medium",
-                    choices=["tiny", "medium", "minibatch", "large", "shard"])
+                    choices=["tiny", "medium", "minibatch", "large", "shard", "hardneg"])
     ap.add_argument("--dataflow", default="dense_then_pool",
                     choices=["pool_then_dense", "dense_then_pool"],
                     help="layer evaluation order (same values; see pinsage_dataflow_t)")
@@ -434,6 +492,8 @@ def main() -> int:
                     help="aggregator of every layer (max implies the pool-then-dense order)")
     ap.add_argument("--mlp", type=int, default=0, metavar="D_HIDDEN",
                     help="append the output dense layers z = G2 ReLU(G1 h + g) to the step")
+    ap.add_argument("--hard-neg", type=int, default=4, metavar="K",
+                    help="draws per query for --workload hardneg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layer", default=None,
                     help="d_in,m,d_out: time one layer on random inputs instead of a workload")
@@ -457,9 +517,10 @@ def main() -> int:
 
     import synth
 
-    wl = synth.WORKLOADS[args.workload]
-    args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[wl.name]
-    args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[wl.name]
+    hardneg = args.workload == "hardneg"
+    wl = synth.WORKLOADS["medium" if hardneg else args.workload]
+    args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.workload]
+    args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[args.workload]
     if args.pool == "max" and args.dataflow == "dense_then_pool":
         args.dataflow = "pool_then_dense"  # max pooling is not linear
     inp = load_inputs(wl, args.dataflow, args.pool)
@@ -467,7 +528,9 @@ def main() -> int:
         import synth as _s
         P = _s.make_mlp(wl.d_out, args.mlp, wl.d_out, seed=wl.seed, dtype=wl.dtype)
         inp["mlp"] = ps_mlp(P, wl)
-    if wl.name == "minibatch":
+    if hardneg:
+        value, unit, metric, elapsed, kernels, extra = bench_hard_negatives(args, wl, inp)
+    elif wl.name == "minibatch":
         value, unit, metric, elapsed, kernels, extra = bench_minibatch(args, wl, inp)
     else:
         value, unit, metric, elapsed, kernels, extra = bench_embed_all(args, wl, inp)
@@ -483,15 +546,19 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": wl.dtype,
+        "dtype": "u32" if hardneg else wl.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
+        "config": {"workload": (f"hard negatives: {wl.num_pins} pins + {wl.num_boards} boards, "
+                                f"{inp['num_edges']} edges, {HN_QUERIES} query pins, {HN_WALKS} "
+                                f"walks x {HN_HOPS} landings each, ranks {HN_LO + 1}-{HN_HI}, "
+                                f"{args.hard_neg} per query") if hardneg else
+                   (f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
                                f"{inp['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
                                f"T={wl.T}, K={wl.K}, dims {wl.d_in}->{wl.m}->{wl.d_out} "
                                f"{wl.dtype}, layer dataflow {args.dataflow}"
                                + (f", pool {args.pool}" if args.pool != "importance" else "")
                                + (f", output layers {wl.d_out}->{args.mlp}->{wl.d_out}"
-                                  if args.mlp else ""),
+                                  if args.mlp else "")),
                    "dataflow": args.dataflow, "pool": args.pool, "output_layers": args.mlp or None,
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
@@ -505,9 +572,12 @@ def main() -> int:
         import oracle
         threads = oracle.default_threads()
         log(f"timing the oracle on a sample ({threads} threads)")
-        result["cpu_baseline"] = (cpu_baseline_minibatch(inp, wl, threads)
-                                  if wl.name == "minibatch" else
-                                  cpu_baseline_embed(inp, wl, threads))
+        if hardneg:
+            result["cpu_baseline"] = cpu_baseline_hard_negatives(inp, wl, threads, args.hard_neg)
+        elif wl.name == "minibatch":
+            result["cpu_baseline"] = cpu_baseline_minibatch(inp, wl, threads)
+        else:
+            result["cpu_baseline"] = cpu_baseline_embed(inp, wl, threads)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -9,7 +9,8 @@
  *   2. K stacked CONVOLVE layers (Algorithm 1) over every node, evaluated
  *      layer by layer so that each node's transformed vector is computed once
  *      (Sec. 3.4),
- *   3. the minibatch forward of Algorithm 2 with the max-margin loss (Eq. 1).
+ *   3. the minibatch forward of Algorithm 2 with the max-margin loss (Eq. 1),
+ *   4. hard negative items for training queries (Sec. 3.3).
  *
  * Conventions shared by every entry point
  *   - Graph (Sec. 3.1): a bipartite graph of pins I and boards C, V = I u C.
@@ -38,7 +39,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 3
+#define PINSAGE_ABI_VERSION 4
 
 enum {
   PINSAGE_OK = 0,
@@ -180,6 +181,39 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph,
                                 pinsage_neighborhoods_t* out,
                                 unsigned long long* total_steps, void* stream);
 
+/* Hard negative items (Sec. 3.3, "Hard negative items"): for each query, pins
+ * are ranked by their Personalized PageRank score with respect to the query
+ * and items in a window of ranks are sampled. The score is estimated by the
+ * visit counts of `walks` random walks of `hops` pin landings from the query,
+ * the walks of pinsage_walk_params_t (same steps, same Philox stream under
+ * `seed`); ranks run over the distinct visited pins (the query excluded) by
+ * count descending, ties by lower node id, from 0. With D ranked pins and
+ * n = min(rank_hi, D) - rank_lo, draw j in [0, num_per_query) of query q takes
+ * word 0, r, of Philox4x32-10 at counter (q, j, 0, 1) under the same key and
+ * returns the pin at rank rank_lo + floor(r * n / 2^32) (independent draws,
+ * with replacement). The paper's window, ranks 2000 to 5000 counted from 1,
+ * is rank_lo = 1999, rank_hi = 5000.
+ * Limits: 1 <= walks * hops <= 16384, 0 <= rank_lo < rank_hi,
+ * 0 <= num_per_query. */
+typedef struct {
+  uint64_t seed;
+  int32_t walks;
+  int32_t hops;
+  int32_t rank_lo;
+  int32_t rank_hi;
+  int32_t num_per_query;
+} pinsage_hard_negative_params_t;
+
+/* out: device int32 [num_queries][num_per_query], pin ids, or -1 for every
+ * draw of a query whose window is empty (n <= 0) or whose id lies outside
+ * [0, num_nodes). queries: device int32 [num_queries]. If total_steps is
+ * non-NULL (device uint64), it receives the number of edge steps all walks
+ * took. Out-of-range CSR entries end the walk that meets them. */
+int pinsage_hard_negatives(const pinsage_graph_t* graph,
+                           const pinsage_hard_negative_params_t* params,
+                           const int32_t* queries, int64_t num_queries, int32_t* out,
+                           unsigned long long* total_steps, void* stream);
+
 /* Workspace bytes needed by pinsage_convolve_layer for these sizes. */
 int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
                                     int64_t n_out, size_t* bytes);
@@ -302,7 +336,8 @@ enum {
   PINSAGE_KERNEL_LOSS = 5,
   PINSAGE_KERNEL_GEMM_R = 6, /* neighbour half of W per pin (DENSE_THEN_POOL) */
   PINSAGE_KERNEL_MLP = 7,    /* output dense layers */
-  PINSAGE_KERNEL_COUNT = 8
+  PINSAGE_KERNEL_HARD_NEG = 8,
+  PINSAGE_KERNEL_COUNT = 9
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

@@ -19,6 +19,7 @@ from .api import (  # noqa: F401
     convolve_workspace_size,
     embed_all,
     embed_all_workspace_size,
+    hard_negatives,
     max_margin_loss,
     output_mlp,
     profile_enable,

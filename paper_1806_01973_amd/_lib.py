@@ -22,11 +22,12 @@ POOLS = {"importance": 0, "mean": 1, "max": 2}
 
 (KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
  KERNEL_GEMM_R, KERNEL_MLP) = range(8)
-KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp"]
+KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp",
+                "hard_neg"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
-    "pinsage_build_neighborhoods", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
+    "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
     "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_output_mlp_workspace_size",
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
@@ -56,6 +57,12 @@ class Layer(ctypes.Structure):
                 ("dtype", ctypes.c_int), ("Q", ctypes.c_void_p), ("q", ctypes.c_void_p),
                 ("W", ctypes.c_void_p), ("w", ctypes.c_void_p), ("dataflow", ctypes.c_int),
                 ("pool", ctypes.c_int)]
+
+
+class HardNegativeParams(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("walks", ctypes.c_int32), ("hops", ctypes.c_int32),
+                ("rank_lo", ctypes.c_int32), ("rank_hi", ctypes.c_int32),
+                ("num_per_query", ctypes.c_int32)]
 
 
 class MLP(ctypes.Structure):
@@ -95,6 +102,8 @@ def lib():
     L.pinsage_last_error.restype = ctypes.c_char_p
     L.pinsage_build_neighborhoods.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                               P, i64, ctypes.POINTER(Neighborhoods), P, P]
+    L.pinsage_hard_negatives.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(HardNegativeParams),
+                                         P, i64, P, P, P]
     L.pinsage_convolve_workspace_size.argtypes = [ctypes.POINTER(Layer), i64, i64,
                                                   ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64, P,

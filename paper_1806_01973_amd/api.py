@@ -191,6 +191,26 @@ def build_neighborhoods(graph: DeviceGraph, walks: int, hops: int, T: int, seed:
     return nb, steps
 
 
+def hard_negatives(graph: DeviceGraph, queries: torch.Tensor, k: int, seed: int, walks: int,
+                   hops: int, rank_lo: int = 1999, rank_hi: int = 5000,
+                   out: Optional[torch.Tensor] = None, count_steps: bool = False, stream=None):
+    """Hard negative items (Sec. 3.3): k pins per query drawn from ranks
+    [rank_lo, rank_hi) of the query's visit-count (PPR) ranking; -1 where the
+    window is empty. Returns (out int32 [n][k], total_steps tensor|None)."""
+    lib = L.lib()
+    queries = _dev(queries, "queries", torch.int32)
+    n = int(queries.numel())
+    if out is None:
+        out = torch.empty((n, k), dtype=torch.int32, device=queries.device)
+    steps = torch.empty(1, dtype=torch.int64, device=queries.device) if count_steps else None
+    g = graph.struct()
+    hp = L.HardNegativeParams(seed, walks, hops, rank_lo, rank_hi, k)
+    st = lib.pinsage_hard_negatives(ctypes.byref(g), ctypes.byref(hp), _ptr(queries), n, _ptr(out),
+                                    _ptr(steps), _stream(stream))
+    L.check(st, "pinsage_hard_negatives")
+    return out, steps
+
+
 def convolve_workspace_size(layer: DeviceLayer, n_transform: int, n_out: int) -> int:
     n = ctypes.c_size_t(0)
     st = L.lib().pinsage_convolve_workspace_size(ctypes.byref(layer.struct()), n_transform, n_out,

@@ -445,6 +445,55 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk
   return PINSAGE_OK;
 }
 
+int pinsage_hard_negatives(const pinsage_graph_t* graph,
+                           const pinsage_hard_negative_params_t* params, const int32_t* queries,
+                           int64_t num_queries, int32_t* out, unsigned long long* total_steps,
+                           void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if (!params) return fail(PINSAGE_EINVAL, "hard negative params are NULL");
+  const pinsage_hard_negative_params_t& h = *params;
+  if (h.walks < 1 || h.hops < 1)
+    return fail(PINSAGE_EINVAL, "walks (%d) and hops (%d) must be >= 1", h.walks, h.hops);
+  if ((int64_t)h.walks * h.hops > 16384)
+    return fail(PINSAGE_EUNSUPPORTED, "walks * hops = %lld exceeds 16384",
+                (long long)h.walks * h.hops);
+  if (h.rank_lo < 0 || h.rank_hi <= h.rank_lo)
+    return fail(PINSAGE_EINVAL, "rank window [%d, %d) is empty or negative", h.rank_lo,
+                h.rank_hi);
+  if (h.num_per_query < 0) return fail(PINSAGE_EINVAL, "negative num_per_query");
+  if (num_queries < 0) return fail(PINSAGE_EINVAL, "negative num_queries");
+  if (num_queries > 0 && !queries) return fail(PINSAGE_EINVAL, "queries is NULL");
+  if (num_queries > 0 && h.num_per_query > 0 && !out) return fail(PINSAGE_EINVAL, "out is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (total_steps) {
+    hipError_t e = launch_zero_u64(total_steps, 1, s);
+    if (e != hipSuccess) return hip_fail(e, "step counter reset");
+  }
+  if (num_queries == 0 || (h.num_per_query == 0 && !total_steps)) return PINSAGE_OK;
+  HardNegLaunch a{};
+  a.row_offsets = graph->row_offsets;
+  a.offsets64 = graph->offset_type == PINSAGE_I64;
+  a.col = graph->col;
+  a.nnz = graph->nnz;
+  a.num_pins = graph->num_pins;
+  a.num_nodes = graph->num_pins + graph->num_boards;
+  a.queries = queries;
+  a.num_queries = num_queries;
+  a.seed = h.seed;
+  a.walks = h.walks;
+  a.hops = h.hops;
+  a.rank_lo = h.rank_lo;
+  a.rank_hi = h.rank_hi;
+  a.k = h.num_per_query;
+  a.out = out;
+  a.total_steps = total_steps;
+  hipError_t e = launch_hard_negatives(a, s);
+  if (e != hipSuccess) return hip_fail(e, "hard negative launch");
+  return PINSAGE_OK;
+}
+
 int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
                                     int64_t n_out, size_t* bytes) {
   g_last_error.clear();

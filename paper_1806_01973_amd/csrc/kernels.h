@@ -9,7 +9,7 @@ namespace pinsage {
 
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
-                   kKGemmR = 6, kKMlp = 7, kKCount = 8 };
+                   kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKCount = 9 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -41,6 +41,29 @@ struct WalkLaunch {
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
 };
 hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
+
+// Hard negative items (Sec. 3.3): out[i][j], j < k, drawn from ranks
+// [rank_lo, rank_hi) of the visit-count ranking of walks from queries[i];
+// walks * hops <= 16384.
+struct HardNegLaunch {
+  const void* row_offsets;
+  bool offsets64;
+  const int32_t* col;
+  int64_t nnz;
+  int64_t num_pins;
+  int64_t num_nodes;
+  const int32_t* queries;
+  int64_t num_queries;
+  uint64_t seed;
+  int walks;
+  int hops;
+  int rank_lo;
+  int rank_hi;
+  int k;
+  int32_t* out;
+  unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
+};
+hipError_t launch_hard_negatives(const HardNegLaunch& a, hipStream_t s);
 
 
 // Pooling modes (values match pinsage_pool_t).

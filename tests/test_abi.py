@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 3
+    assert lib.pinsage_version() == 4
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -83,6 +83,30 @@ def test_build_neighborhoods_validation(L):
         L.PINSAGE_EINVAL  # row mismatch
     assert call(_graph(L), walk, None, 15, L.Neighborhoods(15, 8, None, FAKE, None)) == \
         L.PINSAGE_EINVAL
+
+
+def test_hard_negatives_validation(L):
+    lib = L.lib()
+    hp = lambda **kw: L.HardNegativeParams(**{**dict(seed=1, walks=4096, hops=4, rank_lo=1999,
+                                                      rank_hi=5000, num_per_query=3), **kw})
+    call = lambda g, p, q, n, out: lib.pinsage_hard_negatives(
+        ctypes.byref(g) if g is not None else None, ctypes.byref(p) if p is not None else None,
+        q, n, out, None, None)
+    assert call(None, hp(), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), None, FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(walks=0), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(hops=5), FAKE, 4, FAKE) == L.PINSAGE_EUNSUPPORTED  # 20480 slots
+    assert b"16384" in lib.pinsage_last_error()
+    assert call(_graph(L), hp(rank_lo=-1), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(rank_lo=10, rank_hi=10), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(num_per_query=-1), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(), None, 4, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(), FAKE, 4, None) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(), FAKE, -1, FAKE) == L.PINSAGE_EINVAL
+    assert call(_graph(L, offset_type=7), hp(), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
+    # Nothing to do: accepted without touching the device.
+    assert call(_graph(L), hp(), None, 0, None) == L.PINSAGE_OK
+    assert call(_graph(L), hp(num_per_query=0), FAKE, 4, None) == L.PINSAGE_OK
 
 
 def test_layer_validation_and_workspace_sizes(L):
