@@ -27,6 +27,7 @@ of the same workload.
   python bench.py [--steps K] [--warmup W] [--workload medium] [--no-cpu-baseline]
   python bench.py --copy-calibration   # plain copy of a known size, for counter scaling
   python bench.py --layer 1024,2048,512 --rows 4000000 --dtype bf16   # one layer, for counters
+  python bench.py --workload hardneg   # hard negative items of 2,048 queries
 """
 
 from __future__ import annotations
@@ -58,9 +59,20 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash(name: str) -> str:
-    path = os.path.join(ROOT, "paper_1806_01973_amd", "csrc", name)
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of a kernel source file and the local headers it includes."""
+    csrc = os.path.join(ROOT, "paper_1806_01973_amd", "csrc")
+    h = hashlib.sha256()
+    with open(os.path.join(csrc, name), "rb") as f:
+        text = f.read()
+    h.update(text)
+    for line in text.decode().splitlines():
+        line = line.strip()
+        if line.startswith('#include "'):
+            inc = os.path.join(csrc, line.split('"')[1])
+            if os.path.exists(inc):
+                with open(inc, "rb") as f:
+                    h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(kernel_file: str, workload: str):
@@ -421,11 +433,12 @@ def bench_hard_negatives(args, wl, inp):
 
 
 def cpu_baseline_hard_negatives(inp, wl, threads, k):
-    """The oracle's hard negatives for a sample of 512 query pins."""
+    """The oracle's hard negatives for a sample of 16,384 query pins (eight steps'
+    worth of queries)."""
     import numpy as np
     import oracle
     rng = np.random.default_rng(10_000)
-    q = rng.integers(0, wl.num_pins, 512).astype(np.int32)
+    q = rng.integers(0, wl.num_pins, 16_384).astype(np.int32)
     t0 = time.perf_counter()
     oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins, wl.seed + 1,
                           HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k, nthreads=threads)
@@ -472,8 +485,37 @@ def layer_probe(args) -> int:
                          "frac_mfma": flops[name] / (per_call * 1e-3) / 1e12 / peak}
         elif launches:
             res[name] = {"ms": ms / steps}
+    if args.blas_ref:
+        res["blas_reference"] = blas_reference(n, [(d_in, m), (m, d_out)], dt, peak)
     print(json.dumps(res), flush=True)
     return 0
+
+
+def blas_reference(n, shapes, dt, peak):
+    """Library GEMM rates (torch.matmul, i.e. hipBLASLt) for the plain products
+    [n, K] x [K, N] of the given (K, N) shapes, without bias or epilogue: a
+    reference point for the layer GEMMs, not part of the path."""
+    import torch
+    out = {}
+    for K, N in shapes:
+        a = torch.randn(n, K, device="cuda").to(dt)
+        b = torch.randn(N, K, device="cuda").to(dt)
+        bt = b.t()
+        for _ in range(2):
+            c = a @ bt
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(5):
+            c = a @ bt
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / 5
+        tf = 2.0 * n * K * N / (ms * 1e-3) / 1e12
+        out[f"{n}x{K}x{N}"] = {"ms": ms, "TFLOP/s": tf, "frac_mfma": tf / peak}
+        del a, b, bt, c
+        torch.cuda.empty_cache()
+    return out
 
 
 def main() -> int:
@@ -499,6 +541,8 @@ def main() -> int:
                     help="d_in,m,d_out: time one layer on random inputs instead of a workload")
     ap.add_argument("--rows", type=int, default=4_000_000, help="rows for --layer")
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"], help="dtype for --layer")
+    ap.add_argument("--blas-ref", action="store_true",
+                    help="with --layer: also time torch.matmul on the layer's GEMM shapes")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 

@@ -131,33 +131,29 @@ struct Walker {
 
 // Ascending half-cleaners over the 64*E keys of a wave (strides 32E .. 1):
 // sorts a wave-sized bitonic sequence, e.g. the lower or upper half of a
-// larger bitonic merge once the strides above the wave are done.
-template <int E>
-__device__ __forceinline__ void merge_wave_ascending(uint32_t (&k)[E], int lane) {
-  const int lane_base = lane * E;
+// larger bitonic merge once the strides above the wave are done. Expanded by
+// template recursion so every stride, and every register index, is a
+// compile-time constant.
+template <int E, int STRIDE>
+__device__ __forceinline__ void merge_wave_step(uint32_t (&k)[E], int lane) {
+  if constexpr (STRIDE >= E) {
+    cross_lane_stage<STRIDE / E>(k, lane, ((lane * E) & STRIDE) == 0);
+  } else {
 #pragma unroll
-  for (int stride = kWave * E / 2; stride > 0; stride >>= 1) {
-    if (stride >= E) {
-      const bool take_min = (lane_base & stride) == 0;
-      switch (stride / E) {
-        case 1: cross_lane_stage<1>(k, lane, take_min); break;
-        case 2: cross_lane_stage<2>(k, lane, take_min); break;
-        case 4: cross_lane_stage<4>(k, lane, take_min); break;
-        case 8: cross_lane_stage<8>(k, lane, take_min); break;
-        case 16: cross_lane_stage<16>(k, lane, take_min); break;
-        default: cross_lane_stage<32>(k, lane, take_min); break;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        if ((e & stride) == 0) {
-          const uint32_t x = k[e], y = k[e + stride];
-          k[e] = x < y ? x : y;
-          k[e + stride] = x < y ? y : x;
-        }
+    for (int e = 0; e < E; ++e) {
+      if ((e & STRIDE) == 0) {
+        const uint32_t x = k[e], y = k[e + STRIDE];
+        k[e] = x < y ? x : y;
+        k[e + STRIDE] = x < y ? y : x;
       }
     }
   }
+  if constexpr (STRIDE > 1) merge_wave_step<E, STRIDE / 2>(k, lane);
+}
+
+template <int E>
+__device__ __forceinline__ void merge_wave_ascending(uint32_t (&k)[E], int lane) {
+  merge_wave_step<E, kWave * E / 2>(k, lane);
 }
 
 }  // namespace walkdev
