@@ -84,6 +84,9 @@ def _load():
     lib.orc_output_mlp.restype = None
     lib.orc_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_double, P]
     lib.orc_max_margin_loss.restype = ctypes.c_double
+    lib.orc_max_margin_loss_hard.argtypes = [P, P, i64, P, i64, P, P, i64, i32, ctypes.c_double,
+                                             P]
+    lib.orc_max_margin_loss_hard.restype = ctypes.c_double
     _lib = lib
     return lib
 
@@ -305,14 +308,23 @@ def output_mlp(h, G1, g, G2, nthreads=None):
     return z
 
 
-def max_margin_loss(zq, zpos, zneg, margin):
-    """Eq. (1) with the expectation read as the mean over the shared negatives;
-    returns (minibatch mean loss, per-pair terms)."""
+def max_margin_loss(zq, zpos, zneg, margin, zhard=None, hard_valid=None):
+    """Eq. (1) with the expectation read as the mean over the shared negatives,
+    joined per pair by its hard negatives zhard[b] ([B][k][d]; hard_valid[b][j]
+    false drops an entry); returns (minibatch mean loss, per-pair terms)."""
     lib = _load()
     a, b, c = _c(zq, np.float64), _c(zpos, np.float64), _c(zneg, np.float64)
     per = np.empty(a.shape[0], np.float64)
-    loss = lib.orc_max_margin_loss(_ptr(a), _ptr(b), a.shape[0], _ptr(c), c.shape[0],
-                                   a.shape[1], margin, _ptr(per))
+    if zhard is None:
+        loss = lib.orc_max_margin_loss(_ptr(a), _ptr(b), a.shape[0], _ptr(c), c.shape[0],
+                                       a.shape[1], margin, _ptr(per))
+        return float(loss), per
+    h = _c(zhard, np.float64)
+    B, k = h.shape[0], h.shape[1]
+    assert B == a.shape[0] and h.shape[2] == a.shape[1]
+    v = _c(np.ones((B, k), bool) if hard_valid is None else hard_valid, np.uint8)
+    loss = lib.orc_max_margin_loss_hard(_ptr(a), _ptr(b), B, _ptr(c), c.shape[0], _ptr(h),
+                                        _ptr(v), k, a.shape[1], margin, _ptr(per))
     return float(loss), per
 
 

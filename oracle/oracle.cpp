@@ -667,24 +667,43 @@ void orc_output_mlp(const double* h, int64_t n, int d_in, const double* G1, cons
 // max(0, z_q.z_n - z_q.z_i + margin). Readings: the expectation is the mean
 // over the shared negative set, and the minibatch loss is the mean over pairs.
 // Returns the minibatch loss; per_pair (nullable) receives each pair's term.
-double orc_max_margin_loss(const double* zq, const double* zpos, int64_t B, const double* zneg,
-                           int64_t n_neg, int d, double margin, double* per_pair) {
+//
+// With hard negatives (Sec. 3.3, "Hard negative items"): pair b also has its
+// own items zhard[b][0..k) (entries with hard_valid[b][j] == 0 are absent),
+// which join the negative set of that pair, so its term is the mean over the
+// shared negatives and its present hard negatives together.
+double orc_max_margin_loss_hard(const double* zq, const double* zpos, int64_t B,
+                                const double* zneg, int64_t n_neg, const double* zhard,
+                                const uint8_t* hard_valid, int64_t k, int d, double margin,
+                                double* per_pair) {
+  auto hinge = [&](int64_t b, const double* zn) {
+    double pos = 0.0, neg = 0.0;
+    for (int j = 0; j < d; ++j) pos += zq[b * d + j] * zpos[b * d + j];
+    for (int j = 0; j < d; ++j) neg += zq[b * d + j] * zn[j];
+    const double v = neg - pos + margin;
+    return v > 0.0 ? v : 0.0;
+  };
   double total = 0.0;
   for (int64_t b = 0; b < B; ++b) {
-    double pos = 0.0;
-    for (int j = 0; j < d; ++j) pos += zq[b * d + j] * zpos[b * d + j];
     double acc = 0.0;
-    for (int64_t n = 0; n < n_neg; ++n) {
-      double neg = 0.0;
-      for (int j = 0; j < d; ++j) neg += zq[b * d + j] * zneg[n * d + j];
-      double v = neg - pos + margin;
-      acc += v > 0.0 ? v : 0.0;
+    int64_t count = 0;
+    for (int64_t n = 0; n < n_neg; ++n, ++count) acc += hinge(b, zneg + n * d);
+    for (int64_t j = 0; j < k; ++j) {
+      if (!hard_valid[b * k + j]) continue;
+      acc += hinge(b, zhard + (b * k + j) * d);
+      ++count;
     }
-    double term = n_neg > 0 ? acc / (double)n_neg : 0.0;
+    const double term = count > 0 ? acc / (double)count : 0.0;
     if (per_pair) per_pair[b] = term;
     total += term;
   }
   return B > 0 ? total / (double)B : 0.0;
+}
+
+double orc_max_margin_loss(const double* zq, const double* zpos, int64_t B, const double* zneg,
+                           int64_t n_neg, int d, double margin, double* per_pair) {
+  return orc_max_margin_loss_hard(zq, zpos, B, zneg, n_neg, nullptr, nullptr, 0, d, margin,
+                                  per_pair);
 }
 
 }  // extern "C"

@@ -190,6 +190,36 @@ def test_max_margin_loss_closed_form(orc):
     assert loss == 0.0
 
 
+def test_max_margin_loss_with_hard_negatives(orc):
+    # Hard negatives join each pair's negative set (Sec. 3.3): a worked example.
+    zq = np.array([[1.0, 0.0], [0.6, 0.8]])
+    zpos = np.array([[1.0, 0.0], [0.8, -0.6]])
+    zneg = np.array([[0.0, 1.0], [-1.0, 0.0]])
+    zhard = np.array([[[1.0, 0.0], [0.6, 0.8]], [[0.6, 0.8], [0.0, -1.0]]])
+    valid = np.array([[1, 1], [1, 0]], bool)
+    loss, per = orc.max_margin_loss(zq, zpos, zneg, 0.1, zhard, valid)
+    # Pair 0: shared 0, 0; hard: 1 - 1 + 0.1 = 0.1, 0.6 - 1 + 0.1 < 0 -> 0; mean over 4.
+    # Pair 1: shared 0.9, 0; hard 1 + 0.1 = 1.1 (second entry absent); mean over 3.
+    np.testing.assert_allclose(per, [0.1 / 4, (0.9 + 1.1) / 3], atol=1e-15)
+    assert loss == pytest.approx((0.1 / 4 + 2.0 / 3) / 2, abs=1e-15)
+    # No hard entry present: the shared-only loss, exactly.
+    l0, p0 = orc.max_margin_loss(zq, zpos, zneg, 0.1)
+    l1, p1 = orc.max_margin_loss(zq, zpos, zneg, 0.1, zhard, np.zeros((2, 2), bool))
+    assert l1 == l0 and np.array_equal(p1, p0)
+    # Hard negatives equal to the shared ones: the mean over the multiset,
+    # i.e. the same per-pair terms.
+    rng = np.random.default_rng(1)
+    zq, zpos, zneg = (rng.standard_normal((3, 8)), rng.standard_normal((3, 8)),
+                      rng.standard_normal((5, 8)))
+    zh = np.broadcast_to(zneg, (3, 5, 8))
+    _, pa = orc.max_margin_loss(zq, zpos, zneg, 0.3)
+    _, pb = orc.max_margin_loss(zq, zpos, zneg, 0.3, zh)
+    np.testing.assert_allclose(pb, pa, rtol=1e-14)
+    # Moving an item from the shared set into every pair's hard set keeps the terms.
+    _, pc = orc.max_margin_loss(zq, zpos, zneg[:4], 0.3, np.broadcast_to(zneg[4:], (3, 1, 8)))
+    np.testing.assert_allclose(pc, pa, rtol=1e-14)
+
+
 def test_sampled_route_equals_full_table(orc):
     # The on-demand route (neighbourhoods walked only for the nodes a target set
     # needs, features given only for S^(0)) must reproduce the full-table route.
