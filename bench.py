@@ -14,6 +14,9 @@ Other workloads (measurement of the other rows; not the headline):
   --workload minibatch              one step = the minibatch forward of
                                     Algorithm 2 (2,048 pairs, 500 shared
                                     negatives) plus the loss of Eq. 1
+  --workload minibatch --hard-neg K  the same step preceded by mining K hard
+                                    negatives per query (Sec. 3.3), which join
+                                    every pair's negatives in the loss
   --workload hardneg                one step = hard negative items (Sec. 3.3)
                                     for 2,048 query pins of the 1.2M-node
                                     graph: 4096 walks x 4 landings each, ranks
@@ -343,18 +346,23 @@ def bench_minibatch(args, wl, inp):
     import paper_1806_01973_amd as ps
     import synth
     B, n_neg = 2048, 500
+    k = args.hard_neg or 0
     total = args.steps + args.warmup
     sets = [synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], B, n_neg,
                                   seed=i) for i in range(total)]
     dev = [[torch.as_tensor(a).cuda() for a in s] for s in sets]
     mb = ps.Minibatch(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed, B, n_neg,
-                      mlp=inp.get("mlp"))
+                      mlp=inp.get("mlp"), num_hard=k)
+    hard = torch.empty((B, k), dtype=torch.int32, device="cuda") if k else None
     stream = torch.cuda.current_stream()
     sizes = []
 
     def run(i):
         q, p, n = dev[i]
-        mb.run(inp["x"], q, p, n, 0.1, want_z=False, stream=stream)
+        if k:  # Sec. 3.3: the queries' hard negatives join their negative sets
+            ps.hard_negatives(inp["g"], q, k, wl.seed + 1, HN_WALKS, HN_HOPS, HN_LO, HN_HI,
+                              out=hard, stream=stream)
+        mb.run(inp["x"], q, p, n, 0.1, want_z=False, hard=hard, stream=stream)
         sizes.append(mb.sizes())
 
     elapsed, prof = timed(run, args.steps, args.warmup)
@@ -364,20 +372,33 @@ def bench_minibatch(args, wl, inp):
     value = B * args.steps / elapsed
     extra = {"walk_steps_per_s": None,
              "config_extra": {"pairs": B, "negatives": n_neg, "margin": 0.1,
+                              "hard_negatives_per_pair": k,
                               "mean_frontier_sizes": mean_sizes,
                               "loss_last": float(mb.loss.item())}}
-    metric = "minibatch forward (Algorithm 2) + max-margin loss, training pairs/sec, 1 MI355X"
+    metric = ("minibatch forward (Algorithm 2) + max-margin loss, training pairs/sec, 1 MI355X"
+              if not k else "hard negative mining (Sec. 3.3) + minibatch forward (Algorithm 2) "
+              "+ max-margin loss, training pairs/sec, 1 MI355X")
     return value, "training pairs/s", metric, elapsed, kernels, extra
 
 
-def cpu_baseline_minibatch(inp, wl, threads):
+def cpu_baseline_minibatch(inp, wl, threads, k=0):
     """The oracle's Algorithm 2 route (on-demand neighbourhoods) and Eq. 1 for one
-    full minibatch of the same shape."""
+    full minibatch of the same shape (with k hard negatives per pair, mined by
+    the oracle first)."""
+    import numpy as np
     import oracle
     import synth
     q, p, n = synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], 2048, 500,
                                     seed=10_000)
-    targets = __import__("numpy").concatenate([q, p, n]).astype("int32")
+    t_hard = time.perf_counter()
+    hard = valid = None
+    if k:
+        hard = oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins,
+                                     wl.seed + 1, HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k,
+                                     nthreads=threads)
+        valid = hard >= 0
+    t_hard = time.perf_counter() - t_hard
+    targets = np.concatenate([q, p, n] + ([hard[valid]] if k else [])).astype("int32")
     t0 = time.perf_counter()
     smp = oracle.minibatch_sample(targets, wl.K, inp["host"]["offsets"], inp["host"]["col"],
                                   wl.num_pins, wl.seed, wl.walks, wl.hops, wl.T, nthreads=threads)
@@ -387,13 +408,18 @@ def cpu_baseline_minibatch(inp, wl, threads):
     t1 = time.perf_counter()
     z = oracle.minibatch_embed_sampled(targets, s0, x_rows, smp, inp["layers_np"],
                                        nthreads=threads)
-    oracle.max_margin_loss(z[:2048], z[2048:4096], z[4096:], 0.1)
+    zhard = None
+    if k:
+        zhard = np.zeros((2048, k, z.shape[1]))
+        zhard[valid] = z[4596:]
+    oracle.max_margin_loss(z[:2048], z[2048:4096], z[4096:4596], 0.1, zhard, valid)
     t2 = time.perf_counter()
-    secs = (t1 - t0) + (t2 - t1)
+    secs = t_hard + (t1 - t0) + (t2 - t1)
     return {"value": 2048 / secs, "unit": "training pairs/s", "cores": threads, "kind": "oracle",
-            "sample": (f"one minibatch of 2048 pairs + 500 negatives: on-demand walks "
-                       f"{t1 - t0:.1f}s, fp64 Algorithm 2 + Eq. 1 {t2 - t1:.1f}s (feature "
-                       f"gather excluded)")}
+            "sample": (f"one minibatch of 2048 pairs + 500 negatives"
+                       + (f" + {k} hard negatives per pair (mined in {t_hard:.1f}s)" if k else "")
+                       + f": on-demand walks {t1 - t0:.1f}s, fp64 Algorithm 2 + Eq. 1 "
+                       f"{t2 - t1:.1f}s (feature gather excluded)")}
 
 
 def bench_hard_negatives(args, wl, inp):
@@ -534,8 +560,10 @@ def main() -> int:
                     help="aggregator of every layer (max implies the pool-then-dense order)")
     ap.add_argument("--mlp", type=int, default=0, metavar="D_HIDDEN",
                     help="append the output dense layers z = G2 ReLU(G1 h + g) to the step")
-    ap.add_argument("--hard-neg", type=int, default=4, metavar="K",
-                    help="draws per query for --workload hardneg")
+    ap.add_argument("--hard-neg", type=int, default=None, metavar="K",
+                    help="hard negatives per query: draws for --workload hardneg (default 4); "
+                         "with --workload minibatch, mined each step and added to every "
+                         "pair's negatives (default 0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layer", default=None,
                     help="d_in,m,d_out: time one layer on random inputs instead of a workload")
@@ -562,6 +590,8 @@ def main() -> int:
     import synth
 
     hardneg = args.workload == "hardneg"
+    if hardneg and args.hard_neg is None:
+        args.hard_neg = 4
     wl = synth.WORKLOADS["medium" if hardneg else args.workload]
     args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.workload]
     args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[args.workload]
@@ -619,7 +649,8 @@ def main() -> int:
         if hardneg:
             result["cpu_baseline"] = cpu_baseline_hard_negatives(inp, wl, threads, args.hard_neg)
         elif wl.name == "minibatch":
-            result["cpu_baseline"] = cpu_baseline_minibatch(inp, wl, threads)
+            result["cpu_baseline"] = cpu_baseline_minibatch(inp, wl, threads,
+                                                            args.hard_neg or 0)
         else:
             result["cpu_baseline"] = cpu_baseline_embed(inp, wl, threads)
     print(json.dumps(result), flush=True)

@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 4
+#define PINSAGE_ABI_VERSION 5
 
 enum {
   PINSAGE_OK = 0,
@@ -268,20 +268,28 @@ int pinsage_output_mlp(const pinsage_mlp_t* mlp, const void* h, int64_t n, void*
 
 /* Max-margin loss, Eq. (1) (Sec. 3.3), with the expectation over negatives
  * taken as the mean over the shared negative set (500 per minibatch in the
- * paper):
- *   per_pair[b] = mean_n max(0, zq[b].zneg[n] - zq[b].zpos[b] + margin)
+ * paper) joined by the pair's own hard negatives (Sec. 3.3, "Hard negative
+ * items": they are added to each item's set of negatives):
+ *   per_pair[b] = mean over n in zneg u zhard[b] of
+ *                 max(0, zq[b].z_n - zq[b].zpos[b] + margin)
  *   *loss       = mean_b per_pair[b]
- * zq, zpos: device [B][d]; zneg: device [n_neg][d]; storage dtype `dtype`;
- * dot products and sums in fp32 in a fixed order. loss: device fp32 scalar;
+ * zq, zpos: device [B][d]; zneg: device [n_neg][d]; zhard: device
+ * [B][num_hard][d] or NULL when num_hard = 0; storage dtype `dtype`; dot
+ * products and sums in fp32 in a fixed order. loss: device fp32 scalar;
  * per_pair: device fp32 [B] (required: the mean is taken over it).
- * Limits: 1 <= B, 1 <= n_neg, 1 <= d <= 1024. */
+ * Limits: 1 <= B, 1 <= n_neg, 0 <= num_hard, 1 <= d <= 1024. */
 int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
-                            int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
-                            float* loss, float* per_pair, void* stream);
+                            int64_t n_neg, const void* zhard, int64_t num_hard, int32_t d,
+                            pinsage_dtype_t dtype, float margin, float* loss, float* per_pair,
+                            void* stream);
 
 /* Training pairs of one minibatch (Sec. 3.3): pair b is (queries[b],
  * positives[b]); every pair is scored against the same negatives (the shared
- * negative set of Sec. 3.3); margin is Delta of Eq. (1). Device int32 node ids. */
+ * negative set of Sec. 3.3) and against its own hard negatives
+ * hard_negatives[b][0..num_hard) (e.g. from pinsage_hard_negatives; ids
+ * outside [0, num_nodes), such as -1, are absent entries); margin is Delta of
+ * Eq. (1). Device int32 node ids; hard_negatives may be NULL when
+ * num_hard = 0. */
 typedef struct {
   int64_t num_pairs;
   int64_t num_negatives;
@@ -289,18 +297,22 @@ typedef struct {
   const int32_t* positives;
   const int32_t* negatives;
   float margin;
+  int64_t num_hard;
+  const int32_t* hard_negatives;
 } pinsage_pairs_t;
 
 /* Workspace bytes needed by pinsage_minibatch_forward (sized for the largest
- * frontiers: |S^(K)| <= 2B + n_neg, |S^(k-1)| <= |S^(k)| (T + 1), both <= N). */
+ * frontiers: |S^(K)| <= 2B + n_neg + B num_hard, |S^(k-1)| <= |S^(k)| (T + 1),
+ * both <= N). */
 int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_walk_params_t* walk,
                                      const pinsage_layer_t* layers, int32_t num_layers,
                                      const pinsage_mlp_t* mlp, int64_t num_pairs,
-                                     int64_t num_negatives, size_t* bytes);
+                                     int64_t num_negatives, int64_t num_hard, size_t* bytes);
 
 /* Minibatch forward of Algorithm 2 plus the loss of Eq. (1):
- *   S^(K) = queries u positives u negatives; S^(k-1) = S^(k) u N(S^(k))
+ *   S^(K) = queries u positives u negatives u hard negatives;
+ *   S^(k-1) = S^(k) u N(S^(k))
  *   (neighbourhoods sampled by the walks of pinsage_build_neighborhoods, so
  *   each equals the node's row of the all-node table); every set is sorted
  *   and de-duplicated on the device and neighbour ids are re-indexed into the
@@ -310,8 +322,9 @@ int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
  *   else z = h^(K); and the loss over the pairs on z.
  * x: device [num_nodes][layers[0].d_in]; mlp: NULL or d_in = the last
  * layer's d_out, same dtype; loss: device fp32 scalar; per_pair: device fp32
- * [B] or NULL; z_out: device [2B + n_neg][d] or NULL (d = mlp->d_out, or the
- * last layer's d_out) -- z of queries, then positives, then negatives;
+ * [B] or NULL; z_out: device [2B + n_neg + B num_hard][d] or NULL (d =
+ * mlp->d_out, or the last layer's d_out) -- z of queries, then positives, then
+ * negatives, then hard negatives (pair-major; zero rows for absent entries);
  * set_sizes: host int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|.
  * This call synchronises `stream` K + 1 times to size the frontiers.
  * Limits: as for the layers, plus d <= 1024. */

@@ -74,7 +74,8 @@ class MLP(ctypes.Structure):
 class Pairs(ctypes.Structure):
     _fields_ = [("num_pairs", ctypes.c_int64), ("num_negatives", ctypes.c_int64),
                 ("queries", ctypes.c_void_p), ("positives", ctypes.c_void_p),
-                ("negatives", ctypes.c_void_p), ("margin", ctypes.c_float)]
+                ("negatives", ctypes.c_void_p), ("margin", ctypes.c_float),
+                ("num_hard", ctypes.c_int64), ("hard_negatives", ctypes.c_void_p)]
 
 
 class PinsageError(RuntimeError):
@@ -117,12 +118,12 @@ def lib():
     L.pinsage_output_mlp_workspace_size.argtypes = [ctypes.POINTER(MLP), i64,
                                                     ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_output_mlp.argtypes = [ctypes.POINTER(MLP), P, i64, P, P, ctypes.c_size_t, P]
-    L.pinsage_max_margin_loss.argtypes = [P, P, i64, P, i64, i32, ctypes.c_int, ctypes.c_float,
-                                          P, P, P]
+    L.pinsage_max_margin_loss.argtypes = [P, P, i64, P, i64, P, i64, i32, ctypes.c_int,
+                                          ctypes.c_float, P, P, P]
     L.pinsage_minibatch_workspace_size.argtypes = [ctypes.POINTER(Graph),
                                                    ctypes.POINTER(WalkParams),
                                                    ctypes.POINTER(Layer), i32, ctypes.POINTER(MLP),
-                                                   i64, i64, ctypes.POINTER(ctypes.c_size_t)]
+                                                   i64, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_minibatch_forward.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                             ctypes.POINTER(Layer), i32, ctypes.POINTER(MLP), P,
                                             ctypes.POINTER(Pairs),

@@ -300,59 +300,76 @@ def embed_all(graph: DeviceGraph, layers: List[DeviceLayer], x: torch.Tensor, wa
 
 
 def max_margin_loss(zq: torch.Tensor, zpos: torch.Tensor, zneg: torch.Tensor, margin: float,
-                    stream=None):
-    """Eq. (1) with the mean over the shared negatives; returns (loss, per_pair)."""
+                    zhard: Optional[torch.Tensor] = None, stream=None):
+    """Eq. (1) with the mean over the shared negatives joined by each pair's
+    hard negatives zhard[b] ([B][k][d], optional); returns (loss, per_pair)."""
     dt = zq.dtype
     for t, n in ((zq, "zq"), (zpos, "zpos"), (zneg, "zneg")):
         _dev(t, n, dt)
     B, d = zq.shape
+    k = 0
+    if zhard is not None:
+        _dev(zhard, "zhard", dt)
+        if zhard.dim() != 3 or zhard.shape[0] != B or zhard.shape[2] != d:
+            raise ValueError("zhard must be [B][k][d]")
+        k = int(zhard.shape[1])
     loss = torch.empty(1, dtype=torch.float32, device=zq.device)
     per = torch.empty(B, dtype=torch.float32, device=zq.device)
-    st = L.lib().pinsage_max_margin_loss(_ptr(zq), _ptr(zpos), B, _ptr(zneg), zneg.shape[0], d,
-                                         _dtype_code(dt), margin, _ptr(loss), _ptr(per),
-                                         _stream(stream))
+    st = L.lib().pinsage_max_margin_loss(_ptr(zq), _ptr(zpos), B, _ptr(zneg), zneg.shape[0],
+                                         _ptr(zhard), k, d, _dtype_code(dt), margin, _ptr(loss),
+                                         _ptr(per), _stream(stream))
     L.check(st, "pinsage_max_margin_loss")
     return loss, per
 
 
 class Minibatch:
     """Minibatch forward of Algorithm 2 plus the loss of Eq. (1), with a
-    preallocated workspace sized for num_pairs pairs and num_negatives shared
-    negatives."""
+    preallocated workspace sized for num_pairs pairs, num_negatives shared
+    negatives and num_hard hard negatives per pair."""
 
     def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
                  T: int, seed: int, num_pairs: int, num_negatives: int,
-                 mlp: Optional[DeviceMLP] = None):
+                 mlp: Optional[DeviceMLP] = None, num_hard: int = 0):
         self.graph, self.layers = graph, list(layers)
         self.mlp = mlp
         self._mlp = mlp.struct() if mlp is not None else None
         self.walk = L.WalkParams(seed, walks, hops, T)
-        self.B, self.n_neg = int(num_pairs), int(num_negatives)
+        self.B, self.n_neg, self.k_hard = int(num_pairs), int(num_negatives), int(num_hard)
         self._g = graph.struct()
         self._layers = _layer_array(self.layers)
         n = ctypes.c_size_t(0)
         st = L.lib().pinsage_minibatch_workspace_size(ctypes.byref(self._g), ctypes.byref(self.walk),
                                                       self._layers, len(self.layers),
                                                       self._mlp_ref(), self.B, self.n_neg,
-                                                      ctypes.byref(n))
+                                                      self.k_hard, ctypes.byref(n))
         L.check(st, "pinsage_minibatch_workspace_size")
         dev = graph.col.device
         self.workspace = torch.empty(max(1, int(n.value)), dtype=torch.uint8, device=dev)
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)
         self.per_pair = torch.empty(self.B, dtype=torch.float32, device=dev)
         d = mlp.d_out if mlp is not None else self.layers[-1].d_out
-        self.z = torch.empty((2 * self.B + self.n_neg, d), dtype=self.layers[-1].dtype, device=dev)
+        self.z = torch.empty((2 * self.B + self.n_neg + self.B * self.k_hard, d),
+                             dtype=self.layers[-1].dtype, device=dev)
         self.set_sizes = (ctypes.c_int64 * (len(self.layers) + 1))()
 
     def run(self, x: torch.Tensor, queries: torch.Tensor, positives: torch.Tensor,
-            negatives: torch.Tensor, margin: float, want_z: bool = True, stream=None):
+            negatives: torch.Tensor, margin: float, want_z: bool = True,
+            hard: Optional[torch.Tensor] = None, stream=None):
+        """hard: int32 [num_pairs][num_hard] hard negatives (-1 = absent), required
+        when the workspace was made for num_hard > 0."""
         x = _dev(x, "x", self.layers[0].dtype)
         q = _dev(queries, "queries", torch.int32)
         p = _dev(positives, "positives", torch.int32)
         ng = _dev(negatives, "negatives", torch.int32)
         if q.numel() != self.B or p.numel() != self.B or ng.numel() != self.n_neg:
             raise ValueError("pair counts differ from the sizes this workspace was made for")
-        pairs = L.Pairs(self.B, self.n_neg, q.data_ptr(), p.data_ptr(), ng.data_ptr(), margin)
+        hp = None
+        if self.k_hard:
+            if hard is None or hard.numel() != self.B * self.k_hard:
+                raise ValueError(f"hard must hold num_pairs x {self.k_hard} ids")
+            hp = _dev(hard, "hard", torch.int32).data_ptr()
+        pairs = L.Pairs(self.B, self.n_neg, q.data_ptr(), p.data_ptr(), ng.data_ptr(), margin,
+                        self.k_hard, hp)
         st = L.lib().pinsage_minibatch_forward(ctypes.byref(self._g), ctypes.byref(self.walk),
                                                self._layers, len(self.layers), self._mlp_ref(),
                                                _ptr(x),

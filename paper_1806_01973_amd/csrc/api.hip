@@ -675,12 +675,15 @@ int pinsage_output_mlp(const pinsage_mlp_t* mlp, const void* h, int64_t n, void*
 }
 
 int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const void* zneg,
-                            int64_t n_neg, int32_t d, pinsage_dtype_t dtype, float margin,
-                            float* loss, float* per_pair, void* stream) {
+                            int64_t n_neg, const void* zhard, int64_t num_hard, int32_t d,
+                            pinsage_dtype_t dtype, float margin, float* loss, float* per_pair,
+                            void* stream) {
   g_last_error.clear();
   if (!zq || !zpos || !zneg || !loss || !per_pair)
     return fail(PINSAGE_EINVAL, "a pointer argument is NULL (per_pair is required)");
   if (B < 1 || n_neg < 1) return fail(PINSAGE_EINVAL, "need B >= 1 and n_neg >= 1");
+  if (num_hard < 0) return fail(PINSAGE_EINVAL, "negative num_hard");
+  if (num_hard > 0 && !zhard) return fail(PINSAGE_EINVAL, "zhard is NULL");
   if (d < 1 || d > 1024) return fail(PINSAGE_EUNSUPPORTED, "d %d outside [1, 1024]", d);
   if (dtype != PINSAGE_F32 && dtype != PINSAGE_BF16)
     return fail(PINSAGE_EINVAL, "unknown dtype %d", (int)dtype);
@@ -688,6 +691,8 @@ int pinsage_max_margin_loss(const void* zq, const void* zpos, int64_t B, const v
   a.zq = zq;
   a.zpos = zpos;
   a.zneg = zneg;
+  a.zhard = zhard;
+  a.k_hard = num_hard;
   a.B = B;
   a.n_neg = n_neg;
   a.d = d;
@@ -722,12 +727,12 @@ struct MbPlan {
 
 int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
               const pinsage_layer_t* layers, int K, const pinsage_mlp_t* mlp, int64_t B,
-              int64_t n_neg, MbPlan* p) {
+              int64_t n_neg, int64_t n_hard, MbPlan* p) {
   const int64_t N = g->num_pins + g->num_boards;
   p->K = K;
   p->T = w->top_t;
   p->N = N;
-  const int64_t nt = 2 * B + n_neg;
+  const int64_t nt = 2 * B + n_neg + B * n_hard;  // target ids (rows of the loss tables)
   p->U[K] = nt < N ? nt : N;
   for (int k = K; k >= 1; --k) {
     const int64_t grow = p->U[k] * (int64_t)(w->top_t + 1);
@@ -770,7 +775,7 @@ int make_plan(const pinsage_graph_t* g, const pinsage_walk_params_t* w,
 
 int check_minibatch(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                     const pinsage_layer_t* layers, int32_t K, const pinsage_mlp_t* mlp,
-                    int64_t B, int64_t n_neg) {
+                    int64_t B, int64_t n_neg, int64_t n_hard) {
   int st = check_graph(graph);
   if (st) return st;
   if ((st = check_walk(walk))) return st;
@@ -794,6 +799,9 @@ int check_minibatch(const pinsage_graph_t* graph, const pinsage_walk_params_t* w
   const int d = mlp ? mlp->d_out : layers[K - 1].d_out;
   if (d > 1024) return fail(PINSAGE_EUNSUPPORTED, "output dim %d > 1024", d);
   if (B < 1 || n_neg < 1) return fail(PINSAGE_EINVAL, "need num_pairs >= 1 and num_negatives >= 1");
+  if (n_hard < 0) return fail(PINSAGE_EINVAL, "negative num_hard");
+  if (n_hard > 0 && B > ((1ll << 40) / n_hard))
+    return fail(PINSAGE_EUNSUPPORTED, "num_pairs * num_hard too large");
   return PINSAGE_OK;
 }
 
@@ -814,13 +822,14 @@ int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_walk_params_t* walk,
                                      const pinsage_layer_t* layers, int32_t num_layers,
                                      const pinsage_mlp_t* mlp, int64_t num_pairs,
-                                     int64_t num_negatives, size_t* bytes) {
+                                     int64_t num_negatives, int64_t num_hard, size_t* bytes) {
   g_last_error.clear();
-  int st = check_minibatch(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives);
+  int st = check_minibatch(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives,
+                           num_hard);
   if (st) return st;
   if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
   MbPlan p;
-  make_plan(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives, &p);
+  make_plan(graph, walk, layers, num_layers, mlp, num_pairs, num_negatives, num_hard, &p);
   *bytes = p.total;
   return PINSAGE_OK;
 }
@@ -833,15 +842,17 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
                               size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!pairs) return fail(PINSAGE_EINVAL, "pairs is NULL");
-  const int64_t B = pairs->num_pairs, n_neg = pairs->num_negatives;
+  const int64_t B = pairs->num_pairs, n_neg = pairs->num_negatives, n_hard = pairs->num_hard;
   const int K = num_layers;
-  int st = check_minibatch(graph, walk, layers, K, mlp, B, n_neg);
+  int st = check_minibatch(graph, walk, layers, K, mlp, B, n_neg, n_hard);
   if (st) return st;
   if (!pairs->queries || !pairs->positives || !pairs->negatives)
     return fail(PINSAGE_EINVAL, "pair id arrays must not be NULL");
+  if (n_hard > 0 && !pairs->hard_negatives)
+    return fail(PINSAGE_EINVAL, "hard_negatives is NULL with num_hard > 0");
   if (!x || !loss) return fail(PINSAGE_EINVAL, "x or loss is NULL");
   MbPlan p;
-  make_plan(graph, walk, layers, K, mlp, B, n_neg, &p);
+  make_plan(graph, walk, layers, K, mlp, B, n_neg, n_hard, &p);
   if (!workspace || workspace_bytes < p.total)
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes,
                 p.total);
@@ -910,10 +921,13 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
   PINSAGE_TRY(launch_mark(pairs->queries, B, N, flags, s), "mark");
   PINSAGE_TRY(launch_mark(pairs->positives, B, N, flags, s), "mark");
   PINSAGE_TRY(launch_mark(pairs->negatives, n_neg, N, flags, s), "mark");
+  PINSAGE_TRY(launch_mark(pairs->hard_negatives, B * n_hard, N, flags, s), "mark");
   if ((st = scan_level(K))) return st;
   PINSAGE_TRY(launch_remap(pairs->queries, B, N, pos, rows, s), "remap");
   PINSAGE_TRY(launch_remap(pairs->positives, B, N, pos, rows + B, s), "remap");
   PINSAGE_TRY(launch_remap(pairs->negatives, n_neg, N, pos, rows + 2 * B, s), "remap");
+  PINSAGE_TRY(launch_remap(pairs->hard_negatives, B * n_hard, N, pos, rows + 2 * B + n_neg, s),
+              "remap");
   if ((st = walk_level(K))) return st;
   // Levels K-1 .. 0: S^(k) = S^(k+1) u N(S^(k+1)); re-index level k+1.
   for (int k = K - 1; k >= 0; --k) {
@@ -962,6 +976,9 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
   la.pos_rows = rows + B;
   la.zneg = zsrc;
   la.neg_rows = rows + 2 * B;
+  la.zhard = zsrc;
+  la.hard_rows = rows + 2 * B + n_neg;
+  la.k_hard = n_hard;
   la.B = B;
   la.n_neg = n_neg;
   la.d = d;
@@ -971,7 +988,7 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
   la.loss = loss;
   PINSAGE_TRY(launch_loss(la, s), "loss launch");
   if (z_out)
-    PINSAGE_TRY(launch_gather_rows(zsrc, rows, 2 * B + n_neg,
+    PINSAGE_TRY(launch_gather_rows(zsrc, rows, 2 * B + n_neg + B * n_hard,
                                    (int64_t)d * elem_size(LK->dtype), z_out, s),
                 "target gather");
   if (set_sizes)

@@ -116,9 +116,11 @@ struct GemmLaunch {
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
 
-// Max-margin loss (Eq. 1): per_pair[b] = mean_n max(0, zq.zn - zq.zpos + margin),
-// *loss = mean_b per_pair[b]. Row maps index the three tables (NULL =
-// identity; negative entries read as zero vectors). d <= 1024.
+// Max-margin loss (Eq. 1): per_pair[b] = mean over the shared negatives and
+// pair b's present hard negatives of max(0, zq.zn - zq.zpos + margin),
+// *loss = mean_b per_pair[b]. Row maps index the tables (NULL = identity;
+// negative entries read as zero vectors, except hard rows, where they mark an
+// absent entry). d <= 1024.
 struct LossLaunch {
   const void* zq;
   const int32_t* q_rows;
@@ -126,6 +128,9 @@ struct LossLaunch {
   const int32_t* pos_rows;
   const void* zneg;
   const int32_t* neg_rows;
+  const void* zhard;         // [B * k_hard rows], row b * k_hard + j of pair b
+  const int32_t* hard_rows;  // nullable: identity
+  int64_t k_hard;
   int64_t B;
   int64_t n_neg;
   int d;

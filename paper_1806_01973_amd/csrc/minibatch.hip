@@ -253,7 +253,29 @@ __global__ __launch_bounds__(THREADS) void loss_pairs_kernel(LossLaunch a) {
     for (int o = TPQ / 2; o >= 1; o >>= 1) hc += __shfl_xor(hc, o);
     acc += hc;
   }
-  if (c == 0 && b < a.B) a.per_pair[b] = acc / (float)a.n_neg;
+  // Pair b's own hard negatives (Sec. 3.3): thread c takes entries c, c + TPQ,
+  // ... and forms each dot product over d in index order from the row in
+  // memory; hinge sums and the count of present entries go through the same
+  // butterfly.
+  float hh = 0.0f;
+  int hv = 0;
+  for (int64_t j = c; j < a.k_hard; j += TPQ) {
+    int64_t row = -1;
+    if (b < a.B) row = a.hard_rows ? (int64_t)a.hard_rows[b * a.k_hard + j] : b * a.k_hard + j;
+    if (row < 0) continue;
+    const float* zq = zq_s + q * S;
+    float dn = 0.0f;
+    for (int k = 0; k < d; ++k) dn = fmaf(zq[k], load_elem<BF16>(a.zhard, row * d + k), dn);
+    const float h = dn - pos + a.margin;
+    hh += h > 0.0f ? h : 0.0f;
+    ++hv;
+  }
+#pragma unroll
+  for (int o = TPQ / 2; o >= 1; o >>= 1) {
+    hh += __shfl_xor(hh, o);
+    hv += __shfl_xor(hv, o);
+  }
+  if (c == 0 && b < a.B) a.per_pair[b] = (acc + hh) / (float)(a.n_neg + hv);
 }
 
 // Mean over pairs in a fixed order: strided per-thread sums, then a fixed tree.

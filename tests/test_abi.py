@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 4
+    assert lib.pinsage_version() == 5
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -180,7 +180,7 @@ def test_minibatch_validation_and_workspace(L):
     walk = L.WalkParams(1, 10, 2, 4)
     layers = (L.Layer * 2)(_layer(L), _layer(L))
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                None, 3, 2, ctypes.byref(n)) == 0
+                                                None, 3, 2, 0, ctypes.byref(n)) == 0
     # Frontier capacities: U2 = min(15, 2*3+2) = 8, U1 = U0 = 15 (capped by N).
     a = lambda b: (b + 255) // 256 * 256
     U = [15, 15, 8]
@@ -192,25 +192,51 @@ def test_minibatch_validation_and_workspace(L):
     want += a(conv)
     assert n.value == want
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                None, 0, 2, ctypes.byref(n)) == L.PINSAGE_EINVAL
+                                                None, 0, 2, 0, ctypes.byref(n)) == L.PINSAGE_EINVAL
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 9,
-                                                None, 3, 2, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
-    pairs = L.Pairs(3, 2, FAKE, None, FAKE, 0.1)
+                                                None, 3, 2, 0, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                None, 3, 2, -1, ctypes.byref(n)) == L.PINSAGE_EINVAL
+    # Hard negatives widen the level-K capacity: U2 = min(15, 2*3+2+3*2) = 14,
+    # and the target row table to 14 entries.
+    n_h = ctypes.c_size_t(0)
+    assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
+                                                None, 3, 2, 2, ctypes.byref(n_h)) == 0
+    Uh = [15, 15, 14]
+    want_h = a(15) + a(60) + a(4) + a(64) + sum(a(u * 4) for u in Uh)
+    for k in (1, 2):
+        want_h += (a(Uh[k] * 4 * 4) + a(Uh[k] * 4 * 2) + a(Uh[k] * 4 * 4) + a(Uh[k] * 4) +
+                   a(Uh[k] * 64 * 4))
+    want_h += a(14 * 4) + a(3 * 4)
+    want_h += a(max(a(Uh[k - 1] * 128 * 4) + a(Uh[k] * 128 * 4) for k in (1, 2)))
+    assert n_h.value == want_h
+    pairs = L.Pairs(3, 2, FAKE, None, FAKE, 0.1, 0, None)
     st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
                                        ctypes.byref(pairs), FAKE, None, None, None, FAKE,
                                        1 << 30, None)
     assert st == L.PINSAGE_EINVAL
-    pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1)
+    pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1, 0, None)
     st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
                                        ctypes.byref(pairs), FAKE, None, None, None, FAKE, 16, None)
     assert st == L.PINSAGE_EWORKSPACE
-    # Standalone loss: per_pair is required, d is bounded.
-    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, 64, L.PINSAGE_F32, 0.1, FAKE, None,
-                                     None)
+    pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1, 2, None)  # hard negatives missing
+    st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
+                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE,
+                                       1 << 30, None)
     assert st == L.PINSAGE_EINVAL
-    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, 2048, L.PINSAGE_F32, 0.1, FAKE, FAKE,
-                                     None)
+    # Standalone loss: per_pair is required, d is bounded.
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, None, 0, 64, L.PINSAGE_F32, 0.1,
+                                     FAKE, None, None)
+    assert st == L.PINSAGE_EINVAL
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, None, 0, 2048, L.PINSAGE_F32, 0.1,
+                                     FAKE, FAKE, None)
     assert st == L.PINSAGE_EUNSUPPORTED
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, None, 3, 64, L.PINSAGE_F32, 0.1,
+                                     FAKE, FAKE, None)
+    assert st == L.PINSAGE_EINVAL  # zhard missing
+    st = lib.pinsage_max_margin_loss(FAKE, FAKE, 4, FAKE, 5, FAKE, -1, 64, L.PINSAGE_F32, 0.1,
+                                     FAKE, FAKE, None)
+    assert st == L.PINSAGE_EINVAL
 
 
 def _mlp(L, **kw):
@@ -241,13 +267,13 @@ def test_output_mlp_validation(L):
     layers = (L.Layer * 2)(_layer(L), _layer(L))
     bad = _mlp(L, d_in=32)
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                ctypes.byref(bad), 3, 2, ctypes.byref(n)) == \
+                                                ctypes.byref(bad), 3, 2, 0, ctypes.byref(n)) == \
         L.PINSAGE_EINVAL
     ok = _mlp(L, d_in=64)
     n0 = ctypes.c_size_t(0)
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                None, 3, 2, ctypes.byref(n0)) == 0
+                                                None, 3, 2, 0, ctypes.byref(n0)) == 0
     assert lib.pinsage_minibatch_workspace_size(ctypes.byref(g), ctypes.byref(walk), layers, 2,
-                                                ctypes.byref(ok), 3, 2, ctypes.byref(n)) == 0
+                                                ctypes.byref(ok), 3, 2, 0, ctypes.byref(n)) == 0
     a = lambda b: (b + 255) // 256 * 256
     assert n.value == n0.value + a(8 * 32 * 4) + a(8 * 96 * 4)  # z and hidden rows of S^(2)
