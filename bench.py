@@ -370,7 +370,20 @@ def bench_minibatch(args, wl, inp):
     timed_sizes = np.array(sizes[args.warmup:], dtype=np.float64)
     mean_sizes = timed_sizes.mean(axis=0).tolist()
     value = B * args.steps / elapsed
-    extra = {"walk_steps_per_s": None,
+    # Edge steps of the timed steps' walks (deterministic per minibatch): the
+    # timed minibatches again, outside the timed region.
+    edge_steps = 0
+    for i in range(args.warmup, args.warmup + args.steps):
+        run(i)
+        edge_steps += int(mb.steps.item())
+    edge_steps /= args.steps
+    kd = kernels["walk_topt"]
+    off_b = 8 if wl.offsets64 else 4
+    kd["edge_steps_per_launch"] = edge_steps / (kd["launches"] / args.steps)
+    kd["algo_bytes_per_launch"] = kd["edge_steps_per_launch"] * (2 * off_b + 4)
+    kd["achieved_GBs"] = kd["algo_bytes_per_launch"] / (kd["avg_ms"] * 1e-3) / 1e9
+    kd["edge_steps_per_s"] = kd["edge_steps_per_launch"] / (kd["avg_ms"] * 1e-3)
+    extra = {"walk_steps_per_s": edge_steps / (kd["ms_per_step"] * 1e-3),
              "config_extra": {"pairs": B, "negatives": n_neg, "margin": 0.1,
                               "hard_negatives_per_pair": k,
                               "mean_frontier_sizes": mean_sizes,

@@ -325,15 +325,16 @@ int pinsage_minibatch_workspace_size(const pinsage_graph_t* graph,
  * [B] or NULL; z_out: device [2B + n_neg + B num_hard][d] or NULL (d =
  * mlp->d_out, or the last layer's d_out) -- z of queries, then positives, then
  * negatives, then hard negatives (pair-major; zero rows for absent entries);
- * set_sizes: host int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|.
+ * set_sizes: host int64 [K + 1] or NULL -- |S^(0)|, ..., |S^(K)|;
+ * total_steps: device uint64 or NULL -- edge steps of all walks of the call.
  * This call synchronises `stream` K + 1 times to size the frontiers.
  * Limits: as for the layers, plus d <= 1024. */
 int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                               const pinsage_layer_t* layers, int32_t num_layers,
                               const pinsage_mlp_t* mlp, const void* x,
                               const pinsage_pairs_t* pairs, float* loss, float* per_pair,
-                              void* z_out, int64_t* set_sizes, void* workspace,
-                              size_t workspace_bytes, void* stream);
+                              void* z_out, int64_t* set_sizes, unsigned long long* total_steps,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Per-kernel timing (hipEvents recorded around every launch on the launch
  * stream). pinsage_profile_enable(1) clears and starts collection;

@@ -127,7 +127,7 @@ def lib():
     L.pinsage_minibatch_forward.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                             ctypes.POINTER(Layer), i32, ctypes.POINTER(MLP), P,
                                             ctypes.POINTER(Pairs),
-                                            P, P, P, ctypes.POINTER(ctypes.c_int64), P,
+                                            P, P, P, ctypes.POINTER(ctypes.c_int64), P, P,
                                             ctypes.c_size_t, P]
     L.pinsage_profile_enable.argtypes = [ctypes.c_int]
     L.pinsage_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int64),

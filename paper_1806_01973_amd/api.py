@@ -351,6 +351,7 @@ class Minibatch:
         self.z = torch.empty((2 * self.B + self.n_neg + self.B * self.k_hard, d),
                              dtype=self.layers[-1].dtype, device=dev)
         self.set_sizes = (ctypes.c_int64 * (len(self.layers) + 1))()
+        self.steps = torch.zeros(1, dtype=torch.int64, device=dev)  # edge steps of the last run
 
     def run(self, x: torch.Tensor, queries: torch.Tensor, positives: torch.Tensor,
             negatives: torch.Tensor, margin: float, want_z: bool = True,
@@ -376,7 +377,8 @@ class Minibatch:
                                                ctypes.byref(pairs), _ptr(self.loss),
                                                _ptr(self.per_pair),
                                                _ptr(self.z) if want_z else None, self.set_sizes,
-                                               _ptr(self.workspace), self.workspace.numel(),
+                                               _ptr(self.steps), _ptr(self.workspace),
+                                               self.workspace.numel(),
                                                _stream(stream))
         L.check(st, "pinsage_minibatch_forward")
         return self.loss

@@ -838,8 +838,8 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
                               const pinsage_layer_t* layers, int32_t num_layers,
                               const pinsage_mlp_t* mlp, const void* x,
                               const pinsage_pairs_t* pairs, float* loss, float* per_pair,
-                              void* z_out, int64_t* set_sizes, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+                              void* z_out, int64_t* set_sizes, unsigned long long* total_steps,
+                              void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!pairs) return fail(PINSAGE_EINVAL, "pairs is NULL");
   const int64_t B = pairs->num_pairs, n_neg = pairs->num_negatives, n_hard = pairs->num_hard;
@@ -897,7 +897,7 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
     a.idx = nidx_of(k);
     a.counts = reinterpret_cast<uint16_t*>(ws + p.ncnt[k]);
     a.weights = reinterpret_cast<float*>(ws + p.nw[k]);
-    a.total_steps = nullptr;
+    a.total_steps = total_steps;  // accumulated over the levels
     PINSAGE_TRY(launch_walk_topt(a, s), "walk launch");
     return PINSAGE_OK;
   };
@@ -916,6 +916,7 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
     return PINSAGE_OK;
   };
 
+  if (total_steps) PINSAGE_TRY(launch_zero_u64(total_steps, 1, s), "step counter reset");
   // Level K: the targets of the minibatch (Algorithm 2, S^(K) = M).
   PINSAGE_TRY(launch_fill_zero_u8(flags, N, s), "flag reset");
   PINSAGE_TRY(launch_mark(pairs->queries, B, N, flags, s), "mark");

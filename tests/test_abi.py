@@ -212,16 +212,17 @@ def test_minibatch_validation_and_workspace(L):
     assert n_h.value == want_h
     pairs = L.Pairs(3, 2, FAKE, None, FAKE, 0.1, 0, None)
     st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
-                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE,
+                                       ctypes.byref(pairs), FAKE, None, None, None, None, FAKE,
                                        1 << 30, None)
     assert st == L.PINSAGE_EINVAL
     pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1, 0, None)
     st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
-                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE, 16, None)
+                                       ctypes.byref(pairs), FAKE, None, None, None, None, FAKE, 16,
+                                       None)
     assert st == L.PINSAGE_EWORKSPACE
     pairs = L.Pairs(3, 2, FAKE, FAKE, FAKE, 0.1, 2, None)  # hard negatives missing
     st = lib.pinsage_minibatch_forward(ctypes.byref(g), ctypes.byref(walk), layers, 2, None, FAKE,
-                                       ctypes.byref(pairs), FAKE, None, None, None, FAKE,
+                                       ctypes.byref(pairs), FAKE, None, None, None, None, FAKE,
                                        1 << 30, None)
     assert st == L.PINSAGE_EINVAL
     # Standalone loss: per_pair is required, d is bounded.
