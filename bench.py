@@ -62,7 +62,8 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash(name: str) -> str:
-    """Hash of a kernel source file and the local headers it includes."""
+    """Hash of a kernel source file and the local device headers it includes
+    (kernels.h, the host-side launch declarations, is left out)."""
     csrc = os.path.join(ROOT, "paper_1806_01973_amd", "csrc")
     h = hashlib.sha256()
     with open(os.path.join(csrc, name), "rb") as f:
@@ -70,7 +71,7 @@ def kernel_source_hash(name: str) -> str:
     h.update(text)
     for line in text.decode().splitlines():
         line = line.strip()
-        if line.startswith('#include "'):
+        if line.startswith('#include "') and line.split('"')[1] != "kernels.h":
             inc = os.path.join(csrc, line.split('"')[1])
             if os.path.exists(inc):
                 with open(inc, "rb") as f:
