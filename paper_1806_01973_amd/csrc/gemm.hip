@@ -418,9 +418,11 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
 // request is a full 128-byte line. Chunks travel global -> VGPR -> LDS: two
 // register buffers keep chunks c + 2 and c + 3 in flight while chunk c is
 // multiplied from one LDS stage and chunk c + 1 waits in the other. In a row
-// of a stage, 16-byte vector v sits in slot v ^ (row & 7): the 8 lanes that
-// write one row and the rows read by one fragment instruction both fall on
-// distinct banks. Missing rows and the K tail load from the zero row.
+// of a stage, 16-byte vector v sits in slot v ^ ((row >> 1) & 7): a 16-byte
+// access is served 16 lanes at a time from 64 banks (two 128-byte rows), so
+// the 16 lanes that write two rows, and the 16 rows read by a fragment
+// instruction's lane group, fall on distinct banks. Missing rows and the K
+// tail read zeros through the buffer descriptors' range checks.
 // ---------------------------------------------------------------------------
 template <int WAVES_M_, int WAVES_N_>
 struct RsCfg {
@@ -516,8 +518,9 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
                        b_rsrc, (b_off0 + (i - LOADS / 2) * b_step + koff) | oob, 0, 0));
     }
   };
-  // Row (r0 + RSTEP i) & 7 == r0 & 7: one slot for all of this thread's rows.
-  const int wslot = (v ^ (r0 & 7)) * 16;
+  // ((r0 + RSTEP i) >> 1) & 7 == (r0 >> 1) & 7: one slot for all of this
+  // thread's rows.
+  const int wslot = (v ^ ((r0 >> 1) & 7)) * 16;
   auto store_chunk = [&](int stage, const u32x4 (&r)[LOADS]) __attribute__((always_inline)) {
     unsigned char* base = smem + stage * STAGE_BYTES + r0 * ROW_BYTES + wslot;
 #pragma unroll
@@ -549,7 +552,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
   };
   auto read_frags = [&](int stage, int ks, Frags& f) __attribute__((always_inline)) {
     const unsigned char* st = smem + stage * STAGE_BYTES;
-    const int slot = ((2 * ks + half) ^ (frow & 7)) * 16;
+    const int slot = ((2 * ks + half) ^ ((frow >> 1) & 7)) * 16;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
       f.a[i] = *reinterpret_cast<const u32x4*>(st + fa + i * 32 * ROW_BYTES + slot);
