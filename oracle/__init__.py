@@ -77,6 +77,8 @@ def _load():
     lib.orc_minibatch_embed_sampled.argtypes = [P, i64, i32, P, i64, P, i32, P, i64, P, P, i32,
                                                 P, P, P, P, P, P, P, i32, P]
     lib.orc_minibatch_embed_sampled.restype = None
+    lib.orc_graph_neighborhoods.argtypes = [P, P, i64, u64, i32, P, i64, P, P, P, i32]
+    lib.orc_graph_neighborhoods.restype = None
     lib.orc_hard_negatives.argtypes = [P, P, i64, i64, u64, i32, i32, P, i64, i32, i32, i32, P,
                                        i32]
     lib.orc_hard_negatives.restype = None
@@ -146,6 +148,37 @@ def build_neighborhoods(offsets, col, num_pins, seed, walks, hops, T, sources=No
                                 _ptr(src), ns, _ptr(idx), _ptr(cnt), _ptr(wts), _ptr(steps),
                                 nthreads or default_threads())
     return idx, cnt, wts, int(steps[0])
+
+
+def graph_neighborhoods(offsets, col, seed, T, sources=None, nthreads=None):
+    """Sec. 3.4 MapReduce neighbourhoods: each node's CSR row (sampled with T
+    draws when longer than T), distinct ids ascending with multiplicities and
+    weights multiplicity / kept entries: (idx int32, counts uint16, weights fp32)."""
+    lib = _load()
+    off = _c(offsets, np.int64)
+    cl = _c(col, np.int32)
+    n_nodes = len(off) - 1
+    src = None if sources is None else _c(sources, np.int32)
+    ns = n_nodes if src is None else len(src)
+    idx = np.empty((ns, T), np.int32)
+    cnt = np.empty((ns, T), np.uint16)
+    wts = np.empty((ns, T), np.float32)
+    lib.orc_graph_neighborhoods(_ptr(off), _ptr(cl), n_nodes, seed, T, _ptr(src), ns, _ptr(idx),
+                                _ptr(cnt), _ptr(wts), nthreads or default_threads())
+    return idx, cnt, wts
+
+
+def embed_all_bipartite(x_pins, num_nodes, layers, idx, wts, nthreads=None):
+    """Sec. 3.4 MapReduce inference on the bipartite graph: boards have no
+    features (h^(0) of a board is the zero vector), every node may be a
+    neighbour, so all rows are projected at each layer; K layers, layer-wise."""
+    xp = _c(x_pins, np.float64)
+    h = np.zeros((num_nodes, xp.shape[1]), np.float64)
+    h[: xp.shape[0]] = xp
+    for L in layers:
+        h = convolve_layer(h, num_nodes, L["Q"], L["q"], L["W"], L["w"], idx, wts,
+                           nthreads=nthreads, pool=L.get("pool", "importance"))
+    return h
 
 
 POOLS = {"importance": 0, "mean": 1, "max": 2}

@@ -20,6 +20,8 @@
 //                              mean and max of the compared variants (Sec. 4).
 //   * output dense layers .... Algorithm 2, final loop: z = G2 ReLU(G1 h + g).
 //   * hard negative items .... Sec. 3.3 (PPR rank window, sampled).
+//   * graph neighbourhoods ... Sec. 3.4 (MapReduce: boards pool their pins,
+//                              pins their boards; long rows sampled).
 //
 // Readings of points the paper leaves open are listed in the repository's
 // design notes; the ones that change arithmetic are restated at each function.
@@ -307,6 +309,60 @@ void orc_build_neighborhoods(const int64_t* off, const int32_t* col, int64_t num
   int64_t total = 0;
   for (int64_t s : steps_per_thread) total += s;
   if (total_steps) *total_steps = total;
+}
+
+// Sec. 3.4, MapReduce inference: a board's embedding pools the pins it holds
+// and, one layer up, a pin's pools its boards (the graph's own adjacency, with
+// neighbours "sampled"). Readings: node u's neighbourhood is its CSR row when
+// the row has at most T entries (each once); a longer row is sampled with T
+// independent draws, draw j taking word 0 of Philox4x32-10 at counter
+// (u, j, 0, 2) under the key (lo32(seed), hi32(seed)) and picking row position
+// floor(r * deg / 2^32). Entries outside [0, num_nodes) are dropped. The table
+// row lists the distinct ids ascending with their multiplicities; the weights
+// are multiplicity / (entries kept), one fp32 division (the degree-normalised
+// mean of the row or of the sample). Padding: -1, 0, 0.
+void orc_graph_neighborhoods(const int64_t* off, const int32_t* col, int64_t num_nodes,
+                             uint64_t seed, int T, const int32_t* sources, int64_t num_sources,
+                             int32_t* idx, uint16_t* cnt, float* wts, int nthreads) {
+  const uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+  parallel_rows(num_sources, nthreads, [&](int64_t lo, int64_t hi) {
+    std::vector<int32_t> picked;
+    for (int64_t r = lo; r < hi; ++r) {
+      const int64_t u = sources ? (int64_t)sources[r] : r;
+      for (int t = 0; t < T; ++t) {
+        idx[r * T + t] = -1;
+        cnt[r * T + t] = 0;
+        wts[r * T + t] = 0.0f;
+      }
+      if (u < 0 || u >= num_nodes) continue;
+      const int64_t b = off[u], deg = off[u + 1] - off[u];
+      picked.clear();
+      if (deg <= T) {
+        for (int64_t i = 0; i < deg; ++i) picked.push_back(col[b + i]);
+      } else {
+        for (int j = 0; j < T; ++j) {
+          const uint32_t ctr[4] = {(uint32_t)u, (uint32_t)j, 0u, 2u};
+          uint32_t rr[4];
+          philox4x32_10(ctr, key, rr);
+          picked.push_back(col[b + (int64_t)(((uint64_t)rr[0] * (uint64_t)deg) >> 32)]);
+        }
+      }
+      std::map<int32_t, int64_t> mult;
+      int64_t kept = 0;
+      for (int32_t v : picked)
+        if (v >= 0 && (int64_t)v < num_nodes) {
+          mult[v] += 1;
+          ++kept;
+        }
+      int t = 0;
+      for (const auto& kv : mult) {  // ascending id
+        idx[r * T + t] = kv.first;
+        cnt[r * T + t] = (uint16_t)kv.second;
+        wts[r * T + t] = (float)kv.second / (float)kept;
+        ++t;
+      }
+    }
+  });
 }
 
 // One CONVOLVE layer over a set of output rows, in the layer-wise dataflow of
