@@ -10,7 +10,9 @@
  *      layer by layer so that each node's transformed vector is computed once
  *      (Sec. 3.4),
  *   3. the minibatch forward of Algorithm 2 with the max-margin loss (Eq. 1),
- *   4. hard negative items for training queries (Sec. 3.3).
+ *   4. hard negative items for training queries (Sec. 3.3),
+ *   5. the MapReduce-inference variant of Sec. 3.4 (boards pool their pins,
+ *      pins their boards, boards without features).
  *
  * Conventions shared by every entry point
  *   - Graph (Sec. 3.1): a bipartite graph of pins I and boards C, V = I u C.
@@ -39,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 5
+#define PINSAGE_ABI_VERSION 6
 
 enum {
   PINSAGE_OK = 0,
@@ -214,6 +216,42 @@ int pinsage_hard_negatives(const pinsage_graph_t* graph,
                            const int32_t* queries, int64_t num_queries, int32_t* out,
                            unsigned long long* total_steps, void* stream);
 
+/* Graph neighbourhoods of the MapReduce inference (Sec. 3.4): a board's
+ * embedding pools the pins it holds and a pin's the boards it occurs on,
+ * with neighbours sampled. Node u's neighbourhood is its CSR row if the row
+ * has at most T = out->top_t entries; a longer row is sampled with T
+ * independent draws, draw j taking word 0 of Philox4x32-10 (Salmon et al.,
+ * SC'11) at counter (u, j, 0, 2) under the key (lo32(seed), hi32(seed)) and
+ * the row position floor(r * deg / 2^32). Entries outside [0, num_nodes) are
+ * dropped. Row r of `out` (for sources[r], or node r when sources is NULL,
+ * then num_sources = num_nodes) lists the distinct ids ascending: idx, counts
+ * = multiplicity, weights = multiplicity / kept entries (one fp32 division;
+ * NULL = not written); padding -1, 0, 0. A source outside [0, num_nodes)
+ * yields a padding row. Limits: 1 <= T <= 256. */
+int pinsage_build_graph_neighborhoods(const pinsage_graph_t* graph, uint64_t seed,
+                                      const int32_t* sources, int64_t num_sources,
+                                      pinsage_neighborhoods_t* out, void* stream);
+
+/* Workspace bytes needed by pinsage_embed_all_bipartite. */
+int pinsage_embed_all_bipartite_workspace_size(const pinsage_graph_t* graph,
+                                               const pinsage_layer_t* layers,
+                                               int32_t num_layers, size_t* bytes);
+
+/* All-node embedding in the MapReduce inference of Sec. 3.4: graph
+ * neighbourhoods of every node (pinsage_build_graph_neighborhoods with
+ * T = nbr_out->top_t), then num_layers CONVOLVE layers over all nodes, layer
+ * by layer. Only pins have features (boards' h^(0) is the zero vector), so
+ * the number of layers must be even (pins' outputs then rest on pin
+ * features); every node can be a neighbour, so each layer projects all
+ * num_nodes rows. x_pins: device [num_pins][layers[0].d_in]; h_out: device
+ * [num_nodes][layers[K-1].d_out]; nbr_out: rows = num_nodes (weights may be
+ * NULL). Layers chain as in pinsage_embed_all; one storage dtype. */
+int pinsage_embed_all_bipartite(const pinsage_graph_t* graph, uint64_t seed,
+                                const pinsage_layer_t* layers, int32_t num_layers,
+                                const void* x_pins, pinsage_neighborhoods_t* nbr_out,
+                                void* h_out, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
 /* Workspace bytes needed by pinsage_convolve_layer for these sizes. */
 int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
                                     int64_t n_out, size_t* bytes);
@@ -351,7 +389,8 @@ enum {
   PINSAGE_KERNEL_GEMM_R = 6, /* neighbour half of W per pin (DENSE_THEN_POOL) */
   PINSAGE_KERNEL_MLP = 7,    /* output dense layers */
   PINSAGE_KERNEL_HARD_NEG = 8,
-  PINSAGE_KERNEL_COUNT = 9
+  PINSAGE_KERNEL_GRAPH_NBR = 9, /* graph neighbourhoods (MapReduce variant) */
+  PINSAGE_KERNEL_COUNT = 10
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

@@ -12,8 +12,10 @@ from .api import (  # noqa: F401
     DeviceLayer,
     DeviceMLP,
     EmbedAll,
+    EmbedAllBipartite,
     Minibatch,
     Neighborhoods,
+    build_graph_neighborhoods,
     build_neighborhoods,
     convolve_layer,
     convolve_workspace_size,

@@ -23,11 +23,13 @@ POOLS = {"importance": 0, "mean": 1, "max": 2}
 (KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
  KERNEL_GEMM_R, KERNEL_MLP) = range(8)
 KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp",
-                "hard_neg"]
+                "hard_neg", "graph_nbr"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
-    "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
+    "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_build_graph_neighborhoods",
+    "pinsage_embed_all_bipartite_workspace_size", "pinsage_embed_all_bipartite",
+    "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
     "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_output_mlp_workspace_size",
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
@@ -96,13 +98,21 @@ def lib():
         raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                            "`python -c 'import __graft_entry__ as g; g.build()'`")
     L = ctypes.CDLL(LIB_PATH)
-    P, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    P, i64, i32, u64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
     L.pinsage_version.restype = ctypes.c_int
     L.pinsage_status_string.argtypes = [ctypes.c_int]
     L.pinsage_status_string.restype = ctypes.c_char_p
     L.pinsage_last_error.restype = ctypes.c_char_p
     L.pinsage_build_neighborhoods.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                               P, i64, ctypes.POINTER(Neighborhoods), P, P]
+    L.pinsage_build_graph_neighborhoods.argtypes = [ctypes.POINTER(Graph), u64, P, i64,
+                                                    ctypes.POINTER(Neighborhoods), P]
+    L.pinsage_embed_all_bipartite_workspace_size.argtypes = [ctypes.POINTER(Graph),
+                                                             ctypes.POINTER(Layer), i32,
+                                                             ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_embed_all_bipartite.argtypes = [ctypes.POINTER(Graph), u64, ctypes.POINTER(Layer),
+                                              i32, P, ctypes.POINTER(Neighborhoods), P, P,
+                                              ctypes.c_size_t, P]
     L.pinsage_hard_negatives.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(HardNegativeParams),
                                          P, i64, P, P, P]
     L.pinsage_convolve_workspace_size.argtypes = [ctypes.POINTER(Layer), i64, i64,

@@ -292,6 +292,57 @@ class EmbedAll:
         return self.out
 
 
+def build_graph_neighborhoods(graph: DeviceGraph, T: int, seed: int,
+                              sources: Optional[torch.Tensor] = None, weights: bool = True,
+                              out: Optional[Neighborhoods] = None, stream=None) -> Neighborhoods:
+    """Graph neighbourhoods of the MapReduce inference (Sec. 3.4): CSR rows, or
+    T Philox draws from rows longer than T, distinct ids ascending."""
+    if sources is not None:
+        sources = _dev(sources, "sources", torch.int32)
+    rows = graph.num_nodes if sources is None else int(sources.numel())
+    nb = out if out is not None else Neighborhoods.empty(rows, T, weights, graph.col.device)
+    g, ns = graph.struct(), nb.struct()
+    st = L.lib().pinsage_build_graph_neighborhoods(ctypes.byref(g), seed, _ptr(sources), rows,
+                                                   ctypes.byref(ns), _stream(stream))
+    L.check(st, "pinsage_build_graph_neighborhoods")
+    return nb
+
+
+class EmbedAllBipartite:
+    """Preallocated all-node job of the MapReduce inference (Sec. 3.4): graph
+    neighbourhoods, then an even number of layers over all nodes with
+    featureless boards; x holds the pins' features only."""
+
+    def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], T: int, seed: int,
+                 weights: bool = True):
+        self.graph, self.layers, self.seed = graph, list(layers), int(seed)
+        dev = graph.col.device
+        self.nbr = Neighborhoods.empty(graph.num_nodes, T, weights, dev)
+        self.out = torch.empty((graph.num_nodes, layers[-1].d_out), dtype=layers[-1].dtype,
+                               device=dev)
+        self._g = graph.struct()
+        self._layers = _layer_array(self.layers)
+        self._nbr = self.nbr.struct()
+        n = ctypes.c_size_t(0)
+        st = L.lib().pinsage_embed_all_bipartite_workspace_size(ctypes.byref(self._g),
+                                                                self._layers, len(self.layers),
+                                                                ctypes.byref(n))
+        L.check(st, "pinsage_embed_all_bipartite_workspace_size")
+        self.workspace = torch.empty(max(1, int(n.value)), dtype=torch.uint8, device=dev)
+
+    def run(self, x_pins: torch.Tensor, stream=None) -> torch.Tensor:
+        x = _dev(x_pins, "x_pins", self.layers[0].dtype)
+        if x.shape[0] != self.graph.num_pins:
+            raise ValueError("x_pins must have one row per pin")
+        st = L.lib().pinsage_embed_all_bipartite(ctypes.byref(self._g), self.seed, self._layers,
+                                                 len(self.layers), _ptr(x),
+                                                 ctypes.byref(self._nbr), _ptr(self.out),
+                                                 _ptr(self.workspace), self.workspace.numel(),
+                                                 _stream(stream))
+        L.check(st, "pinsage_embed_all_bipartite")
+        return self.out
+
+
 def embed_all(graph: DeviceGraph, layers: List[DeviceLayer], x: torch.Tensor, walks: int,
               hops: int, T: int, seed: int, stream=None):
     job = EmbedAll(graph, layers, walks, hops, T, seed)

@@ -494,6 +494,132 @@ int pinsage_hard_negatives(const pinsage_graph_t* graph,
   return PINSAGE_OK;
 }
 
+int pinsage_build_graph_neighborhoods(const pinsage_graph_t* graph, uint64_t seed,
+                                      const int32_t* sources, int64_t num_sources,
+                                      pinsage_neighborhoods_t* out, void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  const int64_t n = graph->num_pins + graph->num_boards;
+  if (num_sources < 0) return fail(PINSAGE_EINVAL, "negative num_sources");
+  if (!sources && num_sources != n)
+    return fail(PINSAGE_EINVAL, "sources is NULL but num_sources (%lld) != num_nodes (%lld)",
+                (long long)num_sources, (long long)n);
+  if ((st = check_nbr(out, num_sources, "build_graph_neighborhoods"))) return st;
+  GraphNbrLaunch a{};
+  a.row_offsets = graph->row_offsets;
+  a.offsets64 = graph->offset_type == PINSAGE_I64;
+  a.col = graph->col;
+  a.nnz = graph->nnz;
+  a.num_nodes = n;
+  a.sources = sources;
+  a.num_sources = num_sources;
+  a.seed = seed;
+  a.top_t = out->top_t;
+  a.idx = out->idx;
+  a.counts = out->counts;
+  a.weights = out->weights;
+  hipError_t e = launch_graph_neighborhoods(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "graph neighbourhood launch");
+  return PINSAGE_OK;
+}
+
+}  // extern "C"
+
+namespace pinsage {
+namespace {
+// Workspace of the bipartite all-node job: the layers' workspace (every node
+// projected), the h ping-pong buffers, the pin row map of layer 1.
+struct BipartiteWs {
+  size_t conv = 0, h = 0, map = 0;
+  int hbufs = 0;
+  size_t total() const { return conv + (size_t)hbufs * h + map; }
+};
+int bipartite_ws(const pinsage_graph_t* graph, const pinsage_layer_t* layers, int32_t K,
+                 BipartiteWs* w) {
+  int st;
+  if (K < 1 || !layers) return fail(PINSAGE_EINVAL, "need at least one layer");
+  if (K % 2)
+    return fail(PINSAGE_EUNSUPPORTED,
+                "num_layers %d is odd: with featureless boards the layers must be even", K);
+  const int64_t n = graph->num_pins + graph->num_boards;
+  for (int k = 0; k < K; ++k) {
+    if ((st = check_layer(&layers[k], k))) return st;
+    if (layers[k].dtype != layers[0].dtype)
+      return fail(PINSAGE_EINVAL, "layer %d dtype differs from layer 0", k);
+    if (k > 0 && layers[k].d_in != layers[k - 1].d_out)
+      return fail(PINSAGE_EINVAL, "layer %d d_in %d != layer %d d_out %d", k, layers[k].d_in,
+                  k - 1, layers[k - 1].d_out);
+    const size_t c = convolve_ws(&layers[k], n, n);
+    w->conv = c > w->conv ? c : w->conv;
+    if (k + 1 < K) {
+      const size_t hb = align_up((size_t)n * layers[k].d_out * elem_size(layers[k].dtype));
+      w->h = hb > w->h ? hb : w->h;
+    }
+  }
+  w->hbufs = K > 2 ? 2 : (K > 1 ? 1 : 0);
+  w->map = align_up((size_t)n * 4);
+  return PINSAGE_OK;
+}
+}  // namespace
+}  // namespace pinsage
+
+extern "C" {
+
+int pinsage_embed_all_bipartite_workspace_size(const pinsage_graph_t* graph,
+                                               const pinsage_layer_t* layers,
+                                               int32_t num_layers, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  BipartiteWs w;
+  if ((st = bipartite_ws(graph, layers, num_layers, &w))) return st;
+  *bytes = w.total();
+  return PINSAGE_OK;
+}
+
+int pinsage_embed_all_bipartite(const pinsage_graph_t* graph, uint64_t seed,
+                                const pinsage_layer_t* layers, int32_t num_layers,
+                                const void* x_pins, pinsage_neighborhoods_t* nbr_out,
+                                void* h_out, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  BipartiteWs w;
+  if ((st = bipartite_ws(graph, layers, num_layers, &w))) return st;
+  const int64_t n = graph->num_pins + graph->num_boards;
+  if ((st = check_nbr(nbr_out, n, "embed_all_bipartite"))) return st;
+  if (!x_pins || !h_out) return fail(PINSAGE_EINVAL, "x_pins or h_out is NULL");
+  if (!workspace || workspace_bytes < w.total())
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes,
+                w.total());
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
+  if ((st = pinsage_build_graph_neighborhoods(graph, seed, nullptr, n, nbr_out, stream)))
+    return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  unsigned char* hbuf[2] = {ws + w.conv, ws + w.conv + w.h};
+  int32_t* pin_map = reinterpret_cast<int32_t*>(ws + w.conv + (size_t)w.hbufs * w.h);
+  // Layer 1 reads x through a row map: pins are rows of x, boards (no
+  // features) read as zero rows, for both the projection and the self half.
+  hipError_t e = launch_row_map(pin_map, n, graph->num_pins, s);
+  if (e != hipSuccess) return hip_fail(e, "row map");
+  const void* cur = x_pins;
+  for (int k = 0; k < num_layers; ++k) {
+    void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
+    if (k == 0)
+      st = run_layer(&layers[k], cur, graph->num_pins, n, pin_map, nbr_out, pin_map, dst, n, ws, s);
+    else
+      st = run_layer(&layers[k], cur, n, n, nullptr, nbr_out, nullptr, dst, n, ws, s);
+    if (st) return st;
+    cur = dst;
+  }
+  return PINSAGE_OK;
+}
+
 int pinsage_convolve_workspace_size(const pinsage_layer_t* layer, int64_t n_transform,
                                     int64_t n_out, size_t* bytes) {
   g_last_error.clear();

@@ -9,7 +9,7 @@ namespace pinsage {
 
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
-                   kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKCount = 9 };
+                   kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKGraphNbr = 9, kKCount = 10 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -64,6 +64,27 @@ struct HardNegLaunch {
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
 };
 hipError_t launch_hard_negatives(const HardNegLaunch& a, hipStream_t s);
+
+// Graph neighbourhoods (Sec. 3.4, MapReduce inference): each source's CSR row,
+// or top_t Philox draws from it when longer, as distinct ids ascending with
+// multiplicities and weights multiplicity / kept entries; top_t <= 256.
+struct GraphNbrLaunch {
+  const void* row_offsets;
+  bool offsets64;
+  const int32_t* col;
+  int64_t nnz;
+  int64_t num_nodes;
+  const int32_t* sources;  // nullable: row r is node r
+  int64_t num_sources;
+  uint64_t seed;
+  int top_t;
+  int32_t* idx;
+  uint16_t* counts;
+  float* weights;  // nullable
+};
+hipError_t launch_graph_neighborhoods(const GraphNbrLaunch& a, hipStream_t s);
+// map[i] = i for i < valid, -1 for i in [valid, n).
+hipError_t launch_row_map(int32_t* map, int64_t n, int64_t valid, hipStream_t s);
 
 
 // Pooling modes (values match pinsage_pool_t).

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 5
+    assert lib.pinsage_version() == 6
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -107,6 +107,39 @@ def test_hard_negatives_validation(L):
     # Nothing to do: accepted without touching the device.
     assert call(_graph(L), hp(), None, 0, None) == L.PINSAGE_OK
     assert call(_graph(L), hp(num_per_query=0), FAKE, 4, None) == L.PINSAGE_OK
+
+
+def test_graph_neighborhoods_and_bipartite_validation(L):
+    lib = L.lib()
+    nb = L.Neighborhoods(15, 8, FAKE, FAKE, None)
+    call = lambda g, src, ns, n: lib.pinsage_build_graph_neighborhoods(
+        ctypes.byref(g) if g is not None else None, 3, src, ns,
+        ctypes.byref(n) if n is not None else None, None)
+    assert call(None, None, 15, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L), None, 14, nb) == L.PINSAGE_EINVAL
+    assert call(_graph(L), None, 15, None) == L.PINSAGE_EINVAL
+    assert call(_graph(L), None, 15, L.Neighborhoods(15, 257, FAKE, FAKE, None)) == \
+        L.PINSAGE_EUNSUPPORTED
+    assert call(_graph(L), FAKE, 3, L.Neighborhoods(4, 8, FAKE, FAKE, None)) == L.PINSAGE_EINVAL
+    n = ctypes.c_size_t(0)
+    g = _graph(L)
+    layers = (L.Layer * 3)(_layer(L), _layer(L), _layer(L))
+    ws = lib.pinsage_embed_all_bipartite_workspace_size
+    assert ws(ctypes.byref(g), layers, 2, ctypes.byref(n)) == 0
+    a = lambda b: (b + 255) // 256 * 256
+    # Every node projected: P (15 x 128) and the pooled chunk (15 x 128) fp32,
+    # one h buffer (15 x 64) and the pin row map (15 int32).
+    assert n.value == a(15 * 128 * 4) + a(15 * 128 * 4) + a(15 * 64 * 4) + a(15 * 4)
+    assert ws(ctypes.byref(g), layers, 3, ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED  # odd K
+    assert b"even" in lib.pinsage_last_error()
+    assert ws(ctypes.byref(g), layers, 0, ctypes.byref(n)) == L.PINSAGE_EINVAL
+    nb15 = L.Neighborhoods(15, 8, FAKE, FAKE, None)
+    st = lib.pinsage_embed_all_bipartite(ctypes.byref(g), 1, layers, 2, FAKE, ctypes.byref(nb15),
+                                         FAKE, FAKE, 16, None)
+    assert st == L.PINSAGE_EWORKSPACE
+    st = lib.pinsage_embed_all_bipartite(ctypes.byref(g), 1, layers, 2, None, ctypes.byref(nb15),
+                                         FAKE, FAKE, 1 << 30, None)
+    assert st == L.PINSAGE_EINVAL
 
 
 def test_layer_validation_and_workspace_sizes(L):
