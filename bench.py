@@ -17,6 +17,10 @@ Other workloads (measurement of the other rows; not the headline):
   --workload minibatch --hard-neg K  the same step preceded by mining K hard
                                     negatives per query (Sec. 3.3), which join
                                     every pair's negatives in the loss
+  --workload bipartite              one step = the MapReduce-inference variant
+                                    of Sec. 3.4 on the 1.2M-node graph: graph
+                                    neighbourhoods (T = 50, long rows sampled),
+                                    2 layers over all nodes, featureless boards
   --workload hardneg                one step = hard negative items (Sec. 3.3)
                                     for 2,048 query pins of the 1.2M-node
                                     graph: 4096 walks x 4 landings each, ranks
@@ -49,8 +53,10 @@ METRIC = "node embeddings/sec (K=2 layerwise, all nodes) + walk steps/sec, 1 MI3
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2, "hardneg": 20}
-DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1, "hardneg": 3}
+DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2, "hardneg": 20,
+                 "bipartite": 20}
+DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1, "hardneg": 3,
+                  "bipartite": 3}
 # Hard negative workload: queries per step, walks and landings per query, the
 # rank window [lo, hi) (ranks 2000-5000 counted from 1).
 HN_QUERIES, HN_WALKS, HN_HOPS, HN_LO, HN_HI = 2048, 4096, 4, 1999, 5000
@@ -313,6 +319,64 @@ def bench_embed_all(args, wl, inp):
     return value, "node embeddings/s", METRIC, elapsed, kernels, extra
 
 
+def bench_bipartite(args, wl, inp):
+    """The MapReduce-inference variant of Sec. 3.4 on the same graph and layers:
+    graph neighbourhoods (T per node, long rows sampled), then the layers over
+    every node with featureless boards (x holds the pins' rows only)."""
+    import torch
+
+    import paper_1806_01973_amd as ps
+    job = ps.EmbedAllBipartite(inp["g"], inp["layers"], wl.T, wl.seed)
+    x_pins = inp["x"][: wl.num_pins]
+    stream = torch.cuda.current_stream()
+    elapsed, prof = timed(lambda i: job.run(x_pins, stream), args.steps, args.warmup)
+    N = wl.num_nodes
+    kernels = kernel_table(prof, args.steps)
+    live = sum(int((job.nbr.idx[r0:r0 + (1 << 22)] >= 0).sum(dtype=torch.int64).item())
+               for r0 in range(0, N, 1 << 22))
+    add_rooflines(kernels, wl, inp["layers"], N, N, live, True, 0, args.steps)
+    value = N * args.steps / elapsed
+    extra = {"walk_steps_per_s": None,
+             "config_extra": {"nodes": N, "neighbourhood_entries": live}}
+    metric = ("node embeddings/sec (K=2 layerwise, all nodes), MapReduce inference variant "
+              "(Sec. 3.4: graph neighbourhoods, featureless boards), 1 MI355X")
+    return value, "node embeddings/s", metric, elapsed, kernels, extra
+
+
+def cpu_baseline_bipartite(inp, wl, threads: int) -> dict:
+    """The oracle on a bounded sample of the variant: graph neighbourhoods of
+    every node, and each layer on a row sample with every sampled row
+    projected. Extrapolated per node."""
+    import numpy as np
+    import oracle
+
+    N = wl.num_nodes
+    t0 = time.perf_counter()
+    idx, cnt, wts = oracle.graph_neighborhoods(inp["host"]["offsets"], inp["host"]["col"],
+                                               wl.seed, wl.T, nthreads=threads)
+    t_nbr = time.perf_counter() - t0
+    flops_row = 0.0
+    d_prev = wl.d_in
+    for _ in range(wl.K):
+        flops_row += 2 * (d_prev * wl.m + (d_prev + wl.m) * wl.d_out)
+        d_prev = wl.d_out
+    n_rows = int(min(N, 400_000, 600e9 / flops_row))
+    idx_s = np.where(idx[:n_rows] >= 0, idx[:n_rows] % n_rows, -1).astype(np.int32)
+    h = inp["x_rows"](n_rows)
+    t_layers = 0.0
+    for L in inp["layers_np"]:
+        t0 = time.perf_counter()
+        h = oracle.convolve_layer(h, n_rows, L["Q"], L["q"], L["W"], L["w"], idx_s, wts[:n_rows],
+                                  nthreads=threads)
+        t_layers += time.perf_counter() - t0
+    per_node = t_nbr / N + t_layers / n_rows
+    return {"value": 1.0 / per_node, "unit": "node embeddings/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"graph neighbourhoods of all {N} nodes ({t_nbr:.1f}s) + all {wl.K} "
+                       f"layers on {n_rows} rows, every row projected ({t_layers:.1f}s), fp64, "
+                       f"extrapolated per node")}
+
+
 def mlp_workspace(mlp, n):
     import ctypes
 
@@ -564,7 +628,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="medium",
-                    choices=["tiny", "medium", "minibatch", "large", "shard", "hardneg"])
+                    choices=["tiny", "medium", "minibatch", "large", "shard", "hardneg",
+                             "bipartite"])
     ap.add_argument("--dataflow", default="dense_then_pool",
                     choices=["pool_then_dense", "dense_then_pool"],
                     help="layer evaluation order (same values; see pinsage_dataflow_t)")
@@ -604,9 +669,10 @@ def main() -> int:
     import synth
 
     hardneg = args.workload == "hardneg"
+    bipartite = args.workload == "bipartite"
     if hardneg and args.hard_neg is None:
         args.hard_neg = 4
-    wl = synth.WORKLOADS["medium" if hardneg else args.workload]
+    wl = synth.WORKLOADS["medium" if hardneg or bipartite else args.workload]
     args.steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.workload]
     args.warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP[args.workload]
     if args.pool == "max" and args.dataflow == "dense_then_pool":
@@ -618,6 +684,8 @@ def main() -> int:
         inp["mlp"] = ps_mlp(P, wl)
     if hardneg:
         value, unit, metric, elapsed, kernels, extra = bench_hard_negatives(args, wl, inp)
+    elif bipartite:
+        value, unit, metric, elapsed, kernels, extra = bench_bipartite(args, wl, inp)
     elif wl.name == "minibatch":
         value, unit, metric, elapsed, kernels, extra = bench_minibatch(args, wl, inp)
     else:
@@ -656,12 +724,20 @@ def main() -> int:
         "kernels": kernels,
         "cpu_baseline": None,
     }
+    if bipartite:
+        result["config"]["workload"] = (
+            f"MapReduce inference variant on {wl.name}: {wl.num_pins} pins + {wl.num_boards} "
+            f"boards, {inp['num_edges']} edges, graph neighbourhoods T={wl.T} (longer rows "
+            f"sampled), featureless boards, K={wl.K}, dims {wl.d_in}->{wl.m}->{wl.d_out} "
+            f"{wl.dtype}, layer dataflow {args.dataflow}")
     if not args.no_cpu_baseline:
         import oracle
         threads = oracle.default_threads()
         log(f"timing the oracle on a sample ({threads} threads)")
         if hardneg:
             result["cpu_baseline"] = cpu_baseline_hard_negatives(inp, wl, threads, args.hard_neg)
+        elif bipartite:
+            result["cpu_baseline"] = cpu_baseline_bipartite(inp, wl, threads)
         elif wl.name == "minibatch":
             result["cpu_baseline"] = cpu_baseline_minibatch(inp, wl, threads,
                                                             args.hard_neg or 0)
