@@ -629,20 +629,24 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
     step(c + 1, std::integral_constant<int, 1>{});
   }
 
-  // ---- epilogue: bias (+ ReLU), bf16 stores ---------------------------------
-  // Lane l: output row m0 + WM wm + 32 i + (l & 31); for group g of block j,
-  // columns n0 + WN wn + 32 j + 8 g + 4 (l >> 5) + 0..3.
+  // ---- epilogue: bias (+ ReLU) into a bf16 C tile in LDS, then row stores ---
+  // After the last chunk's barrier both stages are free; they hold the
+  // 256 x 256 tile, row r at byte 512 r with its 16-byte slot s (8 columns)
+  // at position s ^ (r & 31), so the lanes' 4-column pieces (16 rows per LDS
+  // pass) and the row runs read back (16 slots of one row per pass) fall on
+  // distinct banks. Each row then leaves as 32 x 16 B contiguous stores.
+  // Lane l holds output row WM wm + 32 i + (l & 31) of the tile and, for group
+  // g of block j, columns WN wn + 32 j + 8 g + 4 (l >> 5) + 0..3.
+  static_assert(2 * STAGE_BYTES >= BM * BN * 2 && BN == 256, "C tile fits the two stages");
+  constexpr int ROWB = BN * 2;  // bytes per C tile row
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int64_t r = m0 + wm * C::WM + i * 32 + frow;
-    if (r >= a.M) continue;
+    const int rt = wm * C::WM + i * 32 + frow;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cb = wn * C::WN + j * 32 + 8 * g + 4 * half;
-        const int c = n0 + cb;
-        if (c >= a.N) continue;
         const float4 bv = *reinterpret_cast<const float4*>(bias_s + cb);
         float x0 = acc[i][j][4 * g] + bv.x, x1 = acc[i][j][4 * g + 1] + bv.y;
         float x2 = acc[i][j][4 * g + 2] + bv.z, x3 = acc[i][j][4 * g + 3] + bv.w;
@@ -652,9 +656,27 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
           x2 = fmaxf(x2, 0.0f);
           x3 = fmaxf(x3, 0.0f);
         }
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + r * a.N + c) =
+        const int slot = (cb >> 3) ^ (rt & 31);
+        *reinterpret_cast<uint2*>(smem + rt * ROWB + slot * 16 + half * 8) =
             make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3));
       }
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int k = 0; k < BM * (BN / 8) / THREADS; ++k) {
+    const int e = k * THREADS + tid;
+    const int rt = e >> 5, sl = e & 31;
+    const int64_t r = m0 + rt;
+    const int c = n0 + sl * 8;
+    if (r < a.M && c < a.N) {
+      // Streaming stores: the output is not read again by this kernel, so it
+      // should not push the reused B rows out of L2.
+      const uint4 v = *reinterpret_cast<const uint4*>(smem + rt * ROWB + ((sl ^ (rt & 31)) * 16));
+      typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
+      __builtin_nontemporal_store(
+          __builtin_bit_cast(u32x4s, v),
+          reinterpret_cast<u32x4s*>(static_cast<uint16_t*>(a.C) + r * a.N + c));
+    }
   }
 }
 
@@ -664,9 +686,11 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
 bool use_rs(const GemmLaunch& a) {
   const int64_t ldb = a.ldb ? a.ldb : a.K0;
   // Buffer offsets are 32-bit: a tile's 256 rows must span < 2^31 bytes.
+  // The epilogue writes rows in 8-column (16-byte) pieces: N % 8 == 0.
   return a.bf16 && !a.l2norm && a.K1 == 0 && !a.rowmap && !a.addend && a.K0 % 8 == 0 &&
-         a.lda0 % 8 == 0 && ldb % 8 == 0 && a.lda0 <= (1 << 20) && ldb <= (1 << 20) &&
-         reinterpret_cast<uintptr_t>(a.A0) % 16 == 0 && reinterpret_cast<uintptr_t>(a.B) % 16 == 0;
+         a.N % 8 == 0 && a.lda0 % 8 == 0 && ldb % 8 == 0 && a.lda0 <= (1 << 20) &&
+         ldb <= (1 << 20) && reinterpret_cast<uintptr_t>(a.A0) % 16 == 0 &&
+         reinterpret_cast<uintptr_t>(a.B) % 16 == 0 && reinterpret_cast<uintptr_t>(a.C) % 16 == 0;
 }
 
 #ifndef PINSAGE_RS_CFG
