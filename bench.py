@@ -26,7 +26,8 @@ Other workloads (measurement of the other rows; not the headline):
                                     graph: 4096 walks x 4 landings each, ranks
                                     2000-5000, --hard-neg draws per query
 
-Prints one JSON line: throughput of the whole step, walk steps/s, per-kernel
+Prints one JSON line: throughput of the whole step, walk steps/s, node
+embeddings/s over the layer kernels alone (walks excluded), per-kernel
 times from hipEvents recorded around every launch in the timed region, the
 roofline of the dominant kernel and the CPU oracle timed on a bounded sample
 of the same workload.
@@ -301,7 +302,11 @@ def bench_embed_all(args, wl, inp):
     add_rooflines(kernels, wl, inp["layers"], N, wl.num_pins, live, job.nbr.weights is not None,
                   walk_steps, args.steps)
     value = N * args.steps / elapsed
+    layer_ms = sum(v["ms_per_step"] for k, v in kernels.items()
+                   if k in ("gemm_q", "gemm_r", "pool", "gemm_w"))
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
+             # N over the layer kernels' time alone (walks excluded), hipEvents.
+             "layers_embeddings_per_s": N / (layer_ms * 1e-3) if layer_ms else None,
              "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps}}
     if compare_dataflow(args, wl):
         # The other evaluation order of the same layers, timed the same way
@@ -719,6 +724,7 @@ def main() -> int:
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
         "walk_steps_per_s": extra["walk_steps_per_s"],
+        "layers_embeddings_per_s": extra.get("layers_embeddings_per_s"),
         "alt_dataflow": extra.get("alt_dataflow"),
         "roofline": roofline_of(kernels, wl),
         "kernels": kernels,
