@@ -72,6 +72,19 @@ __device__ __forceinline__ int row_total(const PoolLaunch& a, int64_t row, int l
   return wave_sum_i32(part);
 }
 
+// One past the last slot of the row that holds a neighbour (0 for an empty
+// row): the loops stop there, so short rows of a wide table cost little.
+// Skipped slots hold no neighbour and would contribute nothing.
+__device__ __forceinline__ int row_end(const PoolLaunch& a, int64_t row, int lane) {
+  const int T = a.T;
+  int last = -1;
+  for (int t = lane; t < T; t += kWave) {
+    const int32_t v = a.idx[row * T + t];
+    if ((uint64_t)(int64_t)v < (uint64_t)a.n_transform) last = t;
+  }
+  return __builtin_amdgcn_readfirstlane(wave_max_i32(last)) + 1;
+}
+
 // Weight of neighbour slot t of a row (importance or mean pooling).
 template <int MODE>
 __device__ __forceinline__ float slot_alpha(const PoolLaunch& a, int64_t row, int t, int total) {
@@ -102,6 +115,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
     const int64_t row = row0;
     const int32_t* __restrict__ ridx = a.idx + row * T;
     const int total = row_total(a, row, lane);
+    const int tend = row_end(a, row, lane);
     float acc[J][VN];
 #pragma unroll
     for (int j = 0; j < J; ++j)
@@ -109,14 +123,14 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolLaunch a) {
       for (int v = 0; v < VN; ++v) acc[j][v] = MODE == kPoolMax ? -INFINITY : 0.0f;
     bool any = false;
 
-    for (int t0 = 0; t0 < T; t0 += U) {
+    for (int t0 = 0; t0 < tend; t0 += U) {
       Raw buf[U][J];
       float alpha[U];
       bool ok[U];
 #pragma unroll
       for (int i = 0; i < U; ++i) {
         const int t = t0 + i;
-        int32_t v = t < T ? ridx[t] : -1;
+        int32_t v = t < tend ? ridx[t] : -1;
         if ((uint64_t)(int64_t)v >= (uint64_t)a.n_transform) v = -1;
         ok[i] = v >= 0;
         alpha[i] = 0.0f;
@@ -181,18 +195,19 @@ __global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
        row += (int64_t)gridDim.x * kWavesPerBlock) {
     const int32_t* __restrict__ ridx = a.idx + row * T;
     const int total = row_total(a, row, lane);
+    const int tend = row_end(a, row, lane);
     float acc[VN];
 #pragma unroll
     for (int v = 0; v < VN; ++v) acc[v] = MODE == kPoolMax ? -INFINITY : 0.0f;
     bool any = false;
-    for (int t0 = 0; t0 < T; t0 += U * RG) {
+    for (int t0 = 0; t0 < tend; t0 += U * RG) {
       Raw buf[U];
       float alpha[U];
       bool ok[U];
 #pragma unroll
       for (int i = 0; i < U; ++i) {
         const int t = t0 + i * RG + grp;
-        int32_t v = t < T ? ridx[t] : -1;
+        int32_t v = t < tend ? ridx[t] : -1;
         if ((uint64_t)(int64_t)v >= (uint64_t)a.n_transform) v = -1;
         ok[i] = v >= 0;
         alpha[i] = 0.0f;
