@@ -99,3 +99,17 @@ def test_medium_workload(orc):
     np.testing.assert_array_equal(got, ref)
     assert np.all(got < wl.num_pins)
     assert (got >= 0).mean() > 0.9  # most queries reach past rank 5000
+
+
+def test_more_queries_than_workgroups(orc, tiny):
+    # 9,000 queries: past the 8,192-workgroup grid, so workgroups take a second
+    # query (grid-stride), with the one-slot-per-thread width.
+    wl, off, col = tiny
+    rng = np.random.default_rng(12)
+    q = rng.integers(-5, wl.num_nodes + 5, 9000).astype(np.int32)
+    print("[case] hard negatives, 9000 queries (grid-stride)", flush=True)
+    got, steps = _gpu(off, col, wl.num_pins, wl.num_boards, q, 3, 31, 100, 2, 5, 40)
+    np.testing.assert_array_equal(got, orc.hard_negatives(off, col, wl.num_pins, 31, 100, 2, q,
+                                                          5, 40, 3))
+    valid = [int(u) for u in q if 0 <= u < wl.num_nodes]
+    assert steps == sum(orc.walk_visits(off, col, wl.num_pins, 31, u, 100, 2)[1] for u in valid)
