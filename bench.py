@@ -279,9 +279,13 @@ def bench_embed_all(args, wl, inp):
     import torch
 
     import paper_1806_01973_amd as ps
+    ps.set_overlap(args.overlap)
     job = ps.EmbedAll(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed,
                       weights=wl.name != "shard")
-    stream = torch.cuda.current_stream()
+    # A stream of its own: the library's side streams then overlap freely with
+    # it (the legacy default stream would wait for them at every launch).
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
     mlp = inp.get("mlp")
     if mlp is not None:
         z = torch.empty((wl.num_nodes, mlp.d_out), dtype=mlp.dtype, device="cuda")
@@ -307,7 +311,11 @@ def bench_embed_all(args, wl, inp):
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
              # N over the layer kernels' time alone (walks excluded), hipEvents.
              "layers_embeddings_per_s": N / (layer_ms * 1e-3) if layer_ms else None,
-             "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps}}
+             "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps,
+                              # first layer's transform beside the walks on this
+                              # many eighths of the CUs (0: in order); its launches
+                              # and the walk's then time their shared duration
+                              "overlap_cu_eighths": args.overlap}}
     if compare_dataflow(args, wl):
         # The other evaluation order of the same layers, timed the same way
         # (same inputs, same steps), for comparison only.
@@ -648,6 +656,9 @@ def main() -> int:
                     help="hard negatives per query: draws for --workload hardneg (default 4); "
                          "with --workload minibatch, mined each step and added to every "
                          "pair's negatives (default 0)")
+    ap.add_argument("--overlap", type=int, default=4, metavar="EIGHTHS",
+                    help="all-node job: first layer's transform beside the walks on EIGHTHS/8 "
+                         "of the CUs (0: walks, then transform, in order)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layer", default=None,
                     help="d_in,m,d_out: time one layer on random inputs instead of a workload")

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 6
+#define PINSAGE_ABI_VERSION 7
 
 enum {
   PINSAGE_OK = 0,
@@ -288,12 +288,30 @@ int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
  * rows [0, num_pins) once. x: device [num_nodes][layers[0].d_in];
  * h_out: device [num_nodes][layers[K-1].d_out]; nbr_out: caller buffers with
  * rows = num_nodes and top_t = walk->top_t (weights may be NULL).
- * layers[k].d_in must equal layers[k-1].d_out; one storage dtype throughout. */
+ * layers[k].d_in must equal layers[k-1].d_out; one storage dtype throughout.
+ * With 262,144 to 4,194,304 pins the walks and the first layer's transform
+ * run beside each other on two library-owned CU-masked streams forked from
+ * (and joined back into) `stream`; see pinsage_set_overlap. The output does
+ * not depend on that schedule. */
 int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                       const pinsage_layer_t* layers, int32_t num_layers, const void* x,
                       pinsage_neighborhoods_t* nbr_out, void* h_out,
                       unsigned long long* total_steps, void* workspace,
                       size_t workspace_bytes, void* stream);
+
+/* Schedule of pinsage_embed_all (Sec. 3.4 leaves it open: the first layer's
+ * transform of the pins reads only the features, not the neighbourhoods).
+ * cu_eighths in [1, 7]: the first layer's transform of a leading share of
+ * the pins runs on cu_eighths / 8 of the CUs (whole groups of 8 CUs, spread
+ * evenly over the mask) while the walks run on the rest; the share of the
+ * pins follows the last completed call's timing on the device. 0: walks, then transform, in order on the caller's stream. Default
+ * 4. Process-wide; takes effect at the next pinsage_embed_all call. Streams
+ * and events are created on a device's first overlapped call; a call that
+ * changes the share waits for their work and destroys them, so a caller that
+ * tears the runtime down itself (or runs under a profiler) releases them
+ * first with pinsage_set_overlap(0). Concurrent pinsage_embed_all calls on one device are
+ * serialised while they enqueue. Errors: PINSAGE_EINVAL outside [0, 7]. */
+int pinsage_set_overlap(int32_t cu_eighths);
 
 /* Workspace bytes needed by pinsage_output_mlp for n rows. */
 int pinsage_output_mlp_workspace_size(const pinsage_mlp_t* mlp, int64_t n, size_t* bytes);

@@ -26,4 +26,5 @@ from .api import (  # noqa: F401
     output_mlp,
     profile_enable,
     profile_read,
+    set_overlap,
 )

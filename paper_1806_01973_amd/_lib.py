@@ -2,6 +2,7 @@
 
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
 
@@ -30,7 +31,8 @@ EXPORTED = [
     "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_build_graph_neighborhoods",
     "pinsage_embed_all_bipartite_workspace_size", "pinsage_embed_all_bipartite",
     "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
-    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_output_mlp_workspace_size",
+    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_set_overlap",
+    "pinsage_output_mlp_workspace_size",
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
     "pinsage_profile_enable", "pinsage_profile_read",
@@ -125,6 +127,7 @@ def lib():
     L.pinsage_embed_all.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                     ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Neighborhoods),
                                     P, P, P, ctypes.c_size_t, P]
+    L.pinsage_set_overlap.argtypes = [i32]
     L.pinsage_output_mlp_workspace_size.argtypes = [ctypes.POINTER(MLP), i64,
                                                     ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_output_mlp.argtypes = [ctypes.POINTER(MLP), P, i64, P, P, ctypes.c_size_t, P]
@@ -147,6 +150,9 @@ def lib():
         if fn.restype is None or fn.restype is ctypes.c_int:
             fn.restype = ctypes.c_int
     _lib = L
+    # The library's CU-masked streams go while the runtime (and any profiler
+    # attached to it) is still whole.
+    atexit.register(L.pinsage_set_overlap, 0)
     return L
 
 

@@ -441,6 +441,12 @@ class Minibatch:
         return ctypes.byref(self._mlp) if self._mlp is not None else None
 
 
+def set_overlap(cu_eighths: int) -> None:
+    """Schedule of EmbedAll: the first layer's transform beside the walks on
+    cu_eighths/8 of the CUs (1-7), or walks then transform in order (0)."""
+    L.check(L.lib().pinsage_set_overlap(int(cu_eighths)), "pinsage_set_overlap")
+
+
 def profile_enable(on: bool = True) -> None:
     L.check(L.lib().pinsage_profile_enable(1 if on else 0), "pinsage_profile_enable")
 

@@ -241,30 +241,39 @@ hipError_t launch_transform(const pinsage_layer_t* L, const void* h_in, int64_t 
   g.C = C;
   g.bf16 = L->dtype == PINSAGE_BF16;
   g.relu = true;
+  g.row_base = c0;
   return launch_gemm(g, s);
 }
 
 // Layer bodies shared by convolve_layer, embed_all and the minibatch forward;
 // arguments already valid. Phase 1 fills the per-pin table of the workspace (P,
 // or R = P W_n^T when split); phase 2 pools it and applies W.
-int run_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
-                  const int32_t* transform_rows, int64_t n_out, void* ws, hipStream_t s) {
+//
+// Phase 1 for the transformable rows [r0, r1) only. When split, the P chunk
+// buffer is used from row `pbase` on (chunks of kChunkRows - pbase rows), so two
+// row ranges with disjoint P rows can run on two streams at once.
+int run_transform_rows(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
+                       int64_t n_transform, const int32_t* transform_rows, int64_t n_out,
+                       void* ws, int64_t r0, int64_t r1, int64_t pbase, hipStream_t s) {
   const bool bf16 = L->dtype == PINSAGE_BF16;
   const size_t es = elem_size(L->dtype);
   const LayerWs lw = layer_ws(L, n_transform, n_out);
   unsigned char* table = static_cast<unsigned char*>(ws);  // P, or R when split
-  unsigned char* pchunk = table + lw.table;
   hipError_t e;
+  if (r1 <= r0) return PINSAGE_OK;
   if (L->dataflow != PINSAGE_DENSE_THEN_POOL) {
     // Algorithm 1 line 1, once per transformable row (Sec. 3.4).
-    e = launch_transform(L, h_in, n_in, transform_rows, 0, n_transform, table, s);
+    e = launch_transform(L, h_in, n_in, transform_rows, r0, r1 - r0,
+                         table + (size_t)r0 * L->m * es, s);
     if (e != hipSuccess) return hip_fail(e, "Q transform launch");
     return PINSAGE_OK;
   }
   // Per chunk of pins: P = ReLU(h Q^T + q), then R = P W_n^T with W_n the
   // neighbour columns [d_in, d_in + m) of W (row stride d_in + m).
-  for (int64_t c0 = 0; c0 < n_transform; c0 += kChunkRows) {
-    const int64_t rows = (n_transform - c0) < kChunkRows ? (n_transform - c0) : kChunkRows;
+  unsigned char* pchunk = table + lw.table + (size_t)pbase * L->m * es;
+  const int64_t cs = kChunkRows - pbase;
+  for (int64_t c0 = r0; c0 < r1; c0 += cs) {
+    const int64_t rows = (r1 - c0) < cs ? (r1 - c0) : cs;
     e = launch_transform(L, h_in, n_in, transform_rows, c0, rows, pchunk, s);
     if (e != hipSuccess) return hip_fail(e, "Q transform launch");
     GemmLaunch gr{};
@@ -278,10 +287,17 @@ int run_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int6
     gr.N = L->d_out;
     gr.C = table + (size_t)c0 * L->d_out * es;
     gr.bf16 = bf16;
+    gr.row_base = c0;
     e = launch_gemm(gr, s);
     if (e != hipSuccess) return hip_fail(e, "neighbour-half W launch");
   }
   return PINSAGE_OK;
+}
+
+int run_transform(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t n_transform,
+                  const int32_t* transform_rows, int64_t n_out, void* ws, hipStream_t s) {
+  return run_transform_rows(L, h_in, n_in, n_transform, transform_rows, n_out, ws, 0,
+                            n_transform, 0, s);
 }
 
 int run_pool_dense(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
@@ -343,6 +359,7 @@ int run_pool_dense(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
     gw.bf16 = bf16;
     gw.relu = true;
     gw.l2norm = true;
+    gw.row_base = r0;
     e = launch_gemm(gw, s);
     if (e != hipSuccess) return hip_fail(e, "W transform launch");
   }
@@ -357,6 +374,136 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
   return run_pool_dense(L, h_in, n_in, n_transform, nbr, self_rows, h_out, n_out, ws, s);
 }
 
+// ---- walks beside the first layer's transform (embed_all) -----------------
+// The first layer's transform reads only x, so it can run while the
+// neighbourhood walks run. The walks are bound by dependent random reads and
+// leave the matrix cores idle; the GEMM blocks take whole CUs. Both therefore
+// run on CU-masked streams forked from the caller's stream: the transform of
+// the first `a` pins on a side stream holding a share of the CUs, the walks on
+// the other CUs. The remaining pins are transformed on the caller's stream
+// (all CUs) once the walks are done, and the pool waits for both.
+//
+// `a` comes from the last call on the device whose events have completed: with
+// side rate rs and full-chip rate rf (rows per ms) and walk time tw, the side
+// and the caller's stream end together when a / rs = tw + (P - a) / rf, i.e.
+// a = rs (rf tw + P) / (rf + rs). The GEMMs sum every row in the same order
+// whatever the split, so the output does not depend on `a`.
+//
+// Masks: byte j of the CU mask (8 consecutive CUs) goes to the side when
+// floor((j + 1) k / 8) > floor(j k / 8), k = the share in eighths, which spreads
+// the side's bytes evenly over the mask words.
+struct Overlap {
+  int eighths = -1;
+  bool ok = false;
+  hipStream_t side = nullptr, walk = nullptr;
+  hipEvent_t fork = nullptr, side_done = nullptr, walk_done = nullptr, main_done = nullptr;
+  double alpha = 0.0;       // side rows / transformable rows for the next call
+  double rf_over_rs = 0.0;  // full-chip rate over side rate, last measured
+  int64_t side_rows = 0, main_rows = 0, total_rows = 0;  // of the last call
+  bool pending = false;     // the last call's events have not been read
+};
+constexpr int kMaxDevices = 64;
+// Pin counts that overlap: at least 2^18, and at most one transform chunk.
+// With more pins the graph outgrows the MALL, the walks become bound by HBM
+// latency and need every CU (measured on 10M pins: the walks slowed by more
+// than the transform share saved), so larger graphs run in order.
+constexpr int64_t kMinOverlapRows = 1ll << 18;
+constexpr int64_t kMaxOverlapRows = kChunkRows;
+std::mutex g_ov_mu;
+int g_ov_eighths = 4;
+Overlap g_ov[kMaxDevices];
+
+// With g_ov_mu held: waits for and destroys a device's streams and events.
+void overlap_release(Overlap& o, int dev) {
+  if (o.side || o.walk || o.fork || o.side_done || o.walk_done || o.main_done) {
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(dev);
+    for (hipStream_t st : {o.side, o.walk}) {
+      if (!st) continue;
+      (void)hipStreamSynchronize(st);
+      (void)hipStreamDestroy(st);
+    }
+    for (hipEvent_t ev : {o.fork, o.side_done, o.walk_done, o.main_done})
+      if (ev) (void)hipEventDestroy(ev);
+    (void)hipSetDevice(cur);
+    (void)hipGetLastError();
+  }
+  o = Overlap{};
+}
+
+
+// With g_ov_mu held: the current device's streams and events for the current
+// share, created on first use. nullptr when overlap is off or the runtime
+// refuses the masked streams (the caller then runs everything in order).
+Overlap* overlap_state() {
+  if (g_ov_eighths <= 0) return nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  Overlap& o = g_ov[dev];
+  if (o.eighths == g_ov_eighths) return o.ok ? &o : nullptr;
+  // First use on this device for the current share.
+  overlap_release(o, dev);
+  const int k = g_ov_eighths;
+  o.eighths = k;
+  o.alpha = k >= 4 ? 1.0 : 0.3 * k;  // first call: a rough share by CU count
+  o.rf_over_rs = 8.0 / k;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus < 64) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  const int words = (cus + 31) / 32;
+  std::vector<uint32_t> side_mask(words, 0u), walk_mask(words, 0u);
+  for (int i = 0; i < cus; ++i) {
+    const int j = i / 8;
+    const bool to_side = ((j + 1) * k) / 8 > (j * k) / 8;
+    (to_side ? side_mask : walk_mask)[i / 32] |= 1u << (i % 32);
+  }
+  bool good = hipExtStreamCreateWithCUMask(&o.side, (uint32_t)words, side_mask.data()) ==
+                  hipSuccess &&
+              hipExtStreamCreateWithCUMask(&o.walk, (uint32_t)words, walk_mask.data()) ==
+                  hipSuccess &&
+              hipEventCreate(&o.fork) == hipSuccess && hipEventCreate(&o.side_done) == hipSuccess &&
+              hipEventCreate(&o.walk_done) == hipSuccess &&
+              hipEventCreate(&o.main_done) == hipSuccess;
+  if (!good) {
+    (void)hipGetLastError();
+    overlap_release(o, dev);
+    o.eighths = k;  // do not retry this share
+    return nullptr;
+  }
+  o.ok = true;
+  return &o;
+}
+
+// With g_ov_mu held: the side's rows for this call, after folding in the last
+// call's timing when its events have completed.
+int64_t overlap_rows(Overlap& o, int64_t n_transform) {
+  if (o.pending && hipEventQuery(o.main_done) == hipSuccess &&
+      hipEventQuery(o.side_done) == hipSuccess) {
+    float ts = 0.0f, tw = 0.0f, tm = 0.0f;
+    const bool timed = hipEventElapsedTime(&ts, o.fork, o.side_done) == hipSuccess &&
+                       hipEventElapsedTime(&tw, o.fork, o.walk_done) == hipSuccess &&
+                       hipEventElapsedTime(&tm, o.walk_done, o.main_done) == hipSuccess;
+    if (timed && ts > 0.0f && o.side_rows > 0) {
+      const double rs = (double)o.side_rows / ts;
+      if (o.main_rows > 0 && tm > 0.0f) o.rf_over_rs = ((double)o.main_rows / tm) / rs;
+      const double rf = rs * o.rf_over_rs;
+      const double want = rs * (rf * tw + (double)o.total_rows) / (rf + rs);
+      const double frac = want / (double)o.total_rows;
+      o.alpha = frac < 0.05 ? 0.05 : (frac > 1.0 ? 1.0 : frac);  // keep measuring
+    }
+    o.pending = false;
+  }
+  (void)hipGetLastError();  // a not-ready query is not an error
+  const int64_t a = (int64_t)(o.alpha * (double)n_transform) / 256 * 256;
+  return a > n_transform ? n_transform : a;
+}
 }  // namespace
 
 ProfileScope::ProfileScope(int cls, hipStream_t s) : cls_(cls), s_(s) {
@@ -712,9 +859,6 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 256)
     return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
-  if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
-    return st;
-
   hipStream_t s = static_cast<hipStream_t>(stream);
   size_t conv = 0, h = 0;
   for (int k = 0; k < num_layers; ++k) {
@@ -727,13 +871,67 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   }
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   unsigned char* hbuf[2] = {ws + conv, ws + conv + h};
+  const int64_t P = graph->num_pins;
+  const pinsage_layer_t* L0 = &layers[0];
+
+  // Walks, then the first layer's transform: beside each other on masked
+  // streams when the device allows it, else in order on the caller's stream.
+  bool transformed = false;
+  {
+    std::lock_guard<std::mutex> lk(g_ov_mu);
+    Overlap* ov = P >= kMinOverlapRows && P <= kMaxOverlapRows ? overlap_state() : nullptr;
+    const int64_t a = ov ? overlap_rows(*ov, P) : 0;
+    if (a > 0) {
+      hipError_t e = hipEventRecord(ov->fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ov->side, ov->fork, 0);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ov->walk, ov->fork, 0);
+      if (e != hipSuccess) return hip_fail(e, "stream fork");
+      st = run_transform_rows(L0, x, n, P, nullptr, n, ws, 0, a, 0, ov->side);
+      const hipError_t e1 = hipEventRecord(ov->side_done, ov->side);
+      if (!st) st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps,
+                                                ov->walk);
+      const hipError_t e2 = hipEventRecord(ov->walk_done, ov->walk);
+      // Join: the caller's stream waits for the walks before its share of
+      // the transform, and for the side before the pool.
+      const hipError_t e3 = hipStreamWaitEvent(s, ov->walk_done, 0);
+      if (!st) st = run_transform_rows(L0, x, n, P, nullptr, n, ws, a, P, a, s);
+      const hipError_t e4 = hipEventRecord(ov->main_done, s);
+      const hipError_t e5 = hipStreamWaitEvent(s, ov->side_done, 0);
+      if (st) return st;
+      for (hipError_t ej : {e1, e2, e3, e4, e5})
+        if (ej != hipSuccess) return hip_fail(ej, "stream join");
+      ov->side_rows = a;
+      ov->main_rows = P - a;
+      ov->total_rows = P;
+      ov->pending = true;
+      transformed = true;
+    }
+  }
+  if (!transformed) {
+    if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
+      return st;
+    if ((st = run_transform(L0, x, n, P, nullptr, n, ws, s))) return st;
+  }
+
   const void* cur = x;
   for (int k = 0; k < num_layers; ++k) {
     void* dst = (k == num_layers - 1) ? h_out : hbuf[k % 2];
-    st = run_layer(&layers[k], cur, n, graph->num_pins, nullptr, nbr_out, nullptr, dst, n, ws, s);
+    if (k > 0) st = run_transform(&layers[k], cur, n, P, nullptr, n, ws, s);
+    if (!st) st = run_pool_dense(&layers[k], cur, n, P, nbr_out, nullptr, dst, n, ws, s);
     if (st) return st;
     cur = dst;
   }
+  return PINSAGE_OK;
+}
+
+int pinsage_set_overlap(int32_t cu_eighths) {
+  g_last_error.clear();
+  if (cu_eighths < 0 || cu_eighths > 7)
+    return fail(PINSAGE_EINVAL, "cu_eighths %d outside [0, 7]", cu_eighths);
+  std::lock_guard<std::mutex> lk(g_ov_mu);
+  if (cu_eighths != g_ov_eighths)
+    for (int d = 0; d < kMaxDevices; ++d) overlap_release(g_ov[d], d);
+  g_ov_eighths = cu_eighths;
   return PINSAGE_OK;
 }
 

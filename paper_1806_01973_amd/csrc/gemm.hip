@@ -178,15 +178,17 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   }
   const int kvec = vec_slot(lane >> 2, lane & 3) * VEC;
   const int nchunks = (K + BK - 1) / BK;
-  // Tiles start their K sweep at different chunks (rotation by tile index):
+  // Tiles start their K sweep at different chunks (rotation by the tile's
+  // index in the whole product):
   // rows of A and B sit at power-of-two strides, and blocks that all read the
   // same K columns at once would pile onto a few L2 channels.
 #ifndef PINSAGE_GEMM_KSHIFT
 #define PINSAGE_GEMM_KSHIFT 0
 #endif
-  const int kshift = PINSAGE_GEMM_KSHIFT == 0 ? tile % nchunks
+  const int64_t abs_tile = tile + (a.row_base / BM) * tiles_n;
+  const int kshift = PINSAGE_GEMM_KSHIFT == 0 ? (int)(abs_tile % nchunks)
                      : PINSAGE_GEMM_KSHIFT == 1 ? 0
-                     : (tile / tiles_n) % nchunks;
+                     : (int)((abs_tile / tiles_n) % nchunks);
   // Issues the DMAs of the chunk-th chunk of this tile's sweep into its
   // stage. Sweep positions past the end read the zero row, which keeps the
   // in-flight count uniform for wait_vmcnt.

@@ -134,6 +134,10 @@ struct GemmLaunch {
   bool relu;
   bool l2norm;
   int prof_class = -1;  // KernelClass for timing; -1: inferred from the epilogue
+  // Rows of the whole product before row 0 of this launch (a multiple of 256).
+  // Only the K-sweep rotation reads it, so a product split into row ranges
+  // sums every row in the same order as one launch over all rows.
+  int64_t row_base = 0;
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
 

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 6
+    assert lib.pinsage_version() == 7
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"

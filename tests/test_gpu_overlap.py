@@ -1,0 +1,100 @@
+"""GPU: the all-node job's schedule does not change its output.
+
+With 262,144 to 4,194,304 pins the walks and the first layer's transform of a
+leading share of the pins run beside each other on CU-masked streams, and the
+share follows the previous call's timing. The GEMMs sum every row in the same
+order whatever the split, so every schedule must give the same bits as the
+in-order one (walks, then the whole transform on the caller's stream):
+
+* the 1.2M-node fp32 graph, both layer dataflows, side CU shares of 2/8, 3/8
+  and 4/8, three calls in a row (the pin share moves between calls);
+* a 4.5M-node graph with more pins than one 4,194,304-row chunk and a tiny
+  graph: both outside the overlapped range, so every share runs in order.
+The outputs themselves are checked against the oracle by the other GPU tests.
+"""
+
+import dataclasses
+
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _layers(wl, dtype, dataflow):
+    import paper_1806_01973_amd as ps
+    return [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=dtype, dataflow=dataflow)
+            for L in synth.make_layers(wl)]
+
+
+def _runs(g, layers, wl, x, shares, calls):
+    import paper_1806_01973_amd as ps
+    outs = []
+    for k in shares:
+        ps.set_overlap(k)
+        print(f"[case] share {k}/8", flush=True)
+        job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
+        for _ in range(calls if k else 1):
+            out = job.run(x).clone()
+            torch.cuda.synchronize()
+            outs.append((k, out, job.nbr.idx.clone(), int(job.steps.item())))
+    ps.set_overlap(4)
+    return outs
+
+
+def _same(outs, what):
+    k0, ref, ridx, rsteps = outs[0]
+    assert k0 == 0
+    for k, out, idx, steps in outs[1:]:
+        assert steps == rsteps, f"{what} share {k}: steps"
+        assert torch.equal(idx, ridx), f"{what} share {k}: neighbourhoods differ"
+        assert torch.equal(out, ref), f"{what} share {k}: embeddings differ"
+
+
+@pytest.fixture(scope="module")
+def medium():
+    import paper_1806_01973_amd as ps
+    wl = synth.WORKLOADS["medium"]
+    data = synth.make_workload(wl)
+    g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
+    return wl, g, torch.as_tensor(data["x"]).cuda()
+
+
+@pytest.mark.parametrize("dataflow", ["dense_then_pool", "pool_then_dense"])
+def test_medium_schedules_agree(medium, dataflow):
+    wl, g, x = medium
+    print(f"[case] overlap schedules, 1.2M nodes f32 {dataflow}", flush=True)
+    outs = _runs(g, _layers(wl, torch.float32, dataflow), wl, x, (0, 2, 3, 4), 3)
+    _same(outs, f"medium {dataflow}")
+
+
+def test_chunked_schedules_agree():
+    import paper_1806_01973_amd as ps
+    from synth.device_gen import make_features_device, make_graph_device
+    base = synth.WORKLOADS["minibatch"]  # bf16, 256 -> 512 -> 256
+    wl = dataclasses.replace(base.scaled(4_300_000, 200_000, "overlap-chunked"), walks=20)
+    print("[case] schedules, 4.3M pins (two transform chunks, in order) bf16", flush=True)
+    offsets, col, _ = make_graph_device(wl)
+    x = make_features_device(wl, offsets, col)
+    g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards)
+    outs = _runs(g, _layers(wl, torch.bfloat16, "dense_then_pool"), wl, x, (0, 2), 2)
+    _same(outs, "chunked")
+    del outs, g, x, offsets, col
+    torch.cuda.empty_cache()
+
+
+def test_small_graph_and_bad_share():
+    import paper_1806_01973_amd as ps
+    wl = synth.WORKLOADS["tiny"]
+    data = synth.make_workload(wl)
+    g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards)
+    x = torch.as_tensor(data["x"]).cuda()
+    print("[case] overlap below the pin threshold", flush=True)
+    outs = _runs(g, _layers(wl, torch.float32, "dense_then_pool"), wl, x, (0, 7), 2)
+    _same(outs, "tiny")
+    with pytest.raises(ps.PinsageError):
+        ps.set_overlap(8)
+    with pytest.raises(ps.PinsageError):
+        ps.set_overlap(-1)
