@@ -309,8 +309,10 @@ def bench_embed_all(args, wl, inp):
     layer_ms = sum(v["ms_per_step"] for k, v in kernels.items()
                    if k in ("gemm_q", "gemm_r", "pool", "gemm_w"))
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
-             # N over the layer kernels' time alone (walks excluded), hipEvents.
-             "layers_embeddings_per_s": N / (layer_ms * 1e-3) if layer_ms else None,
+             # N over the layer kernels' time alone (walks excluded), hipEvents;
+             # only in the in-order schedule (overlapped launches share the chip).
+             "layers_embeddings_per_s": (N / (layer_ms * 1e-3)
+                                         if layer_ms and args.overlap == 0 else None),
              "config_extra": {"nodes": N, "walk_steps_per_step": walk_steps,
                               # first layer's transform beside the walks on this
                               # many eighths of the CUs (0: in order); its launches
