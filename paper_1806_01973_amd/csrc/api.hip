@@ -482,9 +482,11 @@ Overlap* overlap_state() {
 }
 
 // With g_ov_mu held: the side's rows for this call, after folding in the last
-// call's timing when its events have completed.
-int64_t overlap_rows(Overlap& o, int64_t n_transform) {
-  if (o.pending && hipEventQuery(o.main_done) == hipSuccess &&
+// call's timing when its events have completed. While the caller's stream is
+// being captured into a graph the events are neither read nor marked for
+// reading (their records are graph nodes, not timings).
+int64_t overlap_rows(Overlap& o, int64_t n_transform, bool capturing) {
+  if (!capturing && o.pending && hipEventQuery(o.main_done) == hipSuccess &&
       hipEventQuery(o.side_done) == hipSuccess) {
     float ts = 0.0f, tw = 0.0f, tm = 0.0f;
     const bool timed = hipEventElapsedTime(&ts, o.fork, o.side_done) == hipSuccess &&
@@ -880,7 +882,13 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   {
     std::lock_guard<std::mutex> lk(g_ov_mu);
     Overlap* ov = P >= kMinOverlapRows && P <= kMaxOverlapRows ? overlap_state() : nullptr;
-    const int64_t a = ov ? overlap_rows(*ov, P) : 0;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (ov && hipStreamIsCapturing(s, &cap) != hipSuccess) {
+      (void)hipGetLastError();
+      cap = hipStreamCaptureStatusNone;
+    }
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    const int64_t a = ov ? overlap_rows(*ov, P, capturing) : 0;
     if (a > 0) {
       hipError_t e = hipEventRecord(ov->fork, s);
       if (e == hipSuccess) e = hipStreamWaitEvent(ov->side, ov->fork, 0);
@@ -903,7 +911,7 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
       ov->side_rows = a;
       ov->main_rows = P - a;
       ov->total_rows = P;
-      ov->pending = true;
+      ov->pending = !capturing;
       transformed = true;
     }
   }

@@ -98,3 +98,39 @@ def test_small_graph_and_bad_share():
         ps.set_overlap(8)
     with pytest.raises(ps.PinsageError):
         ps.set_overlap(-1)
+
+
+def test_medium_graph_capture(medium):
+    # The overlapped schedule forks and joins by events only, so the call can be
+    # captured into a HIP graph on the caller's stream. Replays (with eager work
+    # and synchronisations between them) must match the eager in-order result.
+    import paper_1806_01973_amd as ps
+    wl, g, x = medium
+    layers = _layers(wl, torch.float32, "dense_then_pool")
+    ps.set_overlap(0)
+    ref_job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
+    ref = ref_job.run(x).clone()
+    torch.cuda.synchronize()
+    ps.set_overlap(4)
+    job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    job.run(x, s)  # eager call first: creates the masked streams
+    torch.cuda.synchronize()
+    print("[case] overlap schedule captured into a graph, 1.2M nodes f32", flush=True)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        job.run(x, s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        job.out.zero_()
+        job.nbr.idx.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        print(f"[case] replay {rep}", flush=True)
+        assert torch.equal(job.nbr.idx, ref_job.nbr.idx), f"replay {rep}: neighbourhoods"
+        assert torch.equal(job.out, ref), f"replay {rep}: embeddings"
+        assert int(job.steps.item()) == int(ref_job.steps.item())
+    del graph
+    torch.cuda.synchronize()
