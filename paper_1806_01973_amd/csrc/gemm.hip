@@ -725,10 +725,10 @@ hipError_t launch_cfg(const GemmLaunch& a, hipStream_t s) {
 #define PINSAGE_CFG_Q_F32 Cfg<false, 256, 256, 4, 4, false, 4>
 #endif
 #ifndef PINSAGE_CFG_W256_BF16
-#define PINSAGE_CFG_W256_BF16 Cfg<true, 256, 256, 2, 2, true, 4>
+#define PINSAGE_CFG_W256_BF16 Cfg<true, 128, 256, 2, 4, true, 3>
 #endif
 #ifndef PINSAGE_CFG_W256_F32
-#define PINSAGE_CFG_W256_F32 Cfg<false, 256, 256, 4, 4, true, 3>
+#define PINSAGE_CFG_W256_F32 Cfg<false, 128, 256, 2, 4, true, 3>
 #endif
 #ifndef PINSAGE_CFG_W512_BF16
 #define PINSAGE_CFG_W512_BF16 Cfg<true, 128, 512, 2, 4, true, 3>
