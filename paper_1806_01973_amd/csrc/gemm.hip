@@ -589,6 +589,11 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
     constexpr int cur = decltype(CUR)::value, nxt = cur ^ 1;
     Frags f[2];
     read_frags(cur, 0, f[0]);
+    // Scheduling fences at the k-step boundaries keep each step's fragment
+    // reads inside the previous step, so the MFMAs wait only on reads issued
+    // a whole k-step earlier (left to itself the scheduler pulled the current
+    // step's B reads in between its own MFMAs, exposing their latency).
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       // A quarter of chunk c + 1's LDS writes and of chunk c + 3's loads per
@@ -621,6 +626,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_rs_kernel(GemmLaunch a) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
         __builtin_amdgcn_sched_group_barrier(0x020, PER, 0);  // VMEM read
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();
   };
