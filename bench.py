@@ -318,6 +318,17 @@ def bench_embed_all(args, wl, inp):
                               # many eighths of the CUs (0: in order); its launches
                               # and the walk's then time their shared duration
                               "overlap_cu_eighths": args.overlap}}
+    if args.overlap:
+        # The walk kernel alone on every CU (outside the timed steps), next to
+        # its rate on its share of the CUs inside the overlapped step.
+        ps.profile_enable(True)
+        for _ in range(3):
+            ps.build_neighborhoods(inp["g"], wl.walks, wl.hops, wl.T, wl.seed, out=job.nbr,
+                                   count_steps=False, stream=stream)
+        torch.cuda.synchronize()
+        n_w, ms_w = ps.profile_read()["walk_topt"]
+        ps.profile_enable(False)
+        extra["walk_steps_per_s_all_cus"] = walk_steps / (ms_w / n_w * 1e-3)
     if compare_dataflow(args, wl):
         # The other evaluation order of the same layers, timed the same way
         # (same inputs, same steps), for comparison only.
@@ -737,6 +748,7 @@ def main() -> int:
                    "edges": inp["num_edges"], "gpu": torch.cuda.get_device_name(0),
                    **extra["config_extra"]},
         "walk_steps_per_s": extra["walk_steps_per_s"],
+        "walk_steps_per_s_all_cus": extra.get("walk_steps_per_s_all_cus"),
         "layers_embeddings_per_s": extra.get("layers_embeddings_per_s"),
         "alt_dataflow": extra.get("alt_dataflow"),
         "roofline": roofline_of(kernels, wl),
