@@ -304,13 +304,15 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
  * cu_eighths in [1, 7]: the first layer's transform of a leading share of
  * the pins runs on cu_eighths / 8 of the CUs (whole groups of 8 CUs, spread
  * evenly over the mask) while the walks run on the rest; the share of the
- * pins follows the last completed call's timing on the device. 0: walks, then transform, in order on the caller's stream. Default
- * 4. Process-wide; takes effect at the next pinsage_embed_all call. Streams
- * and events are created on a device's first overlapped call; a call that
- * changes the share waits for their work and destroys them, so a caller that
- * tears the runtime down itself (or runs under a profiler) releases them
- * first with pinsage_set_overlap(0). Concurrent pinsage_embed_all calls on one device are
- * serialised while they enqueue. Errors: PINSAGE_EINVAL outside [0, 7]. */
+ * pins follows the last completed call's timing on the device. 0: walks,
+ * then transform, in order on the caller's stream. Default 4. Process-wide;
+ * takes effect at the next pinsage_embed_all call. Streams and events are
+ * created on a device's first overlapped call; a call that changes the share
+ * waits (on the host) for their work and destroys them, so a caller that
+ * tears the runtime down itself, or runs under a profiler, releases them
+ * first with pinsage_set_overlap(0). Concurrent pinsage_embed_all calls on
+ * one device are serialised while they enqueue. Errors: PINSAGE_EINVAL
+ * outside [0, 7]. */
 int pinsage_set_overlap(int32_t cu_eighths);
 
 /* Workspace bytes needed by pinsage_output_mlp for n rows. */

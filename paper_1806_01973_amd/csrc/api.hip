@@ -1,7 +1,8 @@
 // C ABI of libpinsage.so: argument validation, workspace layout, the
 // layer-wise driver (Sec. 3.4) and per-launch timing. Every floating-point or
 // graph step runs in the gfx950 kernels; this file only checks arguments and
-// sequences launches on the caller's stream.
+// sequences launches on the caller's stream (the all-node job also forks two
+// CU-masked streams of its own from it and joins them back).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
