@@ -9,7 +9,10 @@ in-order one (walks, then the whole transform on the caller's stream):
 * the 1.2M-node fp32 graph, both layer dataflows, side CU shares of 2/8, 3/8
   and 4/8, three calls in a row (the pin share moves between calls);
 * a 4.5M-node graph with more pins than one 4,194,304-row chunk and a tiny
-  graph: both outside the overlapped range, so every share runs in order.
+  graph: both outside the overlapped range, so every share runs in order;
+* int64 row offsets with weights derived from counts, at 2^18 pins (the
+  smallest overlapped size) and 2^18 - 1 pins (in order);
+* the overlapped call captured into a HIP graph and replayed.
 The outputs themselves are checked against the oracle by the other GPU tests.
 """
 
@@ -134,3 +137,29 @@ def test_medium_graph_capture(medium):
         assert int(job.steps.item()) == int(ref_job.steps.item())
     del graph
     torch.cuda.synchronize()
+
+
+def test_offsets64_count_weights_and_threshold():
+    # int64 row offsets with weights derived from counts (no weight table), and
+    # graphs at the pin-count threshold: 2^18 pins overlap, 2^18 - 1 do not.
+    # Every schedule must match the in-order one bit for bit.
+    import paper_1806_01973_amd as ps
+    base = synth.WORKLOADS["medium"]
+    for pins, boards, off64 in ((1 << 18, 60_000, True), ((1 << 18) - 1, 60_000, False)):
+        wl = dataclasses.replace(base.scaled(pins, boards, "overlap-threshold"), walks=30)
+        data = synth.make_workload(wl)
+        g = ps.DeviceGraph(data["offsets"], data["col"], wl.num_pins, wl.num_boards,
+                           offsets64=off64)
+        x = torch.as_tensor(data["x"]).cuda()
+        layers = _layers(wl, torch.float32, "dense_then_pool")
+        print(f"[case] schedules, {pins} pins, offsets64={off64}, weights from counts",
+              flush=True)
+        outs = []
+        for k in (0, 4, 4):
+            ps.set_overlap(k)
+            job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed, weights=False)
+            out = job.run(x).clone()
+            torch.cuda.synchronize()
+            outs.append((k, out, job.nbr.idx.clone(), int(job.steps.item())))
+        ps.set_overlap(4)
+        _same(outs, f"{pins} pins")
