@@ -311,3 +311,14 @@ def test_output_mlp_validation(L):
                                                 ctypes.byref(ok), 3, 2, 0, ctypes.byref(n)) == 0
     a = lambda b: (b + 255) // 256 * 256
     assert n.value == n0.value + a(8 * 32 * 4) + a(8 * 96 * 4)  # z and hidden rows of S^(2)
+
+
+def test_set_overlap_validation(L):
+    # Host-only paths: no masked stream exists until an overlapped call, so
+    # changing the share touches no device.
+    lib = L.lib()
+    assert lib.pinsage_set_overlap(8) == L.PINSAGE_EINVAL
+    assert lib.pinsage_set_overlap(-1) == L.PINSAGE_EINVAL
+    assert b"cu_eighths" in lib.pinsage_last_error()
+    for k in (0, 3, 7, 4):
+        assert lib.pinsage_set_overlap(k) == 0
