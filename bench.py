@@ -7,7 +7,10 @@ CONVOLVE layers over every node, layer by layer. Inputs are resident in HBM
 before timing starts. The layers run in the dense-then-pool order (the
 neighbour half of W applied per pin before the weighted mean, which is
 linear); the line also carries the time of Algorithm 1's printed order on the
-same inputs (`alt_dataflow`), and both orders are parity-tested.
+same inputs (`alt_dataflow`), and both orders are parity-tested. The first
+layer's transform runs beside the walks on half of the CUs (`--overlap 4`,
+CU-masked streams inside the library; `--overlap 0` runs them in order); the
+output is the same bit for bit.
 
 Other workloads (measurement of the other rows; not the headline):
   --workload tiny | large | shard   all-node embedding of that graph
@@ -26,8 +29,9 @@ Other workloads (measurement of the other rows; not the headline):
                                     graph: 4096 walks x 4 landings each, ranks
                                     2000-5000, --hard-neg draws per query
 
-Prints one JSON line: throughput of the whole step, walk steps/s, node
-embeddings/s over the layer kernels alone (walks excluded), per-kernel
+Prints one JSON line: throughput of the whole step, walk steps/s (in the
+step, and for the walk kernel alone on all CUs), node embeddings/s over the
+layer kernels alone (in-order schedule only), per-kernel
 times from hipEvents recorded around every launch in the timed region, the
 roofline of the dominant kernel and the CPU oracle timed on a bounded sample
 of the same workload.
