@@ -7,7 +7,8 @@ order whatever the split, so every schedule must give the same bits as the
 in-order one (walks, then the whole transform on the caller's stream):
 
 * the 1.2M-node fp32 graph, both layer dataflows, side CU shares of 2/8, 3/8
-  and 4/8, three calls in a row (the pin share moves between calls);
+  and 4/8, three calls in a row (the pin share moves between calls), and the
+  same graph in bf16;
 * a 4.5M-node graph with more pins than one 4,194,304-row chunk and a tiny
   graph: both outside the overlapped range, so every share runs in order;
 * int64 row offsets with weights derived from counts, at 2^18 pins (the
@@ -163,3 +164,13 @@ def test_offsets64_count_weights_and_threshold():
             outs.append((k, out, job.nbr.idx.clone(), int(job.steps.item())))
         ps.set_overlap(4)
         _same(outs, f"{pins} pins")
+
+
+def test_medium_bf16_schedules_agree(medium):
+    # bf16 storage: the first transform runs in the register-staged GEMM on the
+    # side stream; the split must not change a bit either.
+    wl, g, x = medium
+    print("[case] overlap schedules, 1.2M nodes bf16 dense_then_pool", flush=True)
+    layers = _layers(wl, torch.bfloat16, "dense_then_pool")
+    outs = _runs(g, layers, wl, x.to(torch.bfloat16), (0, 4), 3)
+    _same(outs, "medium bf16")
