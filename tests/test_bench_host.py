@@ -1,0 +1,111 @@
+"""Host-side logic of bench.py (no GPU): the per-kernel table, the algorithmic
+work per launch behind the roofline, the choice of the dominant kernel, the
+counter-summary lookup keyed by the kernel's source hash, and the one-GPU
+refusal of --gpus N > 1."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import synth  # noqa: E402
+
+
+class _Layer:
+    def __init__(self, d_in, m, d_out, dataflow):
+        self.d_in, self.m, self.d_out, self.dataflow = d_in, m, d_out, dataflow
+
+
+def _medium_kernels():
+    # Two timed steps of the 1.2M-node job: per step one walk, two launches of
+    # each layer kernel (hipEvent totals in ms).
+    prof = {"walk_topt": (2, 20.0), "pool": (4, 26.0), "gemm_q": (4, 10.0),
+            "gemm_r": (4, 9.0), "gemm_w": (4, 6.0), "loss": (0, 0.0)}
+    return bench.kernel_table(prof, 2)
+
+
+def test_kernel_table():
+    k = _medium_kernels()
+    assert "loss" not in k
+    assert k["pool"] == {"launches": 4, "avg_ms": 6.5, "ms_per_step": 13.0}
+    assert k["walk_topt"]["ms_per_step"] == 10.0
+
+
+def test_algorithmic_work_per_launch():
+    wl = synth.WORKLOADS["medium"]
+    N, P = wl.num_nodes, wl.num_pins
+    layers = [_Layer(256, 512, 256, "dense_then_pool")] * 2
+    k = _medium_kernels()
+    live, steps = 53_815_669, 639_125_000
+    bench.add_rooflines(k, wl, layers, N, P, live, True, steps, 2)
+    # Pool: gathered d_out-wide fp32 rows + idx and weights + the written rows, per layer.
+    per_layer = live * 256 * 4 + N * wl.T * 8 + N * 256 * 4
+    assert k["pool"]["algo_bytes_per_launch"] == pytest.approx(per_layer)
+    assert k["pool"]["achieved_GBs"] == pytest.approx(per_layer / 6.5e-3 / 1e9)
+    # GEMMs: 2 P d_in m (Q), 2 P m d_out (R), 2 N d_in d_out (W, dense then pool).
+    assert k["gemm_q"]["algo_flops_per_launch"] == pytest.approx(2.0 * P * 256 * 512)
+    assert k["gemm_r"]["algo_flops_per_launch"] == pytest.approx(2.0 * P * 512 * 256)
+    assert k["gemm_w"]["algo_flops_per_launch"] == pytest.approx(2.0 * N * 256 * 256)
+    assert k["gemm_w"]["frac_mfma"] == pytest.approx(
+        2.0 * N * 256 * 256 / 1.5e-3 / 1e12 / 157.3)
+    # Walk: 12 B per edge step with int32 row offsets.
+    assert k["walk_topt"]["algo_bytes_per_launch"] == pytest.approx(steps * 12)
+    # Pool then dense: the pool gathers m-wide rows and W has K = d_in + m.
+    k2 = _medium_kernels()
+    del k2["gemm_r"]
+    bench.add_rooflines(k2, wl, [_Layer(256, 512, 256, "pool_then_dense")] * 2, N, P, live,
+                        True, steps, 2)
+    assert k2["pool"]["algo_bytes_per_launch"] == pytest.approx(
+        live * 512 * 4 + N * wl.T * 8 + N * 512 * 4)
+    assert k2["gemm_w"]["algo_flops_per_launch"] == pytest.approx(2.0 * N * 768 * 256)
+
+
+def test_dominant_kernel_roofline_and_traffic():
+    wl = synth.WORKLOADS["medium"]
+    k = _medium_kernels()
+    bench.add_rooflines(k, wl, [_Layer(256, 512, 256, "dense_then_pool")] * 2,
+                        wl.num_nodes, wl.num_pins, 53_815_669, True, 639_125_000, 2)
+    r = bench.roofline_of(k, wl)
+    assert r["kernel"] == "pool" and r["bound"] == "hbm" and r["unit"] == "GB/s"
+    assert r["peak"] == 8000.0 and r["frac"] == pytest.approx(r["achieved"] / 8000.0)
+    with open(os.path.join(ROOT, "profiles", "traffic.json")) as f:
+        table = json.load(f)
+    assert r["traffic"] == table["pool.hip:medium"]["bytes_per_launch"]
+    # A GEMM-dominated step reports the MFMA roofline for its dtype and no traffic.
+    k["gemm_q"]["ms_per_step"] = 100.0
+    r = bench.roofline_of(k, wl)
+    assert r["kernel"] == "gemm_q" and r["bound"] == "mfma" and r["peak"] == 157.3
+    assert r["traffic"] is None
+
+
+def test_counter_summaries_match_current_sources():
+    # Every committed counter summary was taken on the kernel source now in the
+    # tree (else the bench reports no traffic for it, and the summary is stale).
+    with open(os.path.join(ROOT, "profiles", "traffic.json")) as f:
+        table = json.load(f)
+    for key, ent in table.items():
+        src = key.split(":")[0]
+        assert ent["source_sha"] == bench.kernel_source_hash(src), key
+        assert os.path.exists(os.path.join(ROOT, ent["profile"])), key
+
+
+def test_stale_source_gives_no_traffic(monkeypatch, tmp_path):
+    (tmp_path / "traffic.json").write_text(json.dumps(
+        {"pool.hip:medium": {"source_sha": "0000000000000000", "bytes_per_launch": 1.0,
+                             "profile": "x"}}))
+    monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path))
+    assert bench.load_traffic("pool.hip", "medium") is None
+    assert bench.load_traffic("walk.hip", "medium") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in (r.stdout + r.stderr)
