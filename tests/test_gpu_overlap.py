@@ -7,8 +7,8 @@ order whatever the split, so every schedule must give the same bits as the
 in-order one (walks, then the whole transform on the caller's stream):
 
 * the 1.2M-node fp32 graph, both layer dataflows, side CU shares of 2/8, 3/8
-  and 4/8, three calls in a row (the pin share moves between calls), and the
-  same graph in bf16;
+  and 4/8, three calls in a row (the pin share moves between calls), the
+  same graph in bf16, and a single layer (the overlapped layer is the last);
 * a 4.5M-node graph with more pins than one 4,194,304-row chunk and a tiny
   graph: both outside the overlapped range, so every share runs in order;
 * int64 row offsets with weights derived from counts, at 2^18 pins (the
@@ -174,3 +174,13 @@ def test_medium_bf16_schedules_agree(medium):
     layers = _layers(wl, torch.bfloat16, "dense_then_pool")
     outs = _runs(g, layers, wl, x.to(torch.bfloat16), (0, 4), 3)
     _same(outs, "medium bf16")
+
+
+def test_medium_single_layer_schedules_agree(medium):
+    # K = 1: the overlapped first layer is also the last one (its W GEMM writes
+    # the output directly).
+    wl, g, x = medium
+    print("[case] overlap schedules, 1.2M nodes f32, one layer", flush=True)
+    layers = _layers(wl, torch.float32, "dense_then_pool")[:1]
+    outs = _runs(g, layers, wl, x, (0, 4), 2)
+    _same(outs, "medium K=1")
