@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 7
+#define PINSAGE_ABI_VERSION 8
 
 enum {
   PINSAGE_OK = 0,
@@ -277,6 +277,30 @@ int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64
                            void* h_out, int64_t n_out, void* workspace, size_t workspace_bytes,
                            void* stream);
 
+/* Schedule of pinsage_embed_all (Sec. 3.4 leaves it open: the first layer's
+ * transform of the pins reads only the features, not the neighbourhoods).
+ * A schedule is a caller-owned handle holding two CU-masked streams of the
+ * device current at creation and four events: the first layer's transform of
+ * a leading share of the pins runs on cu_eighths / 8 of the CUs (whole groups
+ * of 8 CUs, spread evenly over the mask) while the walks run on the rest; the
+ * share of the pins follows the timing of the last completed call made with
+ * the same schedule. The library keeps no stream, event or other device state
+ * of its own between calls.
+ *   pinsage_schedule_create   cu_eighths in [1, 7]; *out receives the handle.
+ *                             Errors: PINSAGE_EINVAL (share, NULL out),
+ *                             PINSAGE_EUNSUPPORTED (fewer than 64 CUs),
+ *                             PINSAGE_EHIP (stream or event creation; nothing
+ *                             is left allocated).
+ *   pinsage_schedule_destroy  waits (on the host) for the schedule's streams,
+ *                             then destroys them, its events and the handle.
+ *                             NULL is a no-op. Call it before the HIP runtime
+ *                             (or a profiler attached to it) is torn down, and
+ *                             not while another thread uses the handle.
+ * Calls that share one schedule are serialised while they enqueue. */
+typedef struct pinsage_schedule pinsage_schedule_t;
+int pinsage_schedule_create(int32_t cu_eighths, pinsage_schedule_t** out);
+int pinsage_schedule_destroy(pinsage_schedule_t* schedule);
+
 /* Workspace bytes needed by pinsage_embed_all. */
 int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_layer_t* layers, int32_t num_layers,
@@ -289,31 +313,18 @@ int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
  * h_out: device [num_nodes][layers[K-1].d_out]; nbr_out: caller buffers with
  * rows = num_nodes and top_t = walk->top_t (weights may be NULL).
  * layers[k].d_in must equal layers[k-1].d_out; one storage dtype throughout.
- * With 262,144 to 4,194,304 pins the walks and the first layer's transform
- * run beside each other on two library-owned CU-masked streams forked from
- * (and joined back into) `stream`; see pinsage_set_overlap. The output does
- * not depend on that schedule. */
+ * schedule: NULL (walks, then the transform, in order on `stream`) or a
+ * handle from pinsage_schedule_create on the current device (else
+ * PINSAGE_EINVAL): with 262,144 to 4,194,304 pins the walks and the first
+ * layer's transform then run beside each other on its masked streams, forked
+ * from and joined back into `stream` by events (also on error returns), so
+ * the call stays asynchronous and may be captured into a graph; other pin
+ * counts run in order. The output does not depend on the schedule. */
 int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                       const pinsage_layer_t* layers, int32_t num_layers, const void* x,
                       pinsage_neighborhoods_t* nbr_out, void* h_out,
                       unsigned long long* total_steps, void* workspace,
-                      size_t workspace_bytes, void* stream);
-
-/* Schedule of pinsage_embed_all (Sec. 3.4 leaves it open: the first layer's
- * transform of the pins reads only the features, not the neighbourhoods).
- * cu_eighths in [1, 7]: the first layer's transform of a leading share of
- * the pins runs on cu_eighths / 8 of the CUs (whole groups of 8 CUs, spread
- * evenly over the mask) while the walks run on the rest; the share of the
- * pins follows the last completed call's timing on the device. 0: walks,
- * then transform, in order on the caller's stream. Default 4. Process-wide;
- * takes effect at the next pinsage_embed_all call. Streams and events are
- * created on a device's first overlapped call; a call that changes the share
- * waits (on the host) for their work and destroys them, so a caller that
- * tears the runtime down itself, or runs under a profiler, releases them
- * first with pinsage_set_overlap(0). Concurrent pinsage_embed_all calls on
- * one device are serialised while they enqueue. Errors: PINSAGE_EINVAL
- * outside [0, 7]. */
-int pinsage_set_overlap(int32_t cu_eighths);
+                      size_t workspace_bytes, pinsage_schedule_t* schedule, void* stream);
 
 /* Workspace bytes needed by pinsage_output_mlp for n rows. */
 int pinsage_output_mlp_workspace_size(const pinsage_mlp_t* mlp, int64_t n, size_t* bytes);

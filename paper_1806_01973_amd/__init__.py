@@ -15,6 +15,7 @@ from .api import (  # noqa: F401
     EmbedAllBipartite,
     Minibatch,
     Neighborhoods,
+    Schedule,
     build_graph_neighborhoods,
     build_neighborhoods,
     convolve_layer,
@@ -26,5 +27,4 @@ from .api import (  # noqa: F401
     output_mlp,
     profile_enable,
     profile_read,
-    set_overlap,
 )

@@ -2,7 +2,6 @@
 
 from __future__ import annotations
 
-import atexit
 import ctypes
 import os
 
@@ -31,7 +30,8 @@ EXPORTED = [
     "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_build_graph_neighborhoods",
     "pinsage_embed_all_bipartite_workspace_size", "pinsage_embed_all_bipartite",
     "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
-    "pinsage_embed_all_workspace_size", "pinsage_embed_all", "pinsage_set_overlap",
+    "pinsage_embed_all_workspace_size", "pinsage_embed_all",
+    "pinsage_schedule_create", "pinsage_schedule_destroy",
     "pinsage_output_mlp_workspace_size",
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
@@ -126,8 +126,9 @@ def lib():
                                                    i32, ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_embed_all.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),
                                     ctypes.POINTER(Layer), i32, P, ctypes.POINTER(Neighborhoods),
-                                    P, P, P, ctypes.c_size_t, P]
-    L.pinsage_set_overlap.argtypes = [i32]
+                                    P, P, P, ctypes.c_size_t, P, P]
+    L.pinsage_schedule_create.argtypes = [i32, ctypes.POINTER(ctypes.c_void_p)]
+    L.pinsage_schedule_destroy.argtypes = [P]
     L.pinsage_output_mlp_workspace_size.argtypes = [ctypes.POINTER(MLP), i64,
                                                     ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_output_mlp.argtypes = [ctypes.POINTER(MLP), P, i64, P, P, ctypes.c_size_t, P]
@@ -150,9 +151,6 @@ def lib():
         if fn.restype is None or fn.restype is ctypes.c_int:
             fn.restype = ctypes.c_int
     _lib = L
-    # The library's CU-masked streams go while the runtime (and any profiler
-    # attached to it) is still whole.
-    atexit.register(L.pinsage_set_overlap, 0)
     return L
 
 

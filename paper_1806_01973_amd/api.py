@@ -263,11 +263,40 @@ def embed_all_workspace_size(graph: DeviceGraph, layers: Sequence[DeviceLayer]) 
     return int(n.value)
 
 
+class Schedule:
+    """A caller-owned schedule of the all-node job (pinsage_schedule_t): two
+    CU-masked streams of the current device, on which the walks and the first
+    layer's transform of a leading share of the pins run beside each other
+    (the transform on cu_eighths / 8 of the CUs). close() waits for them and
+    destroys them; so does garbage collection."""
+
+    def __init__(self, cu_eighths: int):
+        h = ctypes.c_void_p(None)
+        L.check(L.lib().pinsage_schedule_create(int(cu_eighths), ctypes.byref(h)),
+                "pinsage_schedule_create")
+        self.cu_eighths = int(cu_eighths)
+        self.handle = h.value
+
+    def close(self) -> None:
+        h, self.handle = getattr(self, "handle", None), None
+        if h:
+            L.check(L.lib().pinsage_schedule_destroy(h), "pinsage_schedule_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 class EmbedAll:
-    """Preallocated all-node embedding job (neighbourhoods + K layers, Sec. 3.4)."""
+    """Preallocated all-node embedding job (neighbourhoods + K layers, Sec. 3.4).
+    overlap: 0 runs the walks and the first transform in order; 1-7 gives the
+    job a Schedule on that many eighths of the CUs (used for graphs of 2^18 to
+    2^22 pins; the output is the same bits either way)."""
 
     def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
-                 T: int, seed: int, weights: bool = True):
+                 T: int, seed: int, weights: bool = True, overlap: int = 0):
         self.graph, self.layers = graph, list(layers)
         self.walk = L.WalkParams(seed, walks, hops, T)
         dev = graph.col.device
@@ -280,16 +309,23 @@ class EmbedAll:
         self._g = graph.struct()
         self._layers = _layer_array(self.layers)
         self._nbr = self.nbr.struct()
+        self.schedule = Schedule(overlap) if overlap else None
 
     def run(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         x = _dev(x, "x", self.layers[0].dtype)
+        sched = self.schedule.handle if self.schedule is not None else None
         st = L.lib().pinsage_embed_all(ctypes.byref(self._g), ctypes.byref(self.walk),
                                        self._layers, len(self.layers), _ptr(x),
                                        ctypes.byref(self._nbr), _ptr(self.out), _ptr(self.steps),
-                                       _ptr(self.workspace), self.workspace.numel(),
+                                       _ptr(self.workspace), self.workspace.numel(), sched,
                                        _stream(stream))
         L.check(st, "pinsage_embed_all")
         return self.out
+
+    def close(self) -> None:
+        if self.schedule is not None:
+            self.schedule.close()
+            self.schedule = None
 
 
 def build_graph_neighborhoods(graph: DeviceGraph, T: int, seed: int,
@@ -439,12 +475,6 @@ class Minibatch:
 
     def _mlp_ref(self):
         return ctypes.byref(self._mlp) if self._mlp is not None else None
-
-
-def set_overlap(cu_eighths: int) -> None:
-    """Schedule of EmbedAll: the first layer's transform beside the walks on
-    cu_eighths/8 of the CUs (1-7), or walks then transform in order (0)."""
-    L.check(L.lib().pinsage_set_overlap(int(cu_eighths)), "pinsage_set_overlap")
 
 
 def profile_enable(on: bool = True) -> None:

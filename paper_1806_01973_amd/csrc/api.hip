@@ -1,8 +1,9 @@
 // C ABI of libpinsage.so: argument validation, workspace layout, the
 // layer-wise driver (Sec. 3.4) and per-launch timing. Every floating-point or
 // graph step runs in the gfx950 kernels; this file only checks arguments and
-// sequences launches on the caller's stream (the all-node job also forks two
-// CU-masked streams of its own from it and joins them back).
+// sequences launches on the caller's stream (the all-node job may also fork
+// the two CU-masked streams of a caller-owned schedule from it and join them
+// back).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -382,20 +383,44 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
 // run on CU-masked streams forked from the caller's stream: the transform of
 // the first `a` pins on a side stream holding a share of the CUs, the walks on
 // the other CUs. The remaining pins are transformed on the caller's stream
-// (all CUs) once the walks are done, and the pool waits for both.
+// (all CUs) once the walks are done, and the pool waits for both. The masked
+// streams and the events belong to a caller-owned pinsage_schedule_t
+// (created and destroyed by explicit calls); the library keeps none.
 //
-// `a` comes from the last call on the device whose events have completed: with
-// side rate rs and full-chip rate rf (rows per ms) and walk time tw, the side
-// and the caller's stream end together when a / rs = tw + (P - a) / rf, i.e.
-// a = rs (rf tw + P) / (rf + rs). The GEMMs sum every row in the same order
-// whatever the split, so the output does not depend on `a`.
+// `a` comes from the last call on the schedule whose events have completed:
+// with side rate rs and full-chip rate rf (rows per ms) and walk time tw, the
+// side and the caller's stream end together when a / rs = tw + (P - a) / rf,
+// i.e. a = rs (rf tw + P) / (rf + rs). The GEMMs sum every row in the same
+// order whatever the split, so the output does not depend on `a`.
 //
 // Masks: byte j of the CU mask (8 consecutive CUs) goes to the side when
 // floor((j + 1) k / 8) > floor(j k / 8), k = the share in eighths, which spreads
 // the side's bytes evenly over the mask words.
-struct Overlap {
-  int eighths = -1;
-  bool ok = false;
+
+// Pin counts that overlap: at least 2^18, and at most one transform chunk.
+// With more pins the graph outgrows the MALL, the walks become bound by HBM
+// latency and need every CU (measured on 10M pins: the walks slowed by more
+// than the transform share saved), so larger graphs run in order.
+constexpr int64_t kMinOverlapRows = 1ll << 18;
+constexpr int64_t kMaxOverlapRows = kChunkRows;
+
+void schedule_release(pinsage_schedule* o);
+
+// The side's rows for this call, after folding in the last call's timing when
+// its events have completed. While the caller's stream is being captured into
+// a graph the events are neither read nor marked for reading (their records
+// are graph nodes, not timings). With o->mu held.
+int64_t overlap_rows(pinsage_schedule& o, int64_t n_transform, bool capturing);
+}  // namespace
+}  // namespace pinsage
+
+// A caller-owned schedule of pinsage_embed_all: two CU-masked streams of one
+// device, the events that fork and join them, and the timing that sets the
+// side's share of the pins.
+struct pinsage_schedule {
+  int device = 0;
+  int eighths = 0;
+  std::mutex mu;
   hipStream_t side = nullptr, walk = nullptr;
   hipEvent_t fork = nullptr, side_done = nullptr, walk_done = nullptr, main_done = nullptr;
   double alpha = 0.0;       // side rows / transformable rows for the next call
@@ -403,90 +428,29 @@ struct Overlap {
   int64_t side_rows = 0, main_rows = 0, total_rows = 0;  // of the last call
   bool pending = false;     // the last call's events have not been read
 };
-constexpr int kMaxDevices = 64;
-// Pin counts that overlap: at least 2^18, and at most one transform chunk.
-// With more pins the graph outgrows the MALL, the walks become bound by HBM
-// latency and need every CU (measured on 10M pins: the walks slowed by more
-// than the transform share saved), so larger graphs run in order.
-constexpr int64_t kMinOverlapRows = 1ll << 18;
-constexpr int64_t kMaxOverlapRows = kChunkRows;
-std::mutex g_ov_mu;
-int g_ov_eighths = 4;
-Overlap g_ov[kMaxDevices];
 
-// With g_ov_mu held: waits for and destroys a device's streams and events.
-void overlap_release(Overlap& o, int dev) {
-  if (o.side || o.walk || o.fork || o.side_done || o.walk_done || o.main_done) {
-    int cur = 0;
-    (void)hipGetDevice(&cur);
-    (void)hipSetDevice(dev);
-    for (hipStream_t st : {o.side, o.walk}) {
-      if (!st) continue;
-      (void)hipStreamSynchronize(st);
-      (void)hipStreamDestroy(st);
-    }
-    for (hipEvent_t ev : {o.fork, o.side_done, o.walk_done, o.main_done})
-      if (ev) (void)hipEventDestroy(ev);
-    (void)hipSetDevice(cur);
-    (void)hipGetLastError();
+namespace pinsage {
+namespace {
+
+// Waits for and destroys a schedule's streams and events (its device made
+// current for the calls), then frees it.
+void schedule_release(pinsage_schedule* o) {
+  int cur = 0;
+  const bool restore = hipGetDevice(&cur) == hipSuccess;
+  (void)hipSetDevice(o->device);
+  for (hipStream_t st : {o->side, o->walk}) {
+    if (!st) continue;
+    (void)hipStreamSynchronize(st);
+    (void)hipStreamDestroy(st);
   }
-  o = Overlap{};
+  for (hipEvent_t ev : {o->fork, o->side_done, o->walk_done, o->main_done})
+    if (ev) (void)hipEventDestroy(ev);
+  if (restore) (void)hipSetDevice(cur);
+  (void)hipGetLastError();
+  delete o;
 }
 
-
-// With g_ov_mu held: the current device's streams and events for the current
-// share, created on first use. nullptr when overlap is off or the runtime
-// refuses the masked streams (the caller then runs everything in order).
-Overlap* overlap_state() {
-  if (g_ov_eighths <= 0) return nullptr;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
-  Overlap& o = g_ov[dev];
-  if (o.eighths == g_ov_eighths) return o.ok ? &o : nullptr;
-  // First use on this device for the current share.
-  overlap_release(o, dev);
-  const int k = g_ov_eighths;
-  o.eighths = k;
-  o.alpha = k >= 4 ? 1.0 : 0.3 * k;  // first call: a rough share by CU count
-  o.rf_over_rs = 8.0 / k;
-  int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus < 64) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
-  const int words = (cus + 31) / 32;
-  std::vector<uint32_t> side_mask(words, 0u), walk_mask(words, 0u);
-  for (int i = 0; i < cus; ++i) {
-    const int j = i / 8;
-    const bool to_side = ((j + 1) * k) / 8 > (j * k) / 8;
-    (to_side ? side_mask : walk_mask)[i / 32] |= 1u << (i % 32);
-  }
-  bool good = hipExtStreamCreateWithCUMask(&o.side, (uint32_t)words, side_mask.data()) ==
-                  hipSuccess &&
-              hipExtStreamCreateWithCUMask(&o.walk, (uint32_t)words, walk_mask.data()) ==
-                  hipSuccess &&
-              hipEventCreate(&o.fork) == hipSuccess && hipEventCreate(&o.side_done) == hipSuccess &&
-              hipEventCreate(&o.walk_done) == hipSuccess &&
-              hipEventCreate(&o.main_done) == hipSuccess;
-  if (!good) {
-    (void)hipGetLastError();
-    overlap_release(o, dev);
-    o.eighths = k;  // do not retry this share
-    return nullptr;
-  }
-  o.ok = true;
-  return &o;
-}
-
-// With g_ov_mu held: the side's rows for this call, after folding in the last
-// call's timing when its events have completed. While the caller's stream is
-// being captured into a graph the events are neither read nor marked for
-// reading (their records are graph nodes, not timings).
-int64_t overlap_rows(Overlap& o, int64_t n_transform, bool capturing) {
+int64_t overlap_rows(pinsage_schedule& o, int64_t n_transform, bool capturing) {
   if (!capturing && o.pending && hipEventQuery(o.main_done) == hipSuccess &&
       hipEventQuery(o.side_done) == hipSuccess) {
     float ts = 0.0f, tw = 0.0f, tm = 0.0f;
@@ -711,6 +675,28 @@ int bipartite_ws(const pinsage_graph_t* graph, const pinsage_layer_t* layers, in
   w->map = align_up((size_t)n * 4);
   return PINSAGE_OK;
 }
+
+// Host-side checks shared by the two convolve_layer entry points.
+int check_convolve(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
+                   int64_t n_transform, const int32_t* transform_rows,
+                   const pinsage_neighborhoods_t* nbr, const int32_t* self_rows, void* h_out,
+                   int64_t n_out) {
+  int st = check_layer(layer, 0);
+  if (st) return st;
+  if (n_in < 0 || n_transform < 0 || n_out < 0) return fail(PINSAGE_EINVAL, "negative row count");
+  if (!transform_rows && n_transform > n_in)
+    return fail(PINSAGE_EINVAL, "n_transform (%lld) > n_in (%lld) without transform_rows",
+                (long long)n_transform, (long long)n_in);
+  if (!self_rows && n_out > n_in)
+    return fail(PINSAGE_EINVAL, "n_out (%lld) > n_in (%lld) without self_rows", (long long)n_out,
+                (long long)n_in);
+  if ((st = check_nbr(nbr, n_out, "convolve_layer"))) return st;
+  if (n_out == 0 && n_transform == 0) return PINSAGE_OK;
+  if ((n_in > 0 && !h_in) || (n_out > 0 && !h_out))
+    return fail(PINSAGE_EINVAL, "h_in or h_out is NULL");
+  return PINSAGE_OK;
+}
+
 }  // namespace
 }  // namespace pinsage
 
@@ -787,19 +773,10 @@ int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64
                            void* h_out, int64_t n_out, void* workspace, size_t workspace_bytes,
                            void* stream) {
   g_last_error.clear();
-  int st = check_layer(layer, 0);
+  int st = check_convolve(layer, h_in, n_in, n_transform, transform_rows, nbr, self_rows, h_out,
+                          n_out);
   if (st) return st;
-  if (n_in < 0 || n_transform < 0 || n_out < 0) return fail(PINSAGE_EINVAL, "negative row count");
-  if (!transform_rows && n_transform > n_in)
-    return fail(PINSAGE_EINVAL, "n_transform (%lld) > n_in (%lld) without transform_rows",
-                (long long)n_transform, (long long)n_in);
-  if (!self_rows && n_out > n_in)
-    return fail(PINSAGE_EINVAL, "n_out (%lld) > n_in (%lld) without self_rows", (long long)n_out,
-                (long long)n_in);
-  if ((st = check_nbr(nbr, n_out, "convolve_layer"))) return st;
   if (n_out == 0 && n_transform == 0) return PINSAGE_OK;
-  if ((n_in > 0 && !h_in) || (n_out > 0 && !h_out))
-    return fail(PINSAGE_EINVAL, "h_in or h_out is NULL");
   const size_t need = convolve_ws(layer, n_transform, n_out);
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
@@ -836,7 +813,7 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
                       const pinsage_layer_t* layers, int32_t num_layers, const void* x,
                       pinsage_neighborhoods_t* nbr_out, void* h_out,
                       unsigned long long* total_steps, void* workspace, size_t workspace_bytes,
-                      void* stream) {
+                      pinsage_schedule_t* schedule, void* stream) {
   g_last_error.clear();
   int st = check_graph(graph);
   if (st) return st;
@@ -877,42 +854,52 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   const int64_t P = graph->num_pins;
   const pinsage_layer_t* L0 = &layers[0];
 
-  // Walks, then the first layer's transform: beside each other on masked
-  // streams when the device allows it, else in order on the caller's stream.
+  // Walks, then the first layer's transform: beside each other on the
+  // schedule's masked streams when one is given and the pin count is in the
+  // overlapped range, else in order on the caller's stream.
   bool transformed = false;
-  {
-    std::lock_guard<std::mutex> lk(g_ov_mu);
-    Overlap* ov = P >= kMinOverlapRows && P <= kMaxOverlapRows ? overlap_state() : nullptr;
+  if (schedule && P >= kMinOverlapRows && P <= kMaxOverlapRows) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "current device");
+    if (dev != schedule->device)
+      return fail(PINSAGE_EINVAL, "schedule belongs to device %d, current device is %d",
+                  schedule->device, dev);
+    std::lock_guard<std::mutex> lk(schedule->mu);
+    pinsage_schedule& ov = *schedule;
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    if (ov && hipStreamIsCapturing(s, &cap) != hipSuccess) {
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) {
       (void)hipGetLastError();
       cap = hipStreamCaptureStatusNone;
     }
     const bool capturing = cap != hipStreamCaptureStatusNone;
-    const int64_t a = ov ? overlap_rows(*ov, P, capturing) : 0;
+    const int64_t a = overlap_rows(ov, P, capturing);
     if (a > 0) {
-      hipError_t e = hipEventRecord(ov->fork, s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(ov->side, ov->fork, 0);
-      if (e == hipSuccess) e = hipStreamWaitEvent(ov->walk, ov->fork, 0);
+      e = hipEventRecord(ov.fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ov.side, ov.fork, 0);
+      if (e == hipSuccess) e = hipStreamWaitEvent(ov.walk, ov.fork, 0);
       if (e != hipSuccess) return hip_fail(e, "stream fork");
-      st = run_transform_rows(L0, x, n, P, nullptr, n, ws, 0, a, 0, ov->side);
-      const hipError_t e1 = hipEventRecord(ov->side_done, ov->side);
+      // Every record and wait below runs whatever the launches returned, so
+      // the side and walk streams are joined back into the caller's stream
+      // on error paths too (no work of this call is left unjoined).
+      st = run_transform_rows(L0, x, n, P, nullptr, n, ws, 0, a, 0, ov.side);
+      const hipError_t e1 = hipEventRecord(ov.side_done, ov.side);
       if (!st) st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps,
-                                                ov->walk);
-      const hipError_t e2 = hipEventRecord(ov->walk_done, ov->walk);
+                                                ov.walk);
+      const hipError_t e2 = hipEventRecord(ov.walk_done, ov.walk);
       // Join: the caller's stream waits for the walks before its share of
       // the transform, and for the side before the pool.
-      const hipError_t e3 = hipStreamWaitEvent(s, ov->walk_done, 0);
+      const hipError_t e3 = hipStreamWaitEvent(s, ov.walk_done, 0);
       if (!st) st = run_transform_rows(L0, x, n, P, nullptr, n, ws, a, P, a, s);
-      const hipError_t e4 = hipEventRecord(ov->main_done, s);
-      const hipError_t e5 = hipStreamWaitEvent(s, ov->side_done, 0);
+      const hipError_t e4 = hipEventRecord(ov.main_done, s);
+      const hipError_t e5 = hipStreamWaitEvent(s, ov.side_done, 0);
       if (st) return st;
       for (hipError_t ej : {e1, e2, e3, e4, e5})
         if (ej != hipSuccess) return hip_fail(ej, "stream join");
-      ov->side_rows = a;
-      ov->main_rows = P - a;
-      ov->total_rows = P;
-      ov->pending = !capturing;
+      ov.side_rows = a;
+      ov.main_rows = P - a;
+      ov.total_rows = P;
+      ov.pending = !capturing;
       transformed = true;
     }
   }
@@ -933,14 +920,52 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   return PINSAGE_OK;
 }
 
-int pinsage_set_overlap(int32_t cu_eighths) {
+int pinsage_schedule_create(int32_t cu_eighths, pinsage_schedule_t** out) {
   g_last_error.clear();
-  if (cu_eighths < 0 || cu_eighths > 7)
-    return fail(PINSAGE_EINVAL, "cu_eighths %d outside [0, 7]", cu_eighths);
-  std::lock_guard<std::mutex> lk(g_ov_mu);
-  if (cu_eighths != g_ov_eighths)
-    for (int d = 0; d < kMaxDevices; ++d) overlap_release(g_ov[d], d);
-  g_ov_eighths = cu_eighths;
+  if (!out) return fail(PINSAGE_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (cu_eighths < 1 || cu_eighths > 7)
+    return fail(PINSAGE_EINVAL, "cu_eighths %d outside [1, 7]", cu_eighths);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "device query");
+  if (cus < 64) return fail(PINSAGE_EUNSUPPORTED, "device has %d CUs (< 64)", cus);
+  auto* o = new pinsage_schedule();
+  o->device = dev;
+  o->eighths = cu_eighths;
+  o->alpha = cu_eighths >= 4 ? 1.0 : 0.3 * cu_eighths;  // first call: a share by CU count
+  o->rf_over_rs = 8.0 / cu_eighths;
+  const int words = (cus + 31) / 32;
+  std::vector<uint32_t> side_mask(words, 0u), walk_mask(words, 0u);
+  for (int i = 0; i < cus; ++i) {
+    const int j = i / 8;
+    const bool to_side = ((j + 1) * cu_eighths) / 8 > (j * cu_eighths) / 8;
+    (to_side ? side_mask : walk_mask)[i / 32] |= 1u << (i % 32);
+  }
+  e = hipExtStreamCreateWithCUMask(&o->side, (uint32_t)words, side_mask.data());
+  if (e == hipSuccess) e = hipExtStreamCreateWithCUMask(&o->walk, (uint32_t)words, walk_mask.data());
+  if (e == hipSuccess) e = hipEventCreate(&o->fork);
+  if (e == hipSuccess) e = hipEventCreate(&o->side_done);
+  if (e == hipSuccess) e = hipEventCreate(&o->walk_done);
+  if (e == hipSuccess) e = hipEventCreate(&o->main_done);
+  if (e != hipSuccess) {
+    const int st = hip_fail(e, "masked stream / event creation");
+    schedule_release(o);
+    return st;
+  }
+  *out = o;
+  return PINSAGE_OK;
+}
+
+int pinsage_schedule_destroy(pinsage_schedule_t* schedule) {
+  g_last_error.clear();
+  if (!schedule) return PINSAGE_OK;
+  {
+    // A call still enqueueing on this schedule finishes first.
+    std::lock_guard<std::mutex> lk(schedule->mu);
+  }
+  schedule_release(schedule);
   return PINSAGE_OK;
 }
 

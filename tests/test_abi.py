@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 7
+    assert lib.pinsage_version() == 8
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -185,14 +185,14 @@ def test_layer_validation_and_workspace_sizes(L):
     walk = L.WalkParams(1, 10, 2, 8)
     nbr = L.Neighborhoods(15, 8, FAKE, FAKE, None)
     st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), bad, 2, FAKE,
-                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None)
+                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None, None)
     assert st == L.PINSAGE_EINVAL and b"d_in" in lib.pinsage_last_error()
     mixed = (L.Layer * 2)(_layer(L), _layer(L, dtype=L.PINSAGE_BF16))
     st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), mixed, 2, FAKE,
-                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None)
+                               ctypes.byref(nbr), FAKE, None, FAKE, 1 << 30, None, None)
     assert st == L.PINSAGE_EINVAL
     st = lib.pinsage_embed_all(ctypes.byref(g), ctypes.byref(walk), layers, 2, FAKE,
-                               ctypes.byref(nbr), FAKE, None, FAKE, 64, None)
+                               ctypes.byref(nbr), FAKE, None, FAKE, 64, None, None)
     assert st == L.PINSAGE_EWORKSPACE
 
 
@@ -313,12 +313,14 @@ def test_output_mlp_validation(L):
     assert n.value == n0.value + a(8 * 32 * 4) + a(8 * 96 * 4)  # z and hidden rows of S^(2)
 
 
-def test_set_overlap_validation(L):
-    # Host-only paths: no masked stream exists until an overlapped call, so
-    # changing the share touches no device.
+def test_schedule_validation(L):
+    # Host-only paths: the share and the output pointer are checked before any
+    # device call; destroying NULL is a no-op.
     lib = L.lib()
-    assert lib.pinsage_set_overlap(8) == L.PINSAGE_EINVAL
-    assert lib.pinsage_set_overlap(-1) == L.PINSAGE_EINVAL
-    assert b"cu_eighths" in lib.pinsage_last_error()
-    for k in (0, 3, 7, 4):
-        assert lib.pinsage_set_overlap(k) == 0
+    h = ctypes.c_void_p(None)
+    for bad in (8, 0, -1):
+        assert lib.pinsage_schedule_create(bad, ctypes.byref(h)) == L.PINSAGE_EINVAL
+        assert b"cu_eighths" in lib.pinsage_last_error()
+        assert h.value is None
+    assert lib.pinsage_schedule_create(4, None) == L.PINSAGE_EINVAL
+    assert lib.pinsage_schedule_destroy(None) == 0

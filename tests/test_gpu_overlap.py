@@ -1,8 +1,8 @@
 """GPU: the all-node job's schedule does not change its output.
 
 With 262,144 to 4,194,304 pins the walks and the first layer's transform of a
-leading share of the pins run beside each other on CU-masked streams, and the
-share follows the previous call's timing. The GEMMs sum every row in the same
+leading share of the pins run beside each other on the CU-masked streams of a
+caller-owned schedule, and the share follows the previous call's timing. The GEMMs sum every row in the same
 order whatever the split, so every schedule must give the same bits as the
 in-order one (walks, then the whole transform on the caller's stream):
 
@@ -37,14 +37,13 @@ def _runs(g, layers, wl, x, shares, calls):
     import paper_1806_01973_amd as ps
     outs = []
     for k in shares:
-        ps.set_overlap(k)
         print(f"[case] share {k}/8", flush=True)
-        job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
+        job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed, overlap=k)
         for _ in range(calls if k else 1):
             out = job.run(x).clone()
             torch.cuda.synchronize()
             outs.append((k, out, job.nbr.idx.clone(), int(job.steps.item())))
-    ps.set_overlap(4)
+        job.close()
     return outs
 
 
@@ -98,10 +97,9 @@ def test_small_graph_and_bad_share():
     print("[case] overlap below the pin threshold", flush=True)
     outs = _runs(g, _layers(wl, torch.float32, "dense_then_pool"), wl, x, (0, 7), 2)
     _same(outs, "tiny")
-    with pytest.raises(ps.PinsageError):
-        ps.set_overlap(8)
-    with pytest.raises(ps.PinsageError):
-        ps.set_overlap(-1)
+    for bad in (8, 0, -1):
+        with pytest.raises(ps.PinsageError):
+            ps.Schedule(bad)
 
 
 def test_medium_graph_capture(medium):
@@ -111,15 +109,13 @@ def test_medium_graph_capture(medium):
     import paper_1806_01973_amd as ps
     wl, g, x = medium
     layers = _layers(wl, torch.float32, "dense_then_pool")
-    ps.set_overlap(0)
     ref_job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
     ref = ref_job.run(x).clone()
     torch.cuda.synchronize()
-    ps.set_overlap(4)
-    job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed)
+    job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed, overlap=4)
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
-    job.run(x, s)  # eager call first: creates the masked streams
+    job.run(x, s)  # eager call first: times the split
     torch.cuda.synchronize()
     print("[case] overlap schedule captured into a graph, 1.2M nodes f32", flush=True)
     graph = torch.cuda.CUDAGraph()
@@ -138,6 +134,7 @@ def test_medium_graph_capture(medium):
         assert int(job.steps.item()) == int(ref_job.steps.item())
     del graph
     torch.cuda.synchronize()
+    job.close()
 
 
 def test_offsets64_count_weights_and_threshold():
@@ -157,12 +154,12 @@ def test_offsets64_count_weights_and_threshold():
               flush=True)
         outs = []
         for k in (0, 4, 4):
-            ps.set_overlap(k)
-            job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed, weights=False)
+            job = ps.EmbedAll(g, layers, wl.walks, wl.hops, wl.T, wl.seed, weights=False,
+                              overlap=k)
             out = job.run(x).clone()
             torch.cuda.synchronize()
             outs.append((k, out, job.nbr.idx.clone(), int(job.steps.item())))
-        ps.set_overlap(4)
+            job.close()
         _same(outs, f"{pins} pins")
 
 
