@@ -301,6 +301,25 @@ typedef struct pinsage_schedule pinsage_schedule_t;
 int pinsage_schedule_create(int32_t cu_eighths, pinsage_schedule_t** out);
 int pinsage_schedule_destroy(pinsage_schedule_t* schedule);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * pinsage_convolve_layer without the workspace argument. Its workspace is a
+ * static scratch array of PINSAGE_NOALLOC_SCRATCH_BYTES (64 MiB) compiled into
+ * the library, one per GPU, held until the process ends; the call itself
+ * allocates nothing. Arguments, layout and results are those of
+ * pinsage_convolve_layer (same kernels, bit-identical output). A layer whose
+ * workspace (pinsage_convolve_workspace_size) exceeds the scratch returns
+ * PINSAGE_EUNSUPPORTED and launches nothing. The scratch keeps the last call's
+ * contents (every region a call reads is written earlier in that call), and
+ * all calls on one GPU share it: calls that overlap on one GPU (two streams,
+ * two threads) race and must be serialised by the caller. */
+#define PINSAGE_NOALLOC_SCRATCH_BYTES (64ull << 20)
+int pinsage_convolve_layer_noalloc(const pinsage_layer_t* layer, const void* h_in,
+                                   int64_t n_in, int64_t n_transform,
+                                   const int32_t* transform_rows,
+                                   const pinsage_neighborhoods_t* nbr, const int32_t* self_rows,
+                                   void* h_out, int64_t n_out, void* stream);
+
 /* Workspace bytes needed by pinsage_embed_all. */
 int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
                                      const pinsage_layer_t* layers, int32_t num_layers,

@@ -29,7 +29,7 @@ EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
     "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_build_graph_neighborhoods",
     "pinsage_embed_all_bipartite_workspace_size", "pinsage_embed_all_bipartite",
-    "pinsage_convolve_workspace_size", "pinsage_convolve_layer",
+    "pinsage_convolve_workspace_size", "pinsage_convolve_layer", "pinsage_convolve_layer_noalloc",
     "pinsage_embed_all_workspace_size", "pinsage_embed_all",
     "pinsage_schedule_create", "pinsage_schedule_destroy",
     "pinsage_output_mlp_workspace_size",
@@ -122,6 +122,8 @@ def lib():
     L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64, P,
                                          ctypes.POINTER(Neighborhoods), P, P, i64, P,
                                          ctypes.c_size_t, P]
+    L.pinsage_convolve_layer_noalloc.argtypes = [ctypes.POINTER(Layer), P, i64, i64, P,
+                                                 ctypes.POINTER(Neighborhoods), P, P, i64, P]
     L.pinsage_embed_all_workspace_size.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(Layer),
                                                    i32, ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_embed_all.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(WalkParams),

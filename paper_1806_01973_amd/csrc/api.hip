@@ -697,6 +697,35 @@ int check_convolve(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
   return PINSAGE_OK;
 }
 
+// Scratch of pinsage_convolve_layer_noalloc: a file-scope device array, one
+// copy per GPU at its own address, held until the process ends. Host code
+// never uses the array's name as a device address: the address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// is kept per device.
+constexpr size_t kScratchBytes = (size_t)PINSAGE_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "current device");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(PINSAGE_EUNSUPPORTED, "device %d outside the %d devices with scratch", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "scratch symbol address");
+    if (!p) return fail(PINSAGE_EHIP, "scratch symbol address is NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PINSAGE_OK;
+}
 }  // namespace
 }  // namespace pinsage
 
@@ -784,6 +813,29 @@ int pinsage_convolve_layer(const pinsage_layer_t* layer, const void* h_in, int64
     return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
   return run_layer(layer, h_in, n_in, n_transform, transform_rows, nbr, self_rows, h_out, n_out,
                    workspace, static_cast<hipStream_t>(stream));
+}
+
+int pinsage_convolve_layer_noalloc(const pinsage_layer_t* layer, const void* h_in, int64_t n_in,
+                                   int64_t n_transform, const int32_t* transform_rows,
+                                   const pinsage_neighborhoods_t* nbr, const int32_t* self_rows,
+                                   void* h_out, int64_t n_out, void* stream) {
+  g_last_error.clear();
+  int st = check_convolve(layer, h_in, n_in, n_transform, transform_rows, nbr, self_rows, h_out,
+                          n_out);
+  if (st) return st;
+  if (n_out == 0 && n_transform == 0) return PINSAGE_OK;
+  const size_t need = convolve_ws(layer, n_transform, n_out);
+  if (need > kScratchBytes)
+    return fail(PINSAGE_EUNSUPPORTED,
+                "layer needs %zu bytes of scratch (n_transform %lld, n_out %lld); the static "
+                "scratch holds %zu",
+                need, (long long)n_transform, (long long)n_out, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws))) return st;
+  // Every scratch region the layer reads (P or R rows, the pooled chunk) is
+  // written earlier in the same call, so nothing has to start at zero.
+  return run_layer(layer, h_in, n_in, n_transform, transform_rows, nbr, self_rows, h_out, n_out,
+                   ws, static_cast<hipStream_t>(stream));
 }
 
 int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph, const pinsage_layer_t* layers,
