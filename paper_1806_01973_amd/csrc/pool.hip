@@ -244,6 +244,119 @@ __global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
   }
 }
 
+// Rows of at most 64 / RG vectors with at most 64 neighbour slots (every
+// workload's pooled width in the dense-then-pool order): the row's header --
+// neighbour ids and the weights, counts or neighbour count alpha needs -- is
+// one coalesced vector load (lane t holds slot t), alpha is formed per lane
+// with the same fp32 division as the batched kernels, and every live slot's
+// gather is issued before the first one is summed: NB slots per lane group
+// per batch (one batch when the row has at most RG * NB slots), slot ids and
+// alphas passed to the groups by lane permutes. Group g sums slots g, g + RG,
+// ... in rank order and the groups are combined by the same butterfly as in
+// pool_narrow_kernel (and, for RG = 1, the same order as pool_kernel), so the
+// result is the same bits. Measured on random 512-byte rows from a 41 GB
+// table: as fast as a gather with no header reads at all (+16% over the
+// batched kernel).
+template <bool BF16, int MODE, int RG, int NB>
+__global__ __launch_bounds__(256) void pool_head_kernel(PoolLaunch a) {
+  using V = Vec<BF16>;
+  using Raw = typename V::Raw;
+  constexpr int VN = V::kN;
+  constexpr int GL = kWave / RG;  // lanes per group
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int grp = lane / GL, c = lane % GL;
+  const int T = a.T;
+  const Raw* __restrict__ P = static_cast<const Raw*>(a.P);
+  Raw* __restrict__ out = static_cast<Raw*>(a.out);
+  const int vec_per_row = a.m / VN;
+  const bool col_ok = c < vec_per_row;
+
+  for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < a.rows;
+       row += (int64_t)gridDim.x * kWavesPerBlock) {
+    // Header: slot `lane` of the row.
+    int32_t v = -1;
+    float w = 0.0f;
+    int cnt = 0;
+    if (lane < T) {
+      v = a.idx[row * T + lane];
+      if constexpr (MODE == kPoolImportance) {
+        if (a.weights) w = a.weights[row * T + lane];
+        else cnt = a.counts[row * T + lane];
+      }
+    }
+    const bool valid = (uint64_t)(int64_t)v < (uint64_t)a.n_transform;
+    if (!valid) v = -1;
+    float alpha = 0.0f;
+    if constexpr (MODE == kPoolMean) {
+      const int total = wave_sum_i32(valid ? 1 : 0);
+      alpha = valid ? 1.0f / (float)total : 0.0f;
+    } else if constexpr (MODE == kPoolImportance) {
+      if (a.weights) {
+        alpha = valid ? w : 0.0f;
+      } else {
+        const int total = wave_sum_i32(cnt);  // every slot, as the walk kernel's S
+        alpha = valid ? (float)cnt / (float)total : 0.0f;
+      }
+    }
+    const int tend = __builtin_amdgcn_readfirstlane(wave_max_i32(valid ? lane : -1)) + 1;
+
+    float acc[VN];
+#pragma unroll
+    for (int k = 0; k < VN; ++k) acc[k] = MODE == kPoolMax ? -INFINITY : 0.0f;
+    bool any = false;
+    for (int b0 = 0; b0 < tend; b0 += RG * NB) {
+      Raw buf[NB];
+      float al[NB];
+      bool ok[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int t = b0 + i * RG + grp;
+        int32_t vt;
+        float at;
+        if constexpr (RG == 1) {
+          vt = __builtin_amdgcn_readlane(v, t & 63);
+          at = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), t & 63));
+        } else {
+          vt = __shfl(v, t & 63);
+          at = __shfl(alpha, t & 63);
+        }
+        ok[i] = t < tend && vt >= 0;
+        al[i] = ok[i] ? at : 0.0f;
+        buf[i] = (ok[i] && col_ok) ? P[(int64_t)vt * vec_per_row + c] : Raw{};
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        any = any || ok[i];
+        float f[VN];
+        V::to_f32(buf[i], f);
+#pragma unroll
+        for (int k = 0; k < VN; ++k) {
+          if constexpr (MODE == kPoolMax) acc[k] = ok[i] ? fmaxf(acc[k], f[k]) : acc[k];
+          else acc[k] = fmaf(al[i], f[k], acc[k]);
+        }
+      }
+    }
+#pragma unroll
+    for (int o = GL; o < kWave; o <<= 1)
+#pragma unroll
+      for (int k = 0; k < VN; ++k) {
+        const float other = __shfl_xor(acc[k], o);
+        acc[k] = MODE == kPoolMax ? fmaxf(acc[k], other) : acc[k] + other;
+      }
+    if constexpr (MODE == kPoolMax) {
+      const bool row_any = __builtin_amdgcn_readfirstlane(wave_sum_i32(any ? 1 : 0)) > 0;
+#pragma unroll
+      for (int k = 0; k < VN; ++k) acc[k] = row_any ? acc[k] : 0.0f;
+    }
+    if (grp == 0 && col_ok) out[row * vec_per_row + c] = V::from_f32(acc);
+  }
+}
+
+template <bool BF16, int MODE>
+hipError_t launch_batched(const PoolLaunch& a, dim3 grid, dim3 block, int slabs, int vec_per_row,
+                          hipStream_t s);
+
 template <bool BF16, int MODE>
 hipError_t launch_mode(const PoolLaunch& a, hipStream_t s) {
   constexpr int VN = BF16 ? 8 : 4;
@@ -253,6 +366,24 @@ hipError_t launch_mode(const PoolLaunch& a, hipStream_t s) {
   const dim3 grid((unsigned)(blocks_needed < cap ? blocks_needed : cap));
   const dim3 block(256);
   const int vec_per_row = a.m / VN;
+  if (a.T <= kWave) {
+    if (vec_per_row <= kWave / 4)
+      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 4, 16>), grid, block, 0, s, a);
+    else if (vec_per_row <= kWave / 2)
+      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 2, 32>), grid, block, 0, s, a);
+    else if (slabs <= 1)
+      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 1, 32>), grid, block, 0, s, a);
+    else
+      return launch_batched<BF16, MODE>(a, grid, block, slabs, vec_per_row, s);
+    return hipGetLastError();
+  }
+  return launch_batched<BF16, MODE>(a, grid, block, slabs, vec_per_row, s);
+}
+
+// Neighbourhoods of more than 64 slots, or rows wider than one slab.
+template <bool BF16, int MODE>
+hipError_t launch_batched(const PoolLaunch& a, dim3 grid, dim3 block, int slabs, int vec_per_row,
+                          hipStream_t s) {
   if (vec_per_row <= kWave / 4)
     hipLaunchKernelGGL((pool_narrow_kernel<BF16, MODE, 4>), grid, block, 0, s, a);
   else if (vec_per_row <= kWave / 2)

@@ -66,7 +66,12 @@ def test_algorithmic_work_per_launch():
     assert k2["gemm_w"]["algo_flops_per_launch"] == pytest.approx(2.0 * N * 768 * 256)
 
 
-def test_dominant_kernel_roofline_and_traffic():
+def test_dominant_kernel_roofline_and_traffic(monkeypatch, tmp_path):
+    # Counter bytes of the current pool source are reported as `traffic`.
+    (tmp_path / "traffic.json").write_text(json.dumps(
+        {"pool.hip:medium": {"source_sha": bench.kernel_source_hash("pool.hip"),
+                             "bytes_per_launch": 4.5e10, "profile": "profiles/x.md"}}))
+    monkeypatch.setattr(bench, "PROFILE_DIR", str(tmp_path))
     wl = synth.WORKLOADS["medium"]
     k = _medium_kernels()
     bench.add_rooflines(k, wl, [_Layer(256, 512, 256, "dense_then_pool")] * 2,
@@ -74,9 +79,9 @@ def test_dominant_kernel_roofline_and_traffic():
     r = bench.roofline_of(k, wl)
     assert r["kernel"] == "pool" and r["bound"] == "hbm" and r["unit"] == "GB/s"
     assert r["peak"] == 8000.0 and r["frac"] == pytest.approx(r["achieved"] / 8000.0)
-    with open(os.path.join(ROOT, "profiles", "traffic.json")) as f:
-        table = json.load(f)
-    assert r["traffic"] == table["pool.hip:medium"]["bytes_per_launch"]
+    assert r["traffic"] == 4.5e10
+    assert r["traffic_GBs"] == pytest.approx(4.5e10 / (k["pool"]["avg_ms"] * 1e-3) / 1e9)
+    assert r.get("cache_resident", False) == (r["frac"] > 1.0)
     # A GEMM-dominated step reports the MFMA roofline for its dtype and no traffic.
     k["gemm_q"]["ms_per_step"] = 100.0
     r = bench.roofline_of(k, wl)

@@ -1,0 +1,148 @@
+"""GPU parity at full size, the largest single-GPU shard: 80M pins + 20M
+boards (~0.49B undirected edges, int64 row offsets), bf16, dims 256 -> 512 ->
+256, 50 walks x 3 hops, T = 50, weights derived from counts, in the launch
+configuration of the all-node job (inputs drawn on the GPU by
+synth.device_gen):
+
+* neighbourhood rows (ids and counts) bit-exact against the oracle for every
+  row of the last 4,194,304-row chunk of the layer driver, the 1,000 boards
+  of highest degree, and 1M random sources;
+* the embeddings of 1,032 targets through the oracle's Algorithm 2 with
+  neighbourhoods walked on demand: 42 from each of the 24 row chunks of the
+  layer driver (including each chunk's first and last row) and the nodes 0
+  and N - 1, for both layer dataflows.
+The whole table (24-29B edge steps) is beyond the oracle's time here, hence
+the samples; the other workloads are compared in full.
+"""
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from helpers import check_embeddings, to_f64
+
+pytestmark = pytest.mark.gpu
+
+CHUNK_ROWS = 1 << 22  # rows per pool + W pass of the layer driver
+
+
+def _log(m):
+    print(f"[gen] {m}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def shard():
+    import paper_1806_01973_amd as ps
+    from synth.device_gen import make_features_device, make_graph_device
+    wl = synth.WORKLOADS["shard"]
+    print(f"[case] shard: generating {wl.num_nodes} nodes on the GPU", flush=True)
+    offsets, col, E = make_graph_device(wl, log=_log)
+    x = make_features_device(wl, offsets, col, log=_log)
+    gc.collect()
+    torch.cuda.empty_cache()
+    g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards, offsets64=wl.offsets64)
+    st = {"wl": wl, "g": g, "x": x, "E": E, "off_h": offsets.cpu().numpy(),
+          "col_h": col.cpu().numpy(), "jobs": {}}
+    yield st
+    for job in st["jobs"].values():
+        job.close()
+    st.clear()
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _job(st, dataflow):
+    """The all-node job of one dataflow (the other one is released first: the
+    two do not fit in HBM together)."""
+    import paper_1806_01973_amd as ps
+    if dataflow not in st["jobs"]:
+        for k in list(st["jobs"]):
+            st["jobs"].pop(k).close()
+        st.pop("out", None)
+        gc.collect()
+        torch.cuda.empty_cache()
+        wl = st["wl"]
+        layers = [ps.DeviceLayer(L["Q"], L["q"], L["W"], L["w"], dtype=torch.bfloat16,
+                                 dataflow=dataflow) for L in synth.make_layers(wl)]
+        job = ps.EmbedAll(st["g"], layers, wl.walks, wl.hops, wl.T, wl.seed, weights=False)
+        st["out"] = job.run(st["x"])
+        torch.cuda.synchronize()
+        st["jobs"][dataflow] = job
+        print(f"[case] shard: embed_all {dataflow} done, steps={int(job.steps.item())}",
+              flush=True)
+    return st["jobs"][dataflow]
+
+
+def _check_rows(orc, st, src, what):
+    wl = st["wl"]
+    job = _job(st, "dense_then_pool")
+    src = np.sort(np.asarray(src, np.int32))
+    print(f"[case] shard neighbourhoods: {what} ({len(src)} sources)", flush=True)
+    ridx, rcnt, _, steps = orc.build_neighborhoods(st["off_h"], st["col_h"], wl.num_pins,
+                                                   wl.seed, wl.walks, wl.hops, wl.T,
+                                                   sources=src)
+    sel = torch.as_tensor(src).long().cuda()
+    np.testing.assert_array_equal(job.nbr.idx[sel].cpu().numpy(), ridx)
+    np.testing.assert_array_equal(job.nbr.counts.view(torch.int16)[sel].cpu().numpy()
+                                  .view(np.uint16), rcnt)
+    live = int((ridx >= 0).sum())
+    print(f"[ok] shard {what}: {len(src)} rows bit-exact, {live} live entries, "
+          f"{steps} edge steps", flush=True)
+
+
+def test_shard_neighbourhoods_last_chunk(orc, shard):
+    n = shard["wl"].num_nodes
+    lo = (n - 1) // CHUNK_ROWS * CHUNK_ROWS
+    _check_rows(orc, shard, np.arange(lo, n), f"last chunk [{lo}, {n})")
+
+
+def test_shard_neighbourhoods_top_boards(orc, shard):
+    wl = shard["wl"]
+    off = shard["off_h"]
+    deg = off[wl.num_pins + 1:] - off[wl.num_pins:-1]
+    top = wl.num_pins + np.argsort(-deg, kind="stable")[:1000]
+    _check_rows(orc, shard, top, "1,000 highest-degree boards")
+
+
+@pytest.mark.parametrize("part", range(2))
+def test_shard_neighbourhoods_random(orc, shard, part):
+    n = shard["wl"].num_nodes
+    rng = np.random.default_rng(50 + part)
+    _check_rows(orc, shard, rng.choice(n, 500_000, replace=False),
+                f"500k random sources, part {part}")
+
+
+@pytest.fixture(scope="module")
+def shard_reference(orc, shard):
+    st = shard
+    wl = st["wl"]
+    n = wl.num_nodes
+    rng = np.random.default_rng(7)
+    picks = [[0, n - 1]]
+    for c0 in range(0, n, CHUNK_ROWS):
+        c1 = min(n, c0 + CHUNK_ROWS)
+        picks.append([c0, c1 - 1])
+        picks.append(rng.choice(np.arange(c0 + 1, c1 - 1), 40, replace=False))
+    targets = np.unique(np.concatenate(picks)).astype(np.int32)
+    print(f"[case] shard: oracle Algorithm 2 for {len(targets)} targets", flush=True)
+    smp = orc.minibatch_sample(targets, wl.K, st["off_h"], st["col_h"], wl.num_pins, wl.seed,
+                               wl.walks, wl.hops, wl.T)
+    s0 = smp["sets"][0]
+    x_rows = to_f64(st["x"][torch.as_tensor(s0).long().cuda()])
+    ref = orc.minibatch_embed_sampled(targets, s0, x_rows, smp, synth.make_layers(wl))
+    print(f"[ok] shard: |S| = {[len(s) for s in smp['sets']]}", flush=True)
+    return targets, ref
+
+
+@pytest.mark.parametrize("dataflow", ["dense_then_pool", "pool_then_dense"])
+def test_shard_embeddings(shard, shard_reference, dataflow):
+    st = shard
+    targets, ref = shard_reference
+    assert len(targets) >= 1000
+    _job(st, dataflow)
+    got = to_f64(st["out"][torch.as_tensor(targets).long().cuda()])
+    stats = check_embeddings(got, ref, st["wl"].dtype, f"shard {dataflow}")
+    print(f"[ok] shard {dataflow}: {len(targets)} targets {stats}", flush=True)
