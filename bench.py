@@ -200,6 +200,16 @@ def kernel_table(prof, steps):
     return kernels
 
 
+def chained_layer(L) -> bool:
+    """Layers whose Q transform and neighbour half of W run as one chained
+    kernel in the library (dense then pool, bf16, d_in = d_out = 256, m a
+    multiple of 32 up to 2048); their work is timed as gemm_qr."""
+    import torch
+    return (L.dataflow == "dense_then_pool" and getattr(L, "dtype", None) == torch.bfloat16
+            and L.d_in == 256
+            and L.d_out == 256 and L.m % 32 == 0 and 0 < L.m <= 2048)
+
+
 def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_stored,
                   walk_steps, steps):
     """Algorithmic work per launch and achieved rates. A step's work of a kernel
@@ -221,9 +231,13 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
             "pool", sum(live_entries * w * esz + idx_bytes + N * w * esz for w in width))
         k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
         k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
-    for name, fl in (("gemm_q", sum(2.0 * n_transform * L.d_in * L.m for L in layers)),
+    chained = [chained_layer(L) for L in layers]
+    for name, fl in (("gemm_q", sum(2.0 * n_transform * L.d_in * L.m
+                                    for L, ch in zip(layers, chained) if not ch)),
                      ("gemm_r", sum(2.0 * n_transform * L.m * L.d_out
-                                    for L, sp in zip(layers, split) if sp)),
+                                    for L, sp, ch in zip(layers, split, chained) if sp and not ch)),
+                     ("gemm_qr", sum(2.0 * n_transform * (L.d_in * L.m + L.m * L.d_out)
+                                     for L, ch in zip(layers, chained) if ch)),
                      ("gemm_w", sum(2.0 * N * (L.d_in + (0 if sp else L.m)) * L.d_out
                                     for L, sp in zip(layers, split)))):
         if name in kernels:
@@ -258,7 +272,7 @@ def walk_rates(k, edge_steps_per_launch, offsets64):
 def roofline_of(kernels, wl):
     dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     kd = kernels[dominant]
-    if dominant in ("gemm_q", "gemm_r", "gemm_w"):
+    if dominant in ("gemm_q", "gemm_r", "gemm_w", "gemm_qr"):
         return {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
                 "peak": MFMA_PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s", "frac": kd["frac_mfma"],
                 "traffic": None}
@@ -349,7 +363,7 @@ def bench_embed_all(args, wl, inp):
                   walk_steps, args.steps)
     value = N * args.steps / elapsed
     layer_ms = sum(v["ms_per_step"] for k, v in kernels.items()
-                   if k in ("gemm_q", "gemm_r", "pool", "gemm_w"))
+                   if k in ("gemm_q", "gemm_r", "gemm_qr", "pool", "gemm_w"))
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
              # N over the layer kernels' time alone (walks excluded), hipEvents;
              # only in the in-order schedule (overlapped launches share the chip).

@@ -440,7 +440,9 @@ enum {
   PINSAGE_KERNEL_MLP = 7,    /* output dense layers */
   PINSAGE_KERNEL_HARD_NEG = 8,
   PINSAGE_KERNEL_GRAPH_NBR = 9, /* graph neighbourhoods (MapReduce variant) */
-  PINSAGE_KERNEL_COUNT = 10
+  PINSAGE_KERNEL_GEMM_QR = 10,  /* Q transform chained into the neighbour half of
+                                   W (DENSE_THEN_POOL, bf16, d_in = d_out = 256) */
+  PINSAGE_KERNEL_COUNT = 11
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

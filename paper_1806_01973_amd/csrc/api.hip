@@ -194,10 +194,20 @@ int check_nbr(const pinsage_neighborhoods_t* n, int64_t rows, const char* what) 
 //   POOL_THEN_DENSE: P [n_transform][m] | pooled chunk [<= kChunkRows][m]
 //   DENSE_THEN_POOL: R [n_transform][d_out] | P chunk [<= kChunkRows][m] |
 //                    pooled chunk [<= kChunkRows][d_out]
+//   DENSE_THEN_POOL with the chained transform (chain_supported shapes): the
+//                    P chunk is replaced by two copies of the reordered W_n'
+//                    [d_out][m] (one per stream of the overlapped schedule);
+//                    P never exists.
 struct LayerWs {
   size_t table = 0, pchunk = 0, pooled = 0;
+  bool chained = false;
   size_t total() const { return table + pchunk + pooled; }
 };
+
+bool chained_layer(const pinsage_layer_t* L) {
+  return L->dataflow == PINSAGE_DENSE_THEN_POOL &&
+         chain_supported(L->d_in, L->m, L->d_out, L->dtype == PINSAGE_BF16);
+}
 
 LayerWs layer_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
   const size_t es = elem_size(L->dtype);
@@ -206,7 +216,9 @@ LayerWs layer_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
   LayerWs w;
   if (L->dataflow == PINSAGE_DENSE_THEN_POOL) {
     w.table = align_up((size_t)n_transform * L->d_out * es);
-    w.pchunk = align_up((size_t)tr_chunk * L->m * es);
+    w.chained = chained_layer(L);
+    w.pchunk = w.chained ? 2 * align_up((size_t)L->d_out * L->m * es)
+                         : align_up((size_t)tr_chunk * L->m * es);
     w.pooled = align_up((size_t)out_chunk * L->d_out * es);
   } else {
     w.table = align_up((size_t)n_transform * L->m * es);
@@ -268,6 +280,31 @@ int run_transform_rows(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
     e = launch_transform(L, h_in, n_in, transform_rows, r0, r1 - r0,
                          table + (size_t)r0 * L->m * es, s);
     if (e != hipSuccess) return hip_fail(e, "Q transform launch");
+    return PINSAGE_OK;
+  }
+  if (lw.chained) {
+    // R = ReLU(h Q^T + q) W_n^T in one kernel over the rows; this stream's
+    // copy of the reordered W_n' first.
+    unsigned char* wp = table + lw.table + (pbase > 0 ? lw.pchunk / 2 : 0);
+    e = launch_permute_wn(L->W, (int64_t)L->d_in + L->m, L->d_in, L->m, L->d_out, wp, s);
+    if (e != hipSuccess) return hip_fail(e, "W_n reorder launch");
+    ChainLaunch c{};
+    c.H = h_in;
+    c.rowmap = transform_rows ? transform_rows + r0 : nullptr;
+    c.row0 = r0;
+    c.rows_h = n_in;
+    c.ldh = L->d_in;
+    c.Q = L->Q;
+    c.q = L->q;
+    c.Wp = wp;
+    c.d_in = L->d_in;
+    c.m = L->m;
+    c.d_out = L->d_out;
+    c.R = table + (size_t)r0 * L->d_out * es;
+    c.ldr = L->d_out;
+    c.rows = r1 - r0;
+    e = launch_chain(c, s);
+    if (e != hipSuccess) return hip_fail(e, "chained transform launch");
     return PINSAGE_OK;
   }
   // Per chunk of pins: P = ReLU(h Q^T + q), then R = P W_n^T with W_n the

@@ -9,7 +9,8 @@ namespace pinsage {
 
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
-                   kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKGraphNbr = 9, kKCount = 10 };
+                   kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKGraphNbr = 9, kKGemmQR = 10,
+                   kKCount = 11 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -140,6 +141,31 @@ struct GemmLaunch {
   int64_t row_base = 0;
 };
 hipError_t launch_gemm(const GemmLaunch& a, hipStream_t s);
+
+// R[r] = ReLU(H[t(r)] Q^T + q) W_n^T for r in [0, rows), t(r) = rowmap[r] or
+// row0 + r (entries outside [0, rows_h) read as zero rows), bf16, with W_n'
+// the neighbour half of W in the column order of launch_permute_wn. P stays
+// in registers. Supported shapes: chain_supported.
+struct ChainLaunch {
+  const void* H;
+  const int32_t* rowmap;  // nullable
+  int64_t row0;
+  int64_t rows_h;
+  int64_t ldh;
+  const void* Q;   // [m][d_in]
+  const float* q;  // [m]
+  const void* Wp;  // [d_out][m], from launch_permute_wn
+  int d_in, m, d_out;
+  void* R;  // [rows][ldr]
+  int64_t ldr;
+  int64_t rows;
+};
+bool chain_supported(int d_in, int m, int d_out, bool bf16);
+// Wp[n][.] = W[n][d_in + .] (row stride ldw) with every 16-column group in
+// the order the chained kernel's second product reads it.
+hipError_t launch_permute_wn(const void* W, int64_t ldw, int d_in, int m, int d_out, void* Wp,
+                             hipStream_t s);
+hipError_t launch_chain(const ChainLaunch& a, hipStream_t s);
 
 // Max-margin loss (Eq. 1): per_pair[b] = mean over the shared negatives and
 // pair b's present hard negatives of max(0, zq.zn - zq.zpos + margin),

@@ -18,8 +18,9 @@ import synth  # noqa: E402
 
 
 class _Layer:
-    def __init__(self, d_in, m, d_out, dataflow):
+    def __init__(self, d_in, m, d_out, dataflow, dtype=None):
         self.d_in, self.m, self.d_out, self.dataflow = d_in, m, d_out, dataflow
+        self.dtype = dtype
 
 
 def _medium_kernels():
@@ -114,3 +115,22 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_chained_transform_accounting():
+    # bf16 dense-then-pool layers of 256 -> 512 -> 256 run the Q transform and
+    # the neighbour half of W as one kernel: its flops are both products'.
+    import torch
+    wl = synth.WORKLOADS["shard"]
+    N, P = wl.num_nodes, wl.num_pins
+    layers = [_Layer(256, 512, 256, "dense_then_pool", torch.bfloat16)] * 2
+    k = {"gemm_qr": {"launches": 2, "avg_ms": 40.0, "ms_per_step": 80.0},
+         "gemm_w": {"launches": 48, "avg_ms": 1.9, "ms_per_step": 91.2}}
+    bench.add_rooflines(k, wl, layers, N, P, 0, False, 0, 1)
+    assert k["gemm_qr"]["algo_flops_per_launch"] == pytest.approx(
+        2.0 * P * (256 * 512 + 512 * 256))
+    assert k["gemm_qr"]["frac_mfma"] == pytest.approx(
+        k["gemm_qr"]["algo_flops_per_launch"] / 40e-3 / 1e12 / 2500.0)
+    assert "gemm_q" not in k and "gemm_r" not in k
+    assert not bench.chained_layer(_Layer(256, 512, 256, "pool_then_dense", torch.bfloat16))
+    assert not bench.chained_layer(_Layer(1024, 2048, 512, "dense_then_pool", torch.bfloat16))
