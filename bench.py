@@ -27,8 +27,11 @@ Other workloads (measurement of the other rows; not the headline):
                                     2 layers over all nodes, featureless boards
   --workload hardneg                one step = hard negative items (Sec. 3.3)
                                     for 2,048 query pins of the 1.2M-node
-                                    graph: 4096 walks x 4 landings each, ranks
-                                    2000-5000, --hard-neg draws per query
+                                    graph: 4096 walks x 4 landings each
+                                    (--hn-walks, --hn-hops; budgets above
+                                    16,384 landings count visits in a global
+                                    table), ranks 2000-5000, --hard-neg draws
+                                    per query
 
 Prints one JSON line: throughput of the whole step, walk steps/s, per-kernel
 times from hipEvents recorded around every launch in the timed region, the
@@ -596,7 +599,7 @@ def bench_hard_negatives(args, wl, inp):
     steps_dev = []
 
     def run(i):
-        _, st = ps.hard_negatives(inp["g"], qs[i], k, wl.seed + 1, HN_WALKS, HN_HOPS, HN_LO,
+        _, st = ps.hard_negatives(inp["g"], qs[i], k, wl.seed + 1, args.hn_walks, args.hn_hops, HN_LO,
                                   HN_HI, out=out, count_steps=True)
         steps_dev.append(st)
 
@@ -607,23 +610,24 @@ def bench_hard_negatives(args, wl, inp):
     walk_rates(kd, edge_steps, wl.offsets64)
     value = HN_QUERIES * args.steps / elapsed
     extra = {"walk_steps_per_s": edge_steps * args.steps / elapsed,
-             "config_extra": {"queries": HN_QUERIES, "walks": HN_WALKS, "hops": HN_HOPS,
+             "config_extra": {"queries": HN_QUERIES, "walks": args.hn_walks, "hops": args.hn_hops,
                               "rank_window": [HN_LO, HN_HI], "per_query": k,
                               "empty_rows_last": int((out[:, 0] < 0).sum().item())}}
     metric = "hard negative items (Sec. 3.3, PPR rank window), queries/sec, 1 MI355X"
     return value, "queries/s", metric, elapsed, kernels, extra
 
 
-def cpu_baseline_hard_negatives(inp, wl, threads, k):
-    """The oracle's hard negatives for a sample of 16,384 query pins (eight steps'
-    worth of queries)."""
+def cpu_baseline_hard_negatives(inp, wl, threads, k, walks=HN_WALKS, hops=HN_HOPS):
+    """The oracle's hard negatives for a sample of query pins (16,384, i.e. eight
+    steps' worth, at the default budget; proportionally fewer at larger ones)."""
     import numpy as np
     import oracle
     rng = np.random.default_rng(10_000)
-    q = rng.integers(0, wl.num_pins, 16_384).astype(np.int32)
+    nq = max(256, 16_384 * HN_WALKS * HN_HOPS // (walks * hops))
+    q = rng.integers(0, wl.num_pins, nq).astype(np.int32)
     t0 = time.perf_counter()
     oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins, wl.seed + 1,
-                          HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k, nthreads=threads)
+                          walks, hops, q, HN_LO, HN_HI, k, nthreads=threads)
     secs = time.perf_counter() - t0
     return {"value": len(q) / secs, "unit": "queries/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(q)} query pins, {secs:.1f}s"}
@@ -721,6 +725,11 @@ def main() -> int:
                     help="hard negatives per query: draws for --workload hardneg (default 4); "
                          "with --workload minibatch, mined each step and added to every "
                          "pair's negatives (default 0)")
+    ap.add_argument("--hn-walks", type=int, default=HN_WALKS,
+                    help="--workload hardneg: walks per query (walks x hops above 16,384 "
+                         "count visits in a global table)")
+    ap.add_argument("--hn-hops", type=int, default=HN_HOPS,
+                    help="--workload hardneg: pin landings per walk")
     ap.add_argument("--overlap", type=int, default=4, metavar="EIGHTHS",
                     help="all-node job: first layer's transform beside the walks on EIGHTHS/8 "
                          "of the CUs (0: walks, then transform, in order)")
@@ -787,8 +796,8 @@ def main() -> int:
         "dtype": "u32" if hardneg else wl.dtype,
         "data": "synthetic",
         "config": {"workload": (f"hard negatives: {wl.num_pins} pins + {wl.num_boards} boards, "
-                                f"{inp['num_edges']} edges, {HN_QUERIES} query pins, {HN_WALKS} "
-                                f"walks x {HN_HOPS} landings each, ranks {HN_LO + 1}-{HN_HI}, "
+                                f"{inp['num_edges']} edges, {HN_QUERIES} query pins, {args.hn_walks} "
+                                f"walks x {args.hn_hops} landings each, ranks {HN_LO + 1}-{HN_HI}, "
                                 f"{args.hard_neg} per query") if hardneg else
                    (f"{wl.name}: {wl.num_pins} pins + {wl.num_boards} boards, "
                                f"{inp['num_edges']} edges, {wl.walks} walks x {wl.hops} hops, "
@@ -819,7 +828,8 @@ def main() -> int:
         threads = oracle.default_threads()
         log(f"timing the oracle on a sample ({threads} threads)")
         if hardneg:
-            result["cpu_baseline"] = cpu_baseline_hard_negatives(inp, wl, threads, args.hard_neg)
+            result["cpu_baseline"] = cpu_baseline_hard_negatives(inp, wl, threads, args.hard_neg,
+                                                                 args.hn_walks, args.hn_hops)
         elif bipartite:
             result["cpu_baseline"] = cpu_baseline_bipartite(inp, wl, threads)
         elif wl.name == "minibatch":

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 8
+#define PINSAGE_ABI_VERSION 9
 
 enum {
   PINSAGE_OK = 0,
@@ -195,8 +195,8 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph,
  * returns the pin at rank rank_lo + floor(r * n / 2^32) (independent draws,
  * with replacement). The paper's window, ranks 2000 to 5000 counted from 1,
  * is rank_lo = 1999, rank_hi = 5000.
- * Limits: 1 <= walks * hops <= 16384, 0 <= rank_lo < rank_hi,
- * 0 <= num_per_query. */
+ * Limits: 1 <= walks * hops <= 2^22, 0 <= rank_lo < rank_hi, 0 <= num_per_query;
+ * with walks * hops > 16384 also rank_hi <= 8192. */
 typedef struct {
   uint64_t seed;
   int32_t walks;
@@ -206,15 +206,26 @@ typedef struct {
   int32_t num_per_query;
 } pinsage_hard_negative_params_t;
 
+/* Workspace bytes pinsage_hard_negatives needs for these parameters and
+ * query count: 0 for walks * hops <= 16384 (the visits of a query are counted
+ * on chip); above that, a global visit table per resident workgroup (at most
+ * 256 workgroups, each table 2^ceil(log2(2 walks hops)) entries of 8 bytes).
+ * Errors as for pinsage_hard_negatives' parameters. */
+int pinsage_hard_negatives_workspace_size(const pinsage_hard_negative_params_t* params,
+                                          int64_t num_queries, size_t* bytes);
+
 /* out: device int32 [num_queries][num_per_query], pin ids, or -1 for every
  * draw of a query whose window is empty (n <= 0) or whose id lies outside
  * [0, num_nodes). queries: device int32 [num_queries]. If total_steps is
  * non-NULL (device uint64), it receives the number of edge steps all walks
- * took. Out-of-range CSR entries end the walk that meets them. */
+ * took. workspace: device, >= pinsage_hard_negatives_workspace_size bytes,
+ * 256-aligned (may be NULL when that size is 0). Out-of-range CSR entries end
+ * the walk that meets them. */
 int pinsage_hard_negatives(const pinsage_graph_t* graph,
                            const pinsage_hard_negative_params_t* params,
                            const int32_t* queries, int64_t num_queries, int32_t* out,
-                           unsigned long long* total_steps, void* stream);
+                           unsigned long long* total_steps, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* Graph neighbourhoods of the MapReduce inference (Sec. 3.4): a board's
  * embedding pools the pins it holds and a pin's the boards it occurs on,

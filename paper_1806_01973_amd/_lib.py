@@ -27,7 +27,8 @@ KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "g
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
-    "pinsage_build_neighborhoods", "pinsage_hard_negatives", "pinsage_build_graph_neighborhoods",
+    "pinsage_build_neighborhoods", "pinsage_hard_negatives",
+    "pinsage_hard_negatives_workspace_size", "pinsage_build_graph_neighborhoods",
     "pinsage_embed_all_bipartite_workspace_size", "pinsage_embed_all_bipartite",
     "pinsage_convolve_workspace_size", "pinsage_convolve_layer", "pinsage_convolve_layer_noalloc",
     "pinsage_embed_all_workspace_size", "pinsage_embed_all",
@@ -116,7 +117,9 @@ def lib():
                                               i32, P, ctypes.POINTER(Neighborhoods), P, P,
                                               ctypes.c_size_t, P]
     L.pinsage_hard_negatives.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(HardNegativeParams),
-                                         P, i64, P, P, P]
+                                         P, i64, P, P, P, ctypes.c_size_t, P]
+    L.pinsage_hard_negatives_workspace_size.argtypes = [ctypes.POINTER(HardNegativeParams), i64,
+                                                        ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_convolve_workspace_size.argtypes = [ctypes.POINTER(Layer), i64, i64,
                                                   ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_convolve_layer.argtypes = [ctypes.POINTER(Layer), P, i64, i64, P,

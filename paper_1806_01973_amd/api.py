@@ -205,8 +205,13 @@ def hard_negatives(graph: DeviceGraph, queries: torch.Tensor, k: int, seed: int,
     steps = torch.empty(1, dtype=torch.int64, device=queries.device) if count_steps else None
     g = graph.struct()
     hp = L.HardNegativeParams(seed, walks, hops, rank_lo, rank_hi, k)
+    need = ctypes.c_size_t(0)
+    L.check(lib.pinsage_hard_negatives_workspace_size(ctypes.byref(hp), n, ctypes.byref(need)),
+            "pinsage_hard_negatives_workspace_size")
+    ws = (torch.empty(int(need.value), dtype=torch.uint8, device=queries.device)
+          if need.value else None)
     st = lib.pinsage_hard_negatives(ctypes.byref(g), ctypes.byref(hp), _ptr(queries), n, _ptr(out),
-                                    _ptr(steps), _stream(stream))
+                                    _ptr(steps), _ptr(ws), int(need.value), _stream(stream))
     L.check(st, "pinsage_hard_negatives")
     return out, steps
 

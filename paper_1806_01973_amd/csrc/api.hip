@@ -596,27 +596,53 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk
   return PINSAGE_OK;
 }
 
-int pinsage_hard_negatives(const pinsage_graph_t* graph,
-                           const pinsage_hard_negative_params_t* params, const int32_t* queries,
-                           int64_t num_queries, int32_t* out, unsigned long long* total_steps,
-                           void* stream) {
-  g_last_error.clear();
-  int st = check_graph(graph);
-  if (st) return st;
+int check_hard_negative_params(const pinsage_hard_negative_params_t* params, int64_t num_queries) {
   if (!params) return fail(PINSAGE_EINVAL, "hard negative params are NULL");
   const pinsage_hard_negative_params_t& h = *params;
   if (h.walks < 1 || h.hops < 1)
     return fail(PINSAGE_EINVAL, "walks (%d) and hops (%d) must be >= 1", h.walks, h.hops);
-  if ((int64_t)h.walks * h.hops > 16384)
-    return fail(PINSAGE_EUNSUPPORTED, "walks * hops = %lld exceeds 16384",
-                (long long)h.walks * h.hops);
+  const int64_t landings = (int64_t)h.walks * h.hops;
+  if (landings > kMaxLandings)
+    return fail(PINSAGE_EUNSUPPORTED, "walks * hops = %lld exceeds %lld", (long long)landings,
+                (long long)kMaxLandings);
   if (h.rank_lo < 0 || h.rank_hi <= h.rank_lo)
     return fail(PINSAGE_EINVAL, "rank window [%d, %d) is empty or negative", h.rank_lo,
                 h.rank_hi);
+  if (landings > kMaxOnChipLandings && h.rank_hi > kMaxGlobalRank)
+    return fail(PINSAGE_EUNSUPPORTED,
+                "rank_hi %d exceeds %d for walks * hops above %lld", h.rank_hi, kMaxGlobalRank,
+                (long long)kMaxOnChipLandings);
   if (h.num_per_query < 0) return fail(PINSAGE_EINVAL, "negative num_per_query");
   if (num_queries < 0) return fail(PINSAGE_EINVAL, "negative num_queries");
+  return PINSAGE_OK;
+}
+
+int pinsage_hard_negatives_workspace_size(const pinsage_hard_negative_params_t* params,
+                                          int64_t num_queries, size_t* bytes) {
+  g_last_error.clear();
+  int st = check_hard_negative_params(params, num_queries);
+  if (st) return st;
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  *bytes = hard_negative_workspace((int64_t)params->walks * params->hops, num_queries);
+  return PINSAGE_OK;
+}
+
+int pinsage_hard_negatives(const pinsage_graph_t* graph,
+                           const pinsage_hard_negative_params_t* params, const int32_t* queries,
+                           int64_t num_queries, int32_t* out, unsigned long long* total_steps,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int st = check_graph(graph);
+  if (st) return st;
+  if ((st = check_hard_negative_params(params, num_queries))) return st;
+  const pinsage_hard_negative_params_t& h = *params;
   if (num_queries > 0 && !queries) return fail(PINSAGE_EINVAL, "queries is NULL");
   if (num_queries > 0 && h.num_per_query > 0 && !out) return fail(PINSAGE_EINVAL, "out is NULL");
+  const size_t need = hard_negative_workspace((int64_t)h.walks * h.hops, num_queries);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(PINSAGE_EWORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(PINSAGE_EINVAL, "workspace is not 256-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (total_steps) {
     hipError_t e = launch_zero_u64(total_steps, 1, s);
@@ -640,7 +666,7 @@ int pinsage_hard_negatives(const pinsage_graph_t* graph,
   a.k = h.num_per_query;
   a.out = out;
   a.total_steps = total_steps;
-  hipError_t e = launch_hard_negatives(a, s);
+  hipError_t e = launch_hard_negatives(a, workspace, s);
   if (e != hipSuccess) return hip_fail(e, "hard negative launch");
   return PINSAGE_OK;
 }

@@ -322,11 +322,20 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
   // columns past N have zero weights and zero bias, so they stay zero.
   // Row bands are finished one at a time to keep few accumulators live.
   auto c0 = [&](int j, int g) __attribute__((always_inline)) { return b_base_row + j * 32 + 8 * g + 4 * half; };
+  // bf16 tiles that fit in the (now free) stage ring are staged there, rows
+  // padded by 16 bytes, and leave as whole rows (16 bytes per lane) rather
+  // than as 8-byte pieces of 32 rows per store instruction. (Loading the
+  // addend tile the same way, in front of the epilogue, measured slower: its
+  // latency is then exposed.)
+  constexpr int TROW = BN * 2 + 16;
+  constexpr bool kStaged = C::kBf16 && BM * TROW <= STAGES * C::STAGE_BYTES;
+  constexpr int PER_ROW = BN / 8;  // 16-byte pieces per tile row
   // + bias (+ addend), then ReLU unless disabled; the L2 epilogue always
   // follows a ReLU.
   const bool relu = a.relu || C::L2;
   auto bias_relu = [&](int i) __attribute__((always_inline)) {
-    const int64_t r = m0 + a_base_row + i * 32 + row_in_blk;
+    const int rt = a_base_row + i * 32 + row_in_blk;
+    const int64_t r = m0 + rt;
     const bool add = a.addend != nullptr && r < a.M;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
@@ -357,24 +366,46 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
       }
   };
   auto store_band = [&](int i, float scale) __attribute__((always_inline)) {
-    const int64_t r = m0 + a_base_row + i * 32 + row_in_blk;
-    if (r >= a.M) return;
+    const int rt = a_base_row + i * 32 + row_in_blk;  // row in the tile
+    const int64_t r = m0 + rt;
+    if (!kStaged && r >= a.M) return;
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int c = n0 + c0(j, g);
-        if (c >= a.N) continue;
-        const int64_t o = r * a.N + c;
         const float v0 = acc[i][j][4 * g] * scale, v1 = acc[i][j][4 * g + 1] * scale;
         const float v2 = acc[i][j][4 * g + 2] * scale, v3 = acc[i][j][4 * g + 3] * scale;
-        if constexpr (C::kBf16) {
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + o) =
+        if constexpr (kStaged) {
+          *reinterpret_cast<uint2*>(smem + rt * TROW + c0(j, g) * 2) =
               make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
         } else {
-          *reinterpret_cast<float4*>(static_cast<float*>(a.C) + o) = make_float4(v0, v1, v2, v3);
+          if (c >= a.N) continue;
+          const int64_t o = r * a.N + c;
+          if constexpr (C::kBf16) {
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + o) =
+                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          } else {
+            *reinterpret_cast<float4*>(static_cast<float*>(a.C) + o) =
+                make_float4(v0, v1, v2, v3);
+          }
         }
       }
+  };
+  // Staged tile -> global, BN / 8 lanes per row.
+  auto flush_tile = [&]() __attribute__((always_inline)) {
+    if constexpr (kStaged) {
+      __syncthreads();
+#pragma unroll 4
+      for (int e = tid; e < BM * PER_ROW; e += THREADS) {
+        const int rt = e / PER_ROW, ck = e % PER_ROW;
+        const int64_t r = m0 + rt;
+        const int c = n0 + 8 * ck;
+        if (r < a.M && c < a.N)
+          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.C) + r * a.N + c) =
+              *reinterpret_cast<const uint4*>(smem + rt * TROW + 16 * ck);
+      }
+    }
   };
 
   if constexpr (!C::L2) {
@@ -383,6 +414,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
       bias_relu(i);
       store_band(i, 1.0f);
     }
+    flush_tile();
   } else {
     // Sum of squares of each row: over the lane's columns, then its partner
     // half-wave (lane ^ 32), then the WAVES_N waves of the row band in a
@@ -407,6 +439,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
       for (int w = 0; w < C::WAVES_N; ++w) ss += red[w * BM + r];
       store_band(i, ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f);
     }
+    flush_tile();
   }
 }
 

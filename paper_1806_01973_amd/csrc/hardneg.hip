@@ -349,6 +349,308 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
   }
 }
 
+// ---------------------------------------------------------------------------
+// Walk budgets above the LDS slots (walks * hops > 16384): the visits of a
+// query are counted in a global open-addressing table (capacity a power of
+// two >= 2 walks * hops, so it is at most half full; Fibonacci hashing,
+// linear probing, claimed by atomicCAS, counted by atomicAdd at device scope:
+// the final (pin, count) multiset does not depend on the order of the walks).
+// One 1024-thread workgroup per query (grid-stride; each workgroup reuses its
+// own table). Only the first rank_hi ranks matter, so the ranking is a
+// selection, not a full sort:
+//   1. count histogram (12-bit digits, two passes) -> the count c* of rank
+//      rank_hi - 1, the number n_above of pins counted more than c*;
+//   2. the pins counted more than c* (fewer than rank_hi) sorted by count
+//      descending, id ascending (64-bit keys, bitonic in LDS);
+//   3. the rank_hi - n_above smallest ids counted exactly c*: radix select on
+//      the id (11 + 10 + 10 bits), gathered and sorted ascending;
+//   4. the draws as in the on-chip kernel.
+// With at most rank_hi distinct pins, all of them take step 2.
+// ---------------------------------------------------------------------------
+constexpr int kGMaxRank = 8192;  // rank_hi limit of this path
+constexpr int kGBins = 4096;
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+
+__device__ __forceinline__ void table_add(uint32_t* keys, uint32_t* cnt, uint32_t mask,
+                                          int lg_cap, uint32_t v) {
+  uint32_t h = (v * 2654435761u) >> (32 - lg_cap);
+  while (true) {
+    const uint32_t k = atomicCAS(&keys[h], kNoKey, v);
+    if (k == kNoKey || k == v) {
+      atomicAdd(&cnt[h], 1u);
+      return;
+    }
+    h = (h + 1) & mask;
+  }
+}
+
+// Ascending bitonic sort of v[0, n), n a power of two <= 2 * 1024 * 4.
+template <typename T>
+__device__ __forceinline__ void lds_bitonic(T* v, int n, int tid) {
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int p = tid; p < n / 2; p += kThreads) {
+        const int i = 2 * stride * (p / stride) + (p % stride);
+        const int j = i + stride;
+        const bool up = (i & size) == 0;
+        const T x = v[i], y = v[j];
+        if ((x > y) == up) {
+          v[i] = y;
+          v[j] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__device__ __forceinline__ int pow2_at_least(int n) {
+  int p = 1;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+// Scans hist[0, kGBins) from the top: the bin holding the want-th largest
+// element (0-based) and the number of elements in the bins above it.
+__device__ __forceinline__ void top_bin(const uint32_t* hist, int64_t want, int* bin,
+                                        int64_t* above) {
+  int64_t cum = 0;
+  int b = kGBins - 1;
+  for (; b > 0; --b) {
+    if (cum + hist[b] > want) break;
+    cum += hist[b];
+  }
+  *bin = b;
+  *above = cum;
+}
+
+// From the bottom: the bin holding the want-th smallest (0-based).
+__device__ __forceinline__ void low_bin(const uint32_t* hist, int nbins, int64_t want, int* bin,
+                                        int64_t* below) {
+  int64_t cum = 0;
+  int b = 0;
+  for (; b < nbins - 1; ++b) {
+    if (cum + hist[b] > want) break;
+    cum += hist[b];
+  }
+  *bin = b;
+  *below = cum;
+}
+
+template <typename OffT>
+__global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegLaunch a,
+                                                                        uint32_t* table,
+                                                                        int lg_cap) {
+  __shared__ uint32_t hist[kGBins];
+  __shared__ uint64_t top[kGMaxRank];  // pins counted more than c*: (~count << 32) | id
+  __shared__ uint32_t cls[kGMaxRank];  // the smallest ids counted exactly c*
+  __shared__ int64_t sh_i64[4];
+  __shared__ int sh_i32[8];
+  const uint32_t cap = 1u << lg_cap, mask = cap - 1;
+  uint32_t* keys = table + (size_t)blockIdx.x * 2 * cap;
+  uint32_t* cnt = keys + cap;
+  const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
+  const int32_t* __restrict__ col = a.col;
+  const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
+  const uint32_t k1 = (uint32_t)(a.seed >> 32);
+  const int tid = threadIdx.x;
+  const int R = a.rank_hi;
+  uint32_t my_steps = 0;
+
+  for (int64_t qi = blockIdx.x; qi < a.num_queries; qi += gridDim.x) {
+    const int64_t u = (int64_t)a.queries[qi];
+    const bool live = u >= 0 && u < a.num_nodes;
+    for (uint32_t i = tid; i < cap; i += kThreads) {
+      keys[i] = kNoKey;
+      cnt[i] = 0u;
+    }
+    if (tid < 8) sh_i32[tid] = 0;
+    __syncthreads();
+
+    // ---- walks, visits counted in the table ------------------------------
+    if (live) {
+      for (int w0 = tid; w0 < a.walks; w0 += kWalkers * kThreads) {
+        Walker<OffT> W[kWalkers];
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) {
+          const int w = w0 + i * kThreads;
+          W[i].start(u, w, nullptr, w < a.walks);
+        }
+        bool any = true;
+        while (any) {
+          int64_t lo[kWalkers], hi[kWalkers];
+#pragma unroll
+          for (int i = 0; i < kWalkers; ++i) {
+            lo[i] = 0;
+            hi[i] = 0;
+            if (W[i].active) {
+              lo[i] = (int64_t)off[W[i].cur];
+              hi[i] = (int64_t)off[W[i].cur + 1];
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < kWalkers; ++i) W[i].pick(lo[i], hi[i], a.nnz, k0, k1);
+          int32_t nx[kWalkers];
+#pragma unroll
+          for (int i = 0; i < kWalkers; ++i) nx[i] = W[i].active ? col[W[i].next_at] : 0;
+          any = false;
+#pragma unroll
+          for (int i = 0; i < kWalkers; ++i) {
+            uint32_t v;
+            if (W[i].advance(nx[i], a.num_pins, a.num_nodes, a.hops, &v) && v != kEmpty)
+              table_add(keys, cnt, mask, lg_cap, v);
+            any = any || W[i].active;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) my_steps += (uint32_t)W[i].s;
+      }
+    }
+    __syncthreads();
+    // The table was updated by atomics in L2: drop this CU's cached copies.
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+    // ---- 1. count threshold ----------------------------------------------
+    for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+    __syncthreads();
+    {
+      int nd = 0;
+      for (uint32_t i = tid; i < cap; i += kThreads) {
+        if (keys[i] == kNoKey) continue;
+        ++nd;
+        const uint32_t c = cnt[i];
+        atomicAdd(&hist[(c >> 12) < kGBins ? (c >> 12) : kGBins - 1], 1u);
+      }
+      atomicAdd(&sh_i32[0], nd);
+    }
+    __syncthreads();
+    const int D = sh_i32[0];
+    uint32_t cstar = 0;  // pins counted more than cstar are ranked by step 2
+    int64_t n_above = D;
+    if (D > R) {
+      if (tid == 0) {
+        int b1;
+        int64_t above;
+        top_bin(hist, R - 1, &b1, &above);
+        sh_i32[1] = b1;
+        sh_i64[0] = above;
+      }
+      __syncthreads();
+      const uint32_t b1 = (uint32_t)sh_i32[1];
+      const int64_t above1 = sh_i64[0];
+      for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+      __syncthreads();
+      for (uint32_t i = tid; i < cap; i += kThreads) {
+        if (keys[i] == kNoKey) continue;
+        const uint32_t c = cnt[i];
+        if ((c >> 12) == b1) atomicAdd(&hist[c & (kGBins - 1)], 1u);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int b2;
+        int64_t above2;
+        top_bin(hist, R - 1 - above1, &b2, &above2);
+        sh_i32[2] = b2;
+        sh_i64[1] = above1 + above2;
+      }
+      __syncthreads();
+      cstar = (b1 << 12) | (uint32_t)sh_i32[2];
+      n_above = sh_i64[1];
+    }
+
+    // ---- 2. pins counted more than c*, by count desc, id asc ---------------
+    for (uint32_t i = tid; i < cap; i += kThreads) {
+      const uint32_t k = keys[i];
+      if (k == kNoKey) continue;
+      const uint32_t c = cnt[i];
+      if (c > cstar) {
+        const int slot = atomicAdd(&sh_i32[3], 1);
+        top[slot] = ((uint64_t)(~c) << 32) | k;
+      }
+    }
+    __syncthreads();
+    const int na = (int)n_above;
+    const int na2 = pow2_at_least(na > 0 ? na : 1);
+    for (int i = na + tid; i < na2; i += kThreads) top[i] = ~0ull;
+    __syncthreads();
+    if (na > 1) lds_bitonic<uint64_t>(top, na2, tid);
+
+    // ---- 3. the smallest ids counted exactly c* ---------------------------
+    const int need = D > R ? R - na : 0;
+    if (need > 0) {
+      // Radix select of the need-th smallest id (0-based need - 1) among the
+      // pins counted c*: digits of 11, 10 and 10 bits.
+      uint32_t prefix = 0;
+      int64_t want = need - 1;
+      constexpr int shifts[3] = {20, 10, 0};
+      constexpr int widths[3] = {11, 10, 10};
+#pragma unroll
+      for (int pass = 0; pass < 3; ++pass) {
+        const int sft = shifts[pass], nb = 1 << widths[pass];
+        const uint32_t hi_mask = pass == 0 ? 0u : (0xFFFFFFFFu << (sft + widths[pass]));
+        for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+        __syncthreads();
+        for (uint32_t i = tid; i < cap; i += kThreads) {
+          const uint32_t k = keys[i];
+          if (k == kNoKey || cnt[i] != cstar || (k & hi_mask) != prefix) continue;
+          atomicAdd(&hist[(k >> sft) & (nb - 1)], 1u);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          int d;
+          int64_t below;
+          low_bin(hist, nb, want, &d, &below);
+          sh_i32[4] = d;
+          sh_i64[2] = want - below;
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sh_i32[4] << sft;
+        want = sh_i64[2];
+        __syncthreads();
+      }
+      // prefix is the need-th smallest id of the class: gather ids <= prefix.
+      for (uint32_t i = tid; i < cap; i += kThreads) {
+        const uint32_t k = keys[i];
+        if (k == kNoKey || cnt[i] != cstar || k > prefix) continue;
+        cls[atomicAdd(&sh_i32[5], 1)] = k;
+      }
+      __syncthreads();
+      const int nc2 = pow2_at_least(need);
+      for (int i = need + tid; i < nc2; i += kThreads) cls[i] = kNoKey;
+      __syncthreads();
+      if (need > 1) lds_bitonic<uint32_t>(cls, nc2, tid);
+    }
+
+    // ---- 4. draws from the window -----------------------------------------
+    const int64_t topn = D < R ? (int64_t)D : (int64_t)R;
+    const int64_t n = topn - a.rank_lo;
+    int32_t* outq = a.out + qi * (int64_t)a.k;
+    for (int j = tid; j < a.k; j += kThreads) {
+      int32_t v = -1;
+      if (n > 0) {
+        const uint4 r = philox4x32_10(make_uint4((uint32_t)u, (uint32_t)j, 0u, 1u), k0, k1);
+        const int rank = a.rank_lo + (int)(((uint64_t)r.x * (uint64_t)n) >> 32);
+        v = rank < na ? (int32_t)(uint32_t)(top[rank] & 0xFFFFFFFFull) : (int32_t)cls[rank - na];
+      }
+      outq[j] = v;
+    }
+    __syncthreads();  // the table and LDS are reused by the next query
+  }
+
+  if (a.total_steps) {
+    const int wave = tid >> 6, lane = tid & (kWave - 1);
+    const int ws = wave_sum_i32((int)my_steps);
+    __shared__ int wave_tot[kWaves];
+    if (lane == 0) wave_tot[wave] = ws;
+    __syncthreads();
+    if (tid == 0) {
+      unsigned long long t = 0;
+      for (int w = 0; w < kWaves; ++w) t += (unsigned long long)(unsigned)wave_tot[w];
+      if (t) atomicAdd(a.total_steps, t);
+    }
+  }
+}
+
 template <typename OffT>
 hipError_t launch_for_offsets(const HardNegLaunch& a, hipStream_t s) {
   const int wh = a.walks * a.hops;
@@ -366,10 +668,36 @@ hipError_t launch_for_offsets(const HardNegLaunch& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_hard_negatives(const HardNegLaunch& a, hipStream_t s) {
+int hard_negative_table_lg(int64_t landings) {
+  int lg = 1;
+  while ((1ll << lg) < 2 * landings) ++lg;
+  return lg;
+}
+
+int64_t hard_negative_blocks(int64_t num_queries) {
+  return num_queries < kGMaxBlocks ? num_queries : kGMaxBlocks;
+}
+
+size_t hard_negative_workspace(int64_t landings, int64_t num_queries) {
+  if (landings <= kMaxOnChipLandings || num_queries <= 0) return 0;
+  return (size_t)hard_negative_blocks(num_queries) * 2 * ((size_t)1 << hard_negative_table_lg(landings)) *
+         sizeof(uint32_t);
+}
+
+hipError_t launch_hard_negatives(const HardNegLaunch& a, void* workspace, hipStream_t s) {
   if (a.num_queries <= 0) return hipSuccess;
   ProfileScope prof(kKHardNeg, s);
-  return a.offsets64 ? launch_for_offsets<int64_t>(a, s) : launch_for_offsets<int32_t>(a, s);
+  const int64_t landings = (int64_t)a.walks * a.hops;
+  if (landings <= kMaxOnChipLandings)
+    return a.offsets64 ? launch_for_offsets<int64_t>(a, s) : launch_for_offsets<int32_t>(a, s);
+  const int lg = hard_negative_table_lg(landings);
+  const dim3 grid((unsigned)hard_negative_blocks(a.num_queries)), block(kThreads);
+  uint32_t* table = static_cast<uint32_t*>(workspace);
+  if (a.offsets64)
+    hipLaunchKernelGGL(hard_negative_global_kernel<int64_t>, grid, block, 0, s, a, table, lg);
+  else
+    hipLaunchKernelGGL(hard_negative_global_kernel<int32_t>, grid, block, 0, s, a, table, lg);
+  return hipGetLastError();
 }
 
 }  // namespace pinsage

@@ -44,8 +44,7 @@ struct WalkLaunch {
 hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
 
 // Hard negative items (Sec. 3.3): out[i][j], j < k, drawn from ranks
-// [rank_lo, rank_hi) of the visit-count ranking of walks from queries[i];
-// walks * hops <= 16384.
+// [rank_lo, rank_hi) of the visit-count ranking of walks from queries[i].
 struct HardNegLaunch {
   const void* row_offsets;
   bool offsets64;
@@ -64,7 +63,15 @@ struct HardNegLaunch {
   int32_t* out;
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
 };
-hipError_t launch_hard_negatives(const HardNegLaunch& a, hipStream_t s);
+// Walk budgets above kMaxOnChipLandings count visits in a global table of the
+// workspace (hard_negative_workspace bytes; one table per resident workgroup)
+// and need rank_hi <= kMaxGlobalRank.
+constexpr int64_t kMaxOnChipLandings = 16384;
+constexpr int64_t kMaxLandings = 1ll << 22;
+constexpr int kMaxGlobalRank = 8192;
+constexpr int64_t kGMaxBlocks = 256;
+size_t hard_negative_workspace(int64_t landings, int64_t num_queries);
+hipError_t launch_hard_negatives(const HardNegLaunch& a, void* workspace, hipStream_t s);
 
 // Graph neighbourhoods (Sec. 3.4, MapReduce inference): each source's CSR row,
 // or top_t Philox draws from it when longer, as distinct ids ascending with

@@ -106,20 +106,31 @@ struct Walker {
     const uint32_t r = pick_word(rnd, s);
     next_at = lo + (int64_t)(((uint64_t)r * (uint64_t)deg) >> 32);
   }
-  // Moves to node nxt (read from col[next_at]) and records a pin landing.
-  __device__ void land(int32_t nxt, int64_t num_pins, int64_t num_nodes, int hops) {
-    if (!active) return;
+  // Moves to node nxt (read from col[next_at]). Returns true when the walk
+  // landed on a pin, with *visit the visit to record: the pin, or kEmpty
+  // when it is the source itself.
+  __device__ bool advance(int32_t nxt, int64_t num_pins, int64_t num_nodes, int hops,
+                          uint32_t* visit) {
+    if (!active) return false;
     if (nxt < 0 || (int64_t)nxt >= num_nodes) {
       active = false;
-      return;
+      return false;
     }
     cur = nxt;
     ++s;
+    bool on_pin = false;
     if (cur < num_pins) {
-      mine[landed] = (cur != u) ? (uint32_t)cur : kEmpty;
+      *visit = (cur != u) ? (uint32_t)cur : kEmpty;
       ++landed;
+      on_pin = true;
     }
     if (landed >= hops || s >= 2 * hops) active = false;
+    return on_pin;
+  }
+  // advance(), recording the visit in the walk's slots.
+  __device__ void land(int32_t nxt, int64_t num_pins, int64_t num_nodes, int hops) {
+    uint32_t v;
+    if (advance(nxt, num_pins, num_nodes, hops, &v)) mine[landed - 1] = v;
   }
   // Pads the unused landing slots; returns the edge steps taken.
   __device__ uint32_t finish(int hops) {

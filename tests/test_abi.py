@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 8
+    assert lib.pinsage_version() == 9
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -89,14 +89,31 @@ def test_hard_negatives_validation(L):
     lib = L.lib()
     hp = lambda **kw: L.HardNegativeParams(**{**dict(seed=1, walks=4096, hops=4, rank_lo=1999,
                                                       rank_hi=5000, num_per_query=3), **kw})
-    call = lambda g, p, q, n, out: lib.pinsage_hard_negatives(
+    call = lambda g, p, q, n, out, ws=None, wsb=0: lib.pinsage_hard_negatives(
         ctypes.byref(g) if g is not None else None, ctypes.byref(p) if p is not None else None,
-        q, n, out, None, None)
+        q, n, out, None, ws, wsb, None)
     assert call(None, hp(), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
     assert call(_graph(L), None, FAKE, 4, FAKE) == L.PINSAGE_EINVAL
     assert call(_graph(L), hp(walks=0), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
-    assert call(_graph(L), hp(hops=5), FAKE, 4, FAKE) == L.PINSAGE_EUNSUPPORTED  # 20480 slots
-    assert b"16384" in lib.pinsage_last_error()
+    assert call(_graph(L), hp(walks=1 << 21, hops=3), FAKE, 4, FAKE) == L.PINSAGE_EUNSUPPORTED
+    assert b"exceeds" in lib.pinsage_last_error()
+    # Budgets past the on-chip slots count visits in the workspace, and rank
+    # only up to rank_hi = 8192 there.
+    n = ctypes.c_size_t(1)
+    assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(hp()), 4, ctypes.byref(n)) == 0
+    assert n.value == 0  # 16384 landings: on chip
+    big = hp(hops=5)     # 20480 landings: a 2^16-entry table per workgroup
+    assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(big), 4, ctypes.byref(n)) == 0
+    assert n.value == 4 * 2 * (1 << 16) * 4
+    assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(big), 10_000,
+                                                     ctypes.byref(n)) == 0
+    assert n.value == 256 * 2 * (1 << 16) * 4  # at most 256 resident workgroups
+    assert call(_graph(L), big, FAKE, 4, FAKE) == L.PINSAGE_EWORKSPACE
+    assert call(_graph(L), big, FAKE, 4, FAKE, FAKE, 100) == L.PINSAGE_EWORKSPACE
+    assert call(_graph(L), big, FAKE, 4, FAKE, FAKE + 8, 1 << 30) == L.PINSAGE_EINVAL
+    assert call(_graph(L), hp(hops=5, rank_hi=8193), FAKE, 4, FAKE, FAKE, 1 << 30) == \
+        L.PINSAGE_EUNSUPPORTED
+    assert b"8192" in lib.pinsage_last_error()
     assert call(_graph(L), hp(rank_lo=-1), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
     assert call(_graph(L), hp(rank_lo=10, rank_hi=10), FAKE, 4, FAKE) == L.PINSAGE_EINVAL
     assert call(_graph(L), hp(num_per_query=-1), FAKE, 4, FAKE) == L.PINSAGE_EINVAL

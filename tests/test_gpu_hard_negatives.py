@@ -113,3 +113,56 @@ def test_more_queries_than_workgroups(orc, tiny):
                                                           5, 40, 3))
     valid = [int(u) for u in q if 0 <= u < wl.num_nodes]
     assert steps == sum(orc.walk_visits(off, col, wl.num_pins, 31, u, 100, 2)[1] for u in valid)
+
+
+# ---- walk budgets past the 16,384 on-chip slots: visits counted in a global
+# table of the workspace, ranks selected by count threshold and id -----------
+
+def test_global_table_medium_paper_window(orc):
+    # 131,072 landings per query on the 1.2M-node graph: the paper's window
+    # [1999, 5000) is then decided by visit counts (pins visited once rank
+    # last), not by the id order of single visits.
+    wl = synth.WORKLOADS["medium"]
+    off, col, _ = synth.make_graph(wl)
+    rng = np.random.default_rng(9)
+    q = rng.integers(0, wl.num_pins, 400).astype(np.int32)
+    walks, hops, lo, hi, k = 32768, 4, 1999, 5000, 8
+    print(f"[case] medium hard negatives, global table n={len(q)} W={walks} H={hops} "
+          f"[{lo},{hi}) k={k}", flush=True)
+    got, steps = _gpu(off, col, wl.num_pins, wl.num_boards, q, k, 77, walks, hops, lo, hi)
+    ref = orc.hard_negatives(off, col, wl.num_pins, 77, walks, hops, q, lo, hi, k)
+    np.testing.assert_array_equal(got, ref)
+    # The window is inside the repeated-visit pins for most queries.
+    u = int(q[0])
+    visits = orc.walk_visits(off, col, wl.num_pins, 77, u, walks, hops)[0]
+    vals, cnts = np.unique(visits[(visits >= 0) & (visits != u)], return_counts=True)
+    assert np.sort(cnts)[::-1][hi - 1] >= 2, "rank 5000 should still be a repeated pin"
+
+
+@pytest.mark.parametrize("pins,boards,walks,hops,lo,hi,k,nq", [
+    (2000, 500, 20000, 1, 100, 1900, 5, 300),   # every pin ranked (D <= rank_hi), > 256 queries
+    (60, 10, 65536, 4, 0, 10, 7, 20),            # counts above 4096: second count digit
+    (300, 40, 8192, 4, 20, 200, 3, 50),          # threshold inside a count class
+])
+def test_global_table_small_graphs(orc, pins, boards, walks, hops, lo, hi, k, nq):
+    base = synth.WORKLOADS["tiny"]
+    wl = base.scaled(pins, boards, f"hn-{pins}")
+    off, col, _ = synth.make_graph(wl)
+    q = _queries(wl, nq, pins + walks)
+    print(f"[case] hard negatives, global table P={pins} B={boards} W={walks} H={hops} "
+          f"[{lo},{hi}) k={k} n={nq}", flush=True)
+    got, steps = _gpu(off, col, wl.num_pins, wl.num_boards, q, k, 5, walks, hops, lo, hi)
+    np.testing.assert_array_equal(got, orc.hard_negatives(off, col, wl.num_pins, 5, walks, hops,
+                                                          q, lo, hi, k))
+    want = sum(orc.walk_visits(off, col, wl.num_pins, 5, u, walks, hops)[1] for u in q.tolist())
+    assert steps == want
+
+
+def test_global_table_int64_offsets(orc, tiny):
+    wl, off, col = tiny
+    q = _queries(wl, 64, 41)
+    print("[case] hard negatives, global table, int64 offsets", flush=True)
+    got, _ = _gpu(off, col, wl.num_pins, wl.num_boards, q, 4, 8, 9000, 3, 50, 700,
+                  offsets64=True)
+    np.testing.assert_array_equal(got, orc.hard_negatives(off, col, wl.num_pins, 8, 9000, 3, q,
+                                                          50, 700, 4))
