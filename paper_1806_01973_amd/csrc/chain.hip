@@ -6,13 +6,14 @@
 // This kernel computes R directly: P = ReLU(H Q^T + q) exists only in
 // registers, 32 columns at a time, and never reaches memory.
 //
-// Block: 8 waves (two per SIMD), 256 rows of H; wave w owns rows
-// 32 w .. 32 w + 31 of the tile and keeps their H fragments for the whole
-// K = d_in of the first product in registers (64 VGPRs) beside its R
-// accumulators (d_out x 32 fp32, 128 VGPRs). (Four waves of 64 rows each,
-// sharing every weight fragment between two MFMAs, measured slower: their
-// 288 accumulator registers overflow the 256 AGPRs.) For each chunk of 32
-// columns of P:
+// Block: 4 waves (one per SIMD), 128 rows of H; two blocks share a CU, so one
+// block's H loads and R stores can run under the other's matrix work. Wave w
+// owns rows 32 w .. 32 w + 31 of the tile and keeps their H fragments for the
+// whole K = d_in of the first product in registers (64 VGPRs) beside its R
+// accumulators (d_out x 32 fp32, 128 registers). (Four waves of 64 rows each,
+// sharing every weight fragment between two MFMAs, measured slower: their 288
+// accumulator registers overflow the 256 AGPRs.) For each chunk of 32 columns
+// of P:
 //   1. acc1 (32 x 32) = Q_chunk H^T over K = d_in (v_mfma_f32_32x32x16_bf16;
 //      Q rows are the first operand, so a lane holds one H row and the P
 //      columns 8 g + 4 h + e, h = lane / 32, e < 4, g < 4);
@@ -24,10 +25,11 @@
 //      exactly what acc1 holds; W_n' is W_n with the columns of every
 //      16-column group reordered to match (permute_wn_kernel), so the product
 //      is the same sum over the same 32 columns.
-// Q and W_n' chunks (16 KB each for d_in = d_out = 256) travel global -> LDS
-// by DMA (global_load_lds_dwordx4) into three stages, two chunks ahead, one
-// barrier per chunk; rows are padded by 16 bytes so fragment reads of 16
-// rows fall on distinct banks. The first product of chunk j + 1 and the
+// Q chunks (16 KB for d_in = 256, with the chunk's 32 bias values behind the
+// padded rows) and W_n' chunks (16 KB for d_out = 256) travel global -> LDS by
+// DMA (global_load_lds_dwordx4) into two rings of two slots each (74 KB per
+// block), one barrier per chunk; rows are padded by 16 bytes so fragment reads
+// of 16 rows fall on distinct banks. The first product of chunk j + 1 and the
 // second of chunk j run interleaved, step by step, so the matrix pipe never
 // waits for the bias/ReLU/rounding of a chunk. R is accumulated in fp32 over
 // the chunks in order and rounded once to bf16.
@@ -42,12 +44,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kWaves = 8;
-constexpr int kRB = 1;  // 32-row blocks per wave
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kTileRows = 32 * kRB * kWaves;
-constexpr int kMC = 32;            // P columns per chunk
-constexpr int kMaxBiasCols = 2048;  // m <= 2048
+constexpr int kTileRows = 32 * kWaves;
+constexpr int kMC = 32;        // P columns per chunk
+constexpr int kMaxCols = 2048;  // m <= 2048 (32-bit DMA offsets within a chunk)
 
 // W_n' [d_out][m]: column 16 G + 8 h + u of row n holds column
 // 16 G + 4 h + u + 4 [u >= 4] of W's neighbour half (W[n][d_in + .]).
@@ -80,23 +81,23 @@ __device__ __forceinline__ void wait_all_and_barrier() {
 // KS = d_in / 16 k-steps of the first product (d_in a multiple of 128, so a
 // Q row has a multiple of 16 vectors), NB = d_out / 32 output blocks.
 template <int KS, int NB>
-__global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void chain_kernel(ChainLaunch a) {
   // LDS rows are padded by 16 bytes: 16 consecutive rows read at the same
   // column then start 4 banks apart (528 = 64 x 8 + 16 bytes, 80 = 64 + 16),
   // so fragment reads are conflict-free and their addresses are one base
   // register plus immediate offsets.
-  constexpr int QROW = KS * 32 + 16;    // bytes of a padded Q row (d_in bf16)
-  constexpr int WROW = 64 + 16;         // bytes of a padded W_n' row (32 bf16)
-  constexpr int QDMA = (kMC * QROW + 1023) / 1024;  // 1 KB DMA blocks of a Q chunk
+  constexpr int QROW = KS * 32 + 16;  // bytes of a padded Q row (d_in bf16)
+  constexpr int WROW = 64 + 16;       // bytes of a padded W_n' row (32 bf16)
+  constexpr int QDATA = kMC * QROW;   // the chunk's bias floats follow the rows
+  constexpr int QDMA = (QDATA + kMC * 4 + 1023) / 1024;  // 1 KB DMA blocks per Q slot
   constexpr int WDMA = (NB * 32 * WROW + 1023) / 1024;
   constexpr int QBYTES = QDMA * 1024;
   constexpr int WBYTES = WDMA * 1024;
-  constexpr int STAGE = QBYTES + WBYTES;
-  constexpr int NDMA = QDMA + WDMA;
-  constexpr int DMA_PER_WAVE = (NDMA + kWaves - 1) / kWaves;
+  constexpr int WRING = 2 * QBYTES;   // the W_n' ring follows the Q ring
   static_assert(KS == 2 * NB, "the two products interleave step for step");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[3 * STAGE];
-  __shared__ __attribute__((aligned(16))) float bias_s[kMaxBiasCols];
+  static_assert(QDATA % 16 == 0, "bias vectors aligned");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * QBYTES + 2 * WBYTES];
   const uint32_t smem_base =
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
 
@@ -106,124 +107,124 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
   const int h = lane >> 5, r32 = lane & 31;
   const int m = a.m;
   const int nc = m / kMC;
-  // Row of this lane in row block b: row0w + 32 b.
-  const int64_t row0w = (int64_t)blockIdx.x * kTileRows + 32 * kRB * wave + r32;
+  const int64_t row0w = (int64_t)blockIdx.x * kTileRows + 32 * wave + r32;
 
-  for (int c = tid; c < m; c += kThreads) bias_s[c] = a.q[c];
-
-  // DMA: 1 KB block blk < QDMA of a stage holds padded Q rows, the rest
-  // padded W_n' rows; wave w issues blocks w, w + 4, ... Lane i of a block
-  // fills byte 16 i of it: the row's vector there, or (pad and tail bytes,
-  // never read) a copy of the chunk's first vector. Offsets are recomputed
-  // per issue (a few integer ops) rather than held in registers, which the
-  // two products' operands and accumulators fill.
+  // DMA: 1 KB block blk of a Q slot holds padded Q rows then the bias; wave w
+  // issues blocks w, w + 4, ... Lane i of a block fills byte 16 i of it: the
+  // row's vector there, or (pad and tail bytes, never read) a copy of the
+  // chunk's first vector; lanes over the bias bytes stay off, and the last
+  // wave fills them from q. Offsets are recomputed per issue (a few integer
+  // ops) rather than held in registers, which the two products' operands and
+  // accumulators fill.
   const unsigned char* const qbase = static_cast<const unsigned char*>(a.Q);
   const unsigned char* const wbase = static_cast<const unsigned char*>(a.Wp);
-  auto issue = [&](int j, int stage) __attribute__((always_inline)) {
+  const unsigned char* const bbase = reinterpret_cast<const unsigned char*>(a.q);
+  auto issue_q = [&](int j) __attribute__((always_inline)) {
+    const int slot = j & 1;
     const unsigned char* qb = qbase + (int64_t)j * kMC * a.d_in * 2;
+#pragma unroll
+    for (int d = 0; d < (QDMA + kWaves - 1) / kWaves; ++d) {
+      const int blk = wave + kWaves * d;
+      if (blk >= QDMA) break;  // wave-uniform
+      const int p = blk * 1024 + 16 * lane;
+      const int r = p / QROW, c = p % QROW;
+      uint32_t off = 0;
+      if (r < kMC && c < KS * 32) off = (uint32_t)((r * a.d_in) * 2 + c);
+      if (p < QDATA || p >= QDATA + kMC * 4)
+        dma16(qb, off, __builtin_amdgcn_readfirstlane(smem_base + slot * QBYTES + blk * 1024));
+    }
+    if (wave == kWaves - 1 && lane < kMC / 4)
+      dma16(bbase, (uint32_t)(j * kMC * 4 + 16 * lane),
+            __builtin_amdgcn_readfirstlane(smem_base + slot * QBYTES + QDATA));
+  };
+  auto issue_w = [&](int j) __attribute__((always_inline)) {
+    const int slot = j & 1;
     const unsigned char* wb = wbase + (int64_t)j * kMC * 2;
 #pragma unroll
-    for (int d = 0; d < DMA_PER_WAVE; ++d) {
+    for (int d = 0; d < (WDMA + kWaves - 1) / kWaves; ++d) {
       const int blk = wave + kWaves * d;
-      if (blk >= NDMA) break;  // wave-uniform
+      if (blk >= WDMA) break;  // wave-uniform
+      const int p = blk * 1024 + 16 * lane;
+      const int n = p / WROW, c = p % WROW;
       uint32_t off = 0;
-      if (blk < QDMA) {
-        const int p = blk * 1024 + 16 * lane;
-        const int r = p / QROW, c = p % QROW;
-        if (r < kMC && c < KS * 32) off = (uint32_t)((r * a.d_in) * 2 + c);
-      } else {
-        const int p = (blk - QDMA) * 1024 + 16 * lane;
-        const int n = p / WROW, c = p % WROW;
-        if (n < NB * 32 && c < 64) off = (uint32_t)(n * m * 2 + c);
-      }
-      dma16(blk < QDMA ? qb : wb, off,
-            __builtin_amdgcn_readfirstlane(smem_base + blk * 1024 + stage * STAGE));
+      if (n < NB * 32 && c < 64) off = (uint32_t)(n * m * 2 + c);
+      dma16(wb, off,
+            __builtin_amdgcn_readfirstlane(smem_base + WRING + slot * WBYTES + blk * 1024));
     }
   };
 
-  // This lane's H rows (through the row map; missing rows read as zeros).
-  u32x4 hf[kRB][KS];
-#pragma unroll
-  for (int b = 0; b < kRB; ++b) {
-    const int64_t row = row0w + 32 * b;
+  // This lane's H row (through the row map; a missing row reads as zeros).
+  u32x4 hf[KS];
+  {
     int64_t hsrc = -1;
-    if (row < a.rows) hsrc = a.rowmap ? (int64_t)a.rowmap[row] : a.row0 + row;
+    if (row0w < a.rows) hsrc = a.rowmap ? (int64_t)a.rowmap[row0w] : a.row0 + row0w;
     const bool hok = hsrc >= 0 && hsrc < a.rows_h;
     const u32x4* hp = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.H) +
                                                      (hok ? hsrc : 0) * a.ldh + 8 * h);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) hf[b][ks] = hok ? hp[2 * ks] : u32x4{0u, 0u, 0u, 0u};
+    for (int ks = 0; ks < KS; ++ks) hf[ks] = hok ? hp[2 * ks] : u32x4{0u, 0u, 0u, 0u};
   }
 
-  f32x16 acc2[kRB][NB];
+  f32x16 acc2[NB];
 #pragma unroll
-  for (int b = 0; b < kRB; ++b)
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc2[b][nb][e] = 0.0f;
-  f32x16 acc1[kRB];
-  u32x4 pa[kRB][2];
+    for (int e = 0; e < 16; ++e) acc2[nb][e] = 0.0f;
+  f32x16 acc1;
+  u32x4 pa[2];
 
   const int qoff = r32 * QROW + 16 * h;
-  const int woff = QBYTES + r32 * WROW + 16 * h;
-  auto read_q = [&](int stage, int ks) __attribute__((always_inline)) {
-    return *reinterpret_cast<const u32x4*>(smem + stage * STAGE + qoff + 32 * ks);
+  const int woff = WRING + r32 * WROW + 16 * h;
+  auto read_q = [&](int slot, int ks) __attribute__((always_inline)) {
+    return *reinterpret_cast<const u32x4*>(smem + slot * QBYTES + qoff + 32 * ks);
   };
   // Step t of the second product: output block t / 2, k-step t % 2.
-  auto read_w = [&](int stage, int t) __attribute__((always_inline)) {
-    return *reinterpret_cast<const u32x4*>(smem + stage * STAGE + woff +
+  auto read_w = [&](int slot, int t) __attribute__((always_inline)) {
+    return *reinterpret_cast<const u32x4*>(smem + slot * WBYTES + woff +
                                            32 * (t >> 1) * WROW + 32 * (t & 1));
   };
   auto zero_acc1 = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int b = 0; b < kRB; ++b)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc1[b][e] = 0.0f;
+    for (int e = 0; e < 16; ++e) acc1[e] = 0.0f;
   };
   auto step1 = [&](int ks, const u32x4& qf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < kRB; ++b)
-      acc1[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qf),
-                                                        __builtin_bit_cast(bf16x8, hf[b][ks]),
-                                                        acc1[b], 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qf),
+                                                   __builtin_bit_cast(bf16x8, hf[ks]), acc1, 0,
+                                                   0, 0);
   };
   auto step2 = [&](int t, const u32x4& wf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < kRB; ++b)
-      acc2[b][t >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, pa[b][t & 1]),
-          acc2[b][t >> 1], 0, 0, 0);
+    acc2[t >> 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        __builtin_bit_cast(bf16x8, wf), __builtin_bit_cast(bf16x8, pa[t & 1]), acc2[t >> 1], 0,
+        0, 0);
   };
-  // acc1 of chunk j (its 32 columns of P) + q, ReLU, bf16 -> pa.
-  auto finish_p = [&](int j) __attribute__((always_inline)) {
+  // acc1 (32 columns of P) + q from Q slot `slot`, ReLU, bf16 -> pa.
+  auto finish_p = [&](int slot) __attribute__((always_inline)) {
+    const float* bias = reinterpret_cast<const float*>(smem + slot * QBYTES + QDATA);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       float4 bv[2];
 #pragma unroll
       for (int gg = 0; gg < 2; ++gg)
-        bv[gg] = *reinterpret_cast<const float4*>(bias_s + kMC * j + 8 * (2 * s + gg) + 4 * h);
+        bv[gg] = *reinterpret_cast<const float4*>(bias + 8 * (2 * s + gg) + 4 * h);
+      uint32_t w[4];
 #pragma unroll
-      for (int b = 0; b < kRB; ++b) {
-        uint32_t w[4];
-#pragma unroll
-        for (int gg = 0; gg < 2; ++gg) {
-          const int g = 2 * s + gg;
-          const float x0 = fmaxf(acc1[b][4 * g] + bv[gg].x, 0.0f);
-          const float x1 = fmaxf(acc1[b][4 * g + 1] + bv[gg].y, 0.0f);
-          const float x2 = fmaxf(acc1[b][4 * g + 2] + bv[gg].z, 0.0f);
-          const float x3 = fmaxf(acc1[b][4 * g + 3] + bv[gg].w, 0.0f);
-          w[2 * gg] = pack_bf16x2(x0, x1);
-          w[2 * gg + 1] = pack_bf16x2(x2, x3);
-        }
-        pa[b][s] = u32x4{w[0], w[1], w[2], w[3]};
+      for (int gg = 0; gg < 2; ++gg) {
+        const int g = 2 * s + gg;
+        const float x0 = fmaxf(acc1[4 * g] + bv[gg].x, 0.0f);
+        const float x1 = fmaxf(acc1[4 * g + 1] + bv[gg].y, 0.0f);
+        const float x2 = fmaxf(acc1[4 * g + 2] + bv[gg].z, 0.0f);
+        const float x3 = fmaxf(acc1[4 * g + 3] + bv[gg].w, 0.0f);
+        w[2 * gg] = pack_bf16x2(x0, x1);
+        w[2 * gg + 1] = pack_bf16x2(x2, x3);
       }
+      pa[s] = u32x4{w[0], w[1], w[2], w[3]};
     }
   };
 
-  // Prologue: chunks 0 and 1 into stages 0 and 1; P of chunk 0.
-  issue(0, 0);
-  if (nc > 1) issue(1, 1);
+  // Prologue: Q chunks 0 and 1 and W_n' chunk 0 in flight; P of chunk 0.
+  issue_q(0);
+  issue_w(0);
+  if (nc > 1) issue_q(1);
   wait_all_and_barrier();
   zero_acc1();
   {
@@ -237,40 +238,44 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
     }
   }
   finish_p(0);
+  // Every wave is done with Q slot 0 before chunk 2 refills it.
+  wait_all_and_barrier();
 
-  // Chunk j: the chunk j + 2 lands in stage (j + 2) % 3 while the first
-  // product of chunk j + 1 (stage (j + 1) % 3) and the second product of
-  // chunk j (stage j % 3) run interleaved step by step, each step's fragment
-  // reads issued one step ahead of its MFMAs.
+  // Iteration j: the first product of chunk j + 1 (Q slot (j + 1) & 1) and
+  // the second of chunk j (W_n' slot j & 1) run interleaved step by step, each
+  // step's fragment reads issued one step ahead of its MFMAs, while Q chunk
+  // j + 2 (into the slot chunk j left) and W_n' chunk j + 1 (into the slot
+  // chunk j - 1 left) land.
   for (int j = 0; j + 1 < nc; ++j) {
-    const int s0 = j % 3, s1 = (j + 1) % 3;
-    if (j + 2 < nc) issue(j + 2, (j + 2) % 3);
+    if (j + 2 < nc) issue_q(j + 2);
+    issue_w(j + 1);
+    const int sq = (j + 1) & 1, sw = j & 1;
     zero_acc1();
-    u32x4 qf = read_q(s1, 0), wf = read_w(s0, 0);
+    u32x4 qf = read_q(sq, 0), wf = read_w(sw, 0);
 #pragma unroll
     for (int t = 0; t < KS; ++t) {
       u32x4 qn = qf, wn = wf;
       if (t + 1 < KS) {
-        qn = read_q(s1, t + 1);
-        wn = read_w(s0, t + 1);
+        qn = read_q(sq, t + 1);
+        wn = read_w(sw, t + 1);
       }
       step1(t, qf);
       step2(t, wf);
       qf = qn;
       wf = wn;
     }
-    finish_p(j + 1);
-    // Chunk j + 2 has landed, and every wave is done with stage j % 3
-    // before chunk j + 3 refills it.
+    finish_p(sq);
+    // The chunks issued above have landed, and every wave is done with the
+    // slots they refill next.
     wait_all_and_barrier();
   }
   {
-    const int s0 = (nc - 1) % 3;
-    u32x4 wf = read_w(s0, 0);
+    const int sw = (nc - 1) & 1;
+    u32x4 wf = read_w(sw, 0);
 #pragma unroll
     for (int t = 0; t < 2 * NB; ++t) {
       u32x4 wn = wf;
-      if (t + 1 < 2 * NB) wn = read_w(s0, t + 1);
+      if (t + 1 < 2 * NB) wn = read_w(sw, t + 1);
       step2(t, wf);
       wf = wn;
     }
@@ -284,10 +289,10 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
   // 256-byte row halves, 16 lanes per row.
   static_assert(NB % 4 == 0, "R staged in 128-column halves");
   constexpr int SROW = 256 + 16;
-  static_assert(kWaves * 32 * SROW <= 3 * STAGE, "staging fits the stages");
-  __syncthreads();  // every wave is done with the stages
+  static_assert(kWaves * 32 * SROW <= 2 * QBYTES + 2 * WBYTES, "staging fits the rings");
+  __syncthreads();  // every wave is done with the rings
   unsigned char* stg = smem + wave * 32 * SROW;
-  const int64_t rbase = (int64_t)blockIdx.x * kTileRows + 32 * kRB * wave;
+  const int64_t rbase = (int64_t)blockIdx.x * kTileRows + 32 * wave;
 #pragma unroll
   for (int half = 0; half < NB / 4; ++half) {
 #pragma unroll
@@ -295,8 +300,8 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int nb = 4 * half + nb4;
-        const u32x2 v = {pack_bf16x2(acc2[0][nb][4 * g], acc2[0][nb][4 * g + 1]),
-                         pack_bf16x2(acc2[0][nb][4 * g + 2], acc2[0][nb][4 * g + 3])};
+        const u32x2 v = {pack_bf16x2(acc2[nb][4 * g], acc2[nb][4 * g + 1]),
+                         pack_bf16x2(acc2[nb][4 * g + 2], acc2[nb][4 * g + 3])};
         *reinterpret_cast<u32x2*>(stg + r32 * SROW + (32 * nb4 + 8 * g + 4 * h) * 2) = v;
       }
     wave_lds_sync();
@@ -316,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(ChainLaunch a) {
 }  // namespace
 
 bool chain_supported(int d_in, int m, int d_out, bool bf16) {
-  return bf16 && d_in == 256 && d_out == 256 && m % kMC == 0 && m > 0 && m <= kMaxBiasCols;
+  return bf16 && d_in == 256 && d_out == 256 && m % kMC == 0 && m > 0 && m <= kMaxCols;
 }
 
 hipError_t launch_permute_wn(const void* W, int64_t ldw, int d_in, int m, int d_out, void* Wp,
