@@ -116,6 +116,37 @@ def copy_calibration(gib: float = 1.0, reps: int = 5) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
 
 
+def random_read_calibration(table_gib: int = 16, steps: int = 32, reps: int = 3) -> None:
+    """Dependent random reads per second (the library's calibration kernel):
+    4-, 8- and 16-byte elements from a table_gib table, and 16-byte elements
+    from its first 256 MiB, at several numbers of chains in flight."""
+    import torch
+    from paper_1806_01973_amd import _lib
+    L = _lib.lib()
+    table = torch.empty(table_gib << 30, dtype=torch.uint8, device="cuda")  # never written
+    chains_max = 16384 * 256
+    sink = torch.empty(chains_max, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {"table_bytes": table.numel(), "steps": steps, "reps": reps}
+    for name, nbytes, eb in (("4B", table.numel(), 4), ("8B", table.numel(), 8),
+                             ("16B", table.numel(), 16), ("16B_256MiB", 256 << 20, 16)):
+        for chains in (2048 * 256, 8192 * 256, chains_max):
+            def launch():
+                _lib.check(L.pinsage_profile_random_reads(table.data_ptr(), nbytes, eb, steps,
+                                                          sink.data_ptr(), chains,
+                                                          stream.cuda_stream), "random reads")
+            launch()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            out[f"reads_per_s_{name}_chains{chains}"] = chains * steps / (ms * 1e-3)
+    print(json.dumps(out), flush=True)
+
+
 def load_inputs(wl, dataflow="pool_then_dense", pool="importance"):
     """Inputs on the GPU plus host views the CPU baseline needs."""
     import numpy as np
@@ -741,6 +772,8 @@ def main() -> int:
     ap.add_argument("--blas-ref", action="store_true",
                     help="with --layer: also time torch.matmul on the layer's GEMM shapes")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--random-read-calibration", action="store_true",
+                    help="dependent random reads/s from a 16 GiB table (the walks' ceiling)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -752,6 +785,9 @@ def main() -> int:
 
     if args.copy_calibration:
         copy_calibration()
+        return 0
+    if args.random_read_calibration:
+        random_read_calibration()
         return 0
     if args.layer:
         return layer_probe(args)

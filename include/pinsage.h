@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 9
+#define PINSAGE_ABI_VERSION 10
 
 enum {
   PINSAGE_OK = 0,
@@ -453,10 +453,29 @@ enum {
   PINSAGE_KERNEL_GRAPH_NBR = 9, /* graph neighbourhoods (MapReduce variant) */
   PINSAGE_KERNEL_GEMM_QR = 10,  /* Q transform chained into the neighbour half of
                                    W (DENSE_THEN_POOL, bf16, d_in = d_out = 256) */
-  PINSAGE_KERNEL_COUNT = 11
+  PINSAGE_KERNEL_WALK_TABLE = 11, /* the walk table of pinsage_embed_all's walks */
+  PINSAGE_KERNEL_COUNT = 12
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);
+
+/* Random-read calibration (bench support, not part of the method): the chip's
+ * rate of dependent random reads, the resource that bounds the walks of
+ * Sec. 3.2 (one read of a neighbour id at an unrelated address per edge step).
+ * `chains` lanes each make `steps` reads from the table, the index of each read
+ * a hash of the value the one before returned, so a lane has one read in
+ * flight at a time.
+ * table: device, aligned to elem_bytes, table_bytes bytes, contents arbitrary
+ *   (never written); the
+ *   reads use its first 2^k elements of elem_bytes bytes, 2^k the largest
+ *   power of two that fits;
+ * elem_bytes: 4, 8 or 16;  steps >= 1;  chains >= 1;
+ * sink: device uint32 [chains], written (one value per chain keeps the reads
+ *   live). Asynchronous on `stream`; time it with events on that stream.
+ * Errors: PINSAGE_EINVAL for a NULL pointer, an element size other than 4, 8
+ * or 16, a table smaller than one element, or steps or chains below 1. */
+int pinsage_profile_random_reads(const void* table, size_t table_bytes, int32_t elem_bytes,
+                                 int32_t steps, uint32_t* sink, int64_t chains, void* stream);
 
 #ifdef __cplusplus
 }

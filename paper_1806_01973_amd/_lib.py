@@ -23,7 +23,7 @@ POOLS = {"importance": 0, "mean": 1, "max": 2}
 (KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
  KERNEL_GEMM_R, KERNEL_MLP) = range(8)
 KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp",
-                "hard_neg", "graph_nbr", "gemm_qr"]
+                "hard_neg", "graph_nbr", "gemm_qr", "walk_table"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",
@@ -36,7 +36,7 @@ EXPORTED = [
     "pinsage_output_mlp_workspace_size",
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
-    "pinsage_profile_enable", "pinsage_profile_read",
+    "pinsage_profile_enable", "pinsage_profile_read", "pinsage_profile_random_reads",
 ]
 
 
@@ -151,6 +151,9 @@ def lib():
     L.pinsage_profile_enable.argtypes = [ctypes.c_int]
     L.pinsage_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
                                        ctypes.POINTER(ctypes.c_double)]
+    L.pinsage_profile_random_reads.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                               ctypes.c_void_p]
     for name in EXPORTED:
         fn = getattr(L, name)
         if fn.restype is None or fn.restype is ctypes.c_int:

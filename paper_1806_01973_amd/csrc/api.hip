@@ -553,6 +553,43 @@ const char* pinsage_status_string(int status) {
 
 const char* pinsage_last_error(void) { return g_last_error.c_str(); }
 
+// Bytes of a graph's walk table (0 when nnz is too large for one).
+size_t walk_table_bytes(const pinsage_graph_t* g) {
+  return g->nnz > 0 && g->nnz <= kWalkTableMaxNnz ? align_up((size_t)g->nnz * 16) : 0;
+}
+
+// The walks and top-T of validated arguments; `table` is the graph's walk
+// table or NULL (read the CSR).
+int run_walks(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+              const int32_t* sources, int64_t num_sources, pinsage_neighborhoods_t* out,
+              unsigned long long* total_steps, const void* table, hipStream_t s) {
+  if (total_steps) {
+    hipError_t e = launch_zero_u64(total_steps, 1, s);
+    if (e != hipSuccess) return hip_fail(e, "step counter reset");
+  }
+  WalkLaunch a{};
+  a.row_offsets = graph->row_offsets;
+  a.offsets64 = graph->offset_type == PINSAGE_I64;
+  a.col = graph->col;
+  a.nnz = graph->nnz;
+  a.num_pins = graph->num_pins;
+  a.num_nodes = graph->num_pins + graph->num_boards;
+  a.sources = sources;
+  a.num_sources = num_sources;
+  a.seed = walk->seed;
+  a.walks = walk->walks_per_node;
+  a.hops = walk->hops;
+  a.top_t = walk->top_t;
+  a.idx = out->idx;
+  a.counts = out->counts;
+  a.weights = out->weights;
+  a.total_steps = total_steps;
+  a.table = table;
+  hipError_t e = launch_walk_topt(a, s);
+  if (e != hipSuccess) return hip_fail(e, "walk launch");
+  return PINSAGE_OK;
+}
+
 int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                                 const int32_t* sources, int64_t num_sources,
                                 pinsage_neighborhoods_t* out, unsigned long long* total_steps,
@@ -569,31 +606,8 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk
   if ((st = check_nbr(out, num_sources, "build_neighborhoods"))) return st;
   if (out->top_t != walk->top_t)
     return fail(PINSAGE_EINVAL, "out->top_t %d != walk->top_t %d", out->top_t, walk->top_t);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (total_steps) {
-    hipError_t e = launch_zero_u64(total_steps, 1, s);
-    if (e != hipSuccess) return hip_fail(e, "step counter reset");
-  }
-  WalkLaunch a{};
-  a.row_offsets = graph->row_offsets;
-  a.offsets64 = graph->offset_type == PINSAGE_I64;
-  a.col = graph->col;
-  a.nnz = graph->nnz;
-  a.num_pins = graph->num_pins;
-  a.num_nodes = n;
-  a.sources = sources;
-  a.num_sources = num_sources;
-  a.seed = walk->seed;
-  a.walks = walk->walks_per_node;
-  a.hops = walk->hops;
-  a.top_t = walk->top_t;
-  a.idx = out->idx;
-  a.counts = out->counts;
-  a.weights = out->weights;
-  a.total_steps = total_steps;
-  hipError_t e = launch_walk_topt(a, s);
-  if (e != hipSuccess) return hip_fail(e, "walk launch");
-  return PINSAGE_OK;
+  return run_walks(graph, walk, sources, num_sources, out, total_steps, nullptr,
+                   static_cast<hipStream_t>(stream));
 }
 
 int check_hard_negative_params(const pinsage_hard_negative_params_t* params, int64_t num_queries) {
@@ -920,7 +934,10 @@ int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph, const pinsage
     }
   }
   const int hbufs = num_layers > 2 ? 2 : (num_layers > 1 ? 1 : 0);
-  *bytes = conv + (size_t)hbufs * h;
+  // The walk table shares the layers' region: the in-order walks finish before
+  // the first transform writes it.
+  const size_t tb = walk_table_bytes(graph);
+  *bytes = (conv > tb ? conv : tb) + (size_t)hbufs * h;
   return PINSAGE_OK;
 }
 
@@ -964,6 +981,8 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
       h = hb > h ? hb : h;
     }
   }
+  const size_t tb = walk_table_bytes(graph);
+  if (tb > conv) conv = tb;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   unsigned char* hbuf[2] = {ws + conv, ws + conv + h};
   const int64_t P = graph->num_pins;
@@ -1019,7 +1038,14 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
     }
   }
   if (!transformed) {
-    if ((st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps, stream)))
+    // In order: the walks read the graph's walk table, built in the layers'
+    // region of the workspace (one read per edge step instead of two).
+    if (tb) {
+      const hipError_t e = launch_walk_table(graph->row_offsets, graph->offset_type == PINSAGE_I64,
+                                             graph->col, graph->nnz, n, ws, s);
+      if (e != hipSuccess) return hip_fail(e, "walk table launch");
+    }
+    if ((st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, tb ? ws : nullptr, s)))
       return st;
     if ((st = run_transform(L0, x, n, P, nullptr, n, ws, s))) return st;
   }
@@ -1118,6 +1144,22 @@ int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms) {
   g_pending.clear();
   *launches = g_prof_count[kernel];
   *total_ms = g_prof_ms[kernel];
+  return PINSAGE_OK;
+}
+
+int pinsage_profile_random_reads(const void* table, size_t table_bytes, int32_t elem_bytes,
+                                 int32_t steps, uint32_t* sink, int64_t chains, void* stream) {
+  g_last_error.clear();
+  if (!table || !sink) return fail(PINSAGE_EINVAL, "NULL table or sink");
+  if (elem_bytes != 4 && elem_bytes != 8 && elem_bytes != 16)
+    return fail(PINSAGE_EINVAL, "element size %d (4, 8 or 16)", elem_bytes);
+  if (table_bytes < (size_t)elem_bytes) return fail(PINSAGE_EINVAL, "table smaller than one element");
+  if (steps < 1 || chains < 1) return fail(PINSAGE_EINVAL, "steps %d, chains %lld", steps, (long long)chains);
+  uint64_t elements = 1;
+  while (elements * 2 <= table_bytes / (size_t)elem_bytes) elements *= 2;
+  hipError_t e = launch_random_reads(table, elements, elem_bytes, steps, sink, chains,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "random read launch");
   return PINSAGE_OK;
 }
 

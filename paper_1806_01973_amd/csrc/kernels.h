@@ -10,7 +10,7 @@ namespace pinsage {
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
                    kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKGraphNbr = 9, kKGemmQR = 10,
-                   kKCount = 11 };
+                   kKWalkTable = 11, kKCount = 12 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -40,8 +40,18 @@ struct WalkLaunch {
   uint16_t* counts;
   float* weights;           // nullable
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
+  const void* table;        // nullable: the walk table of the graph (below)
 };
 hipError_t launch_walk_topt(const WalkLaunch& a, hipStream_t s);
+
+// Walk table: for every CSR position e, 16 bytes {col[e], degree of col[e],
+// row start of col[e] (low, high 32 bits)}, degree 0 for an out-of-range id or
+// an empty or malformed row. A walk then takes one read per edge step instead
+// of an offset pair and a neighbour id. For graphs with nnz < 2^31 (degrees
+// fit 31 bits).
+constexpr int64_t kWalkTableMaxNnz = 0x7FFFFFFFll;
+hipError_t launch_walk_table(const void* row_offsets, bool offsets64, const int32_t* col,
+                             int64_t nnz, int64_t num_nodes, void* table, hipStream_t s);
 
 // Hard negative items (Sec. 3.3): out[i][j], j < k, drawn from ranks
 // [rank_lo, rank_hi) of the visit-count ranking of walks from queries[i].
@@ -173,6 +183,11 @@ bool chain_supported(int d_in, int m, int d_out, bool bf16);
 hipError_t launch_permute_wn(const void* W, int64_t ldw, int d_in, int m, int d_out, void* Wp,
                              hipStream_t s);
 hipError_t launch_chain(const ChainLaunch& a, hipStream_t s);
+
+// Dependent random reads (calib.hip): `chains` lanes, `steps` reads each, from
+// `elements` (a power of two) elements of elem_bytes (4, 8 or 16) bytes.
+hipError_t launch_random_reads(const void* table, uint64_t elements, int elem_bytes, int steps,
+                               uint32_t* sink, int64_t chains, hipStream_t s);
 
 // Max-margin loss (Eq. 1): per_pair[b] = mean over the shared negatives and
 // pair b's present hard negatives of max(0, zq.zn - zq.zpos + margin),

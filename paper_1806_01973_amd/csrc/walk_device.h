@@ -75,6 +75,8 @@ __device__ __forceinline__ uint32_t pick_word(const uint4& r, int s) {
 template <typename OffT>
 struct Walker {
   int64_t u, cur, next_at;
+  int64_t lo;   // walk-table path: row start and degree of the current node
+  int32_t deg;  // (0 when its row is empty or out of range)
   uint32_t w;
   int landed, s;
   bool exists, active;
@@ -105,6 +107,26 @@ struct Walker {
       rnd = philox4x32_10(make_uint4((uint32_t)u, w, (uint32_t)(s >> 2), 0u), k0, k1);
     const uint32_t r = pick_word(rnd, s);
     next_at = lo + (int64_t)(((uint64_t)r * (uint64_t)deg) >> 32);
+  }
+  // Walk-table path: the same choice from the current node's row [lo, lo + deg)
+  // carried by the walker (deg = 0 when the row is empty or malformed).
+  __device__ void pick_carried(uint32_t k0, uint32_t k1) {
+    if (!active) return;
+    if (deg <= 0) {
+      active = false;
+      return;
+    }
+    if ((s & 3) == 0)
+      rnd = philox4x32_10(make_uint4((uint32_t)u, w, (uint32_t)(s >> 2), 0u), k0, k1);
+    const uint32_t r = pick_word(rnd, s);
+    next_at = lo + (int64_t)(((uint64_t)r * (uint64_t)(uint32_t)deg) >> 32);
+  }
+  // Walk-table path: moves to the node of table entry e = {id, degree, row
+  // start lo, hi}, recording a pin landing, and carries the node's row.
+  __device__ void land_entry(const uint4& e, int64_t num_pins, int64_t num_nodes, int hops) {
+    land((int32_t)e.x, num_pins, num_nodes, hops);
+    deg = (int32_t)e.y;
+    lo = (int64_t)(((uint64_t)e.w << 32) | (uint64_t)e.z);
   }
   // Moves to node nxt (read from col[next_at]). Returns true when the walk
   // landed on a pin, with *visit the visit to record: the pin, or kEmpty

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 9
+    assert lib.pinsage_version() == 10
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -221,6 +221,21 @@ def test_profile_read_validation(L):
     assert lib.pinsage_profile_enable(0) == 0
     assert lib.pinsage_profile_read(0, ctypes.byref(n), ctypes.byref(ms)) == 0
     assert n.value == 0 and ms.value == 0.0
+
+
+def test_random_read_calibration_validation(L):
+    lib = L.lib()
+    E = L.PINSAGE_EINVAL
+    f = lib.pinsage_profile_random_reads
+    assert f(None, 1 << 20, 4, 8, FAKE, 256, None) == E
+    assert f(FAKE, 1 << 20, 4, 8, None, 256, None) == E
+    for eb in (0, 2, 12, 32):
+        assert f(FAKE, 1 << 20, eb, 8, FAKE, 256, None) == E
+    assert f(FAKE, 8, 16, 8, FAKE, 256, None) == E  # smaller than one element
+    assert f(FAKE, 1 << 20, 16, 0, FAKE, 256, None) == E
+    assert f(FAKE, 1 << 20, 16, 8, FAKE, 0, None) == E
+    assert f(FAKE, 1 << 20, 12, 8, FAKE, 256, None) == E
+    assert b"element size 12" in lib.pinsage_last_error()
 
 
 def test_minibatch_validation_and_workspace(L):
