@@ -280,27 +280,45 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
             k["achieved_TFLOPs"] = k["algo_flops_per_launch"] / (k["avg_ms"] * 1e-3) / 1e12
             k["frac_mfma"] = k["achieved_TFLOPs"] / peak_tf
     if "walk_topt" in kernels and walk_steps:
-        walk_rates(kernels["walk_topt"], per_launch("walk_topt", walk_steps), wl.offsets64)
+        walk_rates(kernels["walk_topt"], per_launch("walk_topt", walk_steps), wl.offsets64,
+                   table=kernels.get("walk_table", {}).get("launches", 0) > 0)
 
 
-# Each edge step of a walk reads the offset pair of its node and one neighbour
-# id at unrelated addresses: two random transactions of at least 64 bytes.
-WALK_TRANSACTION_BYTES = 128
+# Each edge step of a walk reading the CSR takes the offset pair of its node and
+# one neighbour id at unrelated addresses; with the walk table, one 16-byte
+# entry. A random read moves a 64-byte sector at most.
+WALK_SECTOR_BYTES = 64
+# Dependent random reads per second served from a 16 GiB table, 16-byte
+# elements, 0.5-4M chains in flight (pinsage_profile_random_reads, the
+# --random-read-calibration mode; 61.9-63.4 G/s on two boxes, see
+# profiles/random_read_calibration.md). Every edge step needs at least one such
+# read (the neighbour at a uniform position of the node's row), so this rate,
+# not HBM bytes, bounds the walks.
+RANDOM_READS_PER_S = 62.5e9
 
 
-def walk_rates(k, edge_steps_per_launch, offsets64):
-    """Rates of a walk kernel: algorithmic bytes (offset pair + one column id
-    per edge step) against the HBM peak, and the time two 64-byte random
-    transactions per edge step would take at that peak."""
+def walk_rates(k, edge_steps_per_launch, offsets64, table=False):
+    """Rates of a walk kernel: algorithmic bytes per edge step (the offset pair
+    and a column id, or one 16-byte walk-table entry) against the HBM peak;
+    the time the step's random reads would take as whole 64-byte sectors at
+    that peak (transaction floor); and the time one dependent random read per
+    step takes at the chip's measured random-read rate (random-read floor)."""
     off_b = 8 if offsets64 else 4
+    step_bytes = 16 if table else 2 * off_b + 4
+    reads_per_step = 1 if table else 2
+    k["walk_table"] = bool(table)
     k["edge_steps_per_launch"] = edge_steps_per_launch
-    k["algo_bytes_per_launch"] = edge_steps_per_launch * (2 * off_b + 4)
+    k["algo_bytes_per_launch"] = edge_steps_per_launch * step_bytes
     k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
     k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
     k["edge_steps_per_s"] = edge_steps_per_launch / (k["avg_ms"] * 1e-3)
-    floor_ms = edge_steps_per_launch * WALK_TRANSACTION_BYTES / (HBM_PEAK_GBS * 1e9) * 1e3
+    floor_ms = (edge_steps_per_launch * reads_per_step * WALK_SECTOR_BYTES
+                / (HBM_PEAK_GBS * 1e9) * 1e3)
     k["transaction_floor_ms"] = floor_ms
     k["frac_of_transaction_floor"] = floor_ms / k["avg_ms"]
+    rr_ms = edge_steps_per_launch / RANDOM_READS_PER_S * 1e3
+    k["random_read_floor_ms"] = rr_ms
+    k["frac_of_random_read_floor"] = rr_ms / k["avg_ms"]
 
 
 def roofline_of(kernels, wl):

@@ -134,3 +134,19 @@ def test_chained_transform_accounting():
     assert "gemm_q" not in k and "gemm_r" not in k
     assert not bench.chained_layer(_Layer(256, 512, 256, "pool_then_dense", torch.bfloat16))
     assert not bench.chained_layer(_Layer(1024, 2048, 512, "dense_then_pool", torch.bfloat16))
+
+
+def test_walk_rates_csr_and_table():
+    steps = 1e9
+    csr = {"avg_ms": 100.0}
+    bench.walk_rates(csr, steps, offsets64=True)
+    assert csr["algo_bytes_per_launch"] == steps * 20  # offset pair (2 x 8 B) + id
+    assert csr["transaction_floor_ms"] == pytest.approx(steps * 128 / 8e12 * 1e3)
+    tab = {"avg_ms": 100.0}
+    bench.walk_rates(tab, steps, offsets64=True, table=True)
+    assert tab["walk_table"] and not csr["walk_table"]
+    assert tab["algo_bytes_per_launch"] == steps * 16  # one table entry
+    assert tab["transaction_floor_ms"] == pytest.approx(steps * 64 / 8e12 * 1e3)
+    rr = steps / bench.RANDOM_READS_PER_S * 1e3
+    assert tab["random_read_floor_ms"] == pytest.approx(rr)
+    assert tab["frac_of_random_read_floor"] == pytest.approx(rr / 100.0)
