@@ -244,6 +244,14 @@ def chained_layer(L) -> bool:
             and L.d_out == 256 and L.m % 32 == 0 and 0 < L.m <= 2048)
 
 
+def fused_layer(L, T) -> bool:
+    """Layers whose pool and W run as one kernel in the library (dense then
+    pool, bf16, d_in = d_out = 256, T <= 64); timed as pool_w."""
+    import torch
+    return (L.dataflow == "dense_then_pool" and getattr(L, "dtype", None) == torch.bfloat16
+            and L.d_in == 256 and L.d_out == 256 and 1 <= T <= 64)
+
+
 def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_stored,
                   walk_steps, steps):
     """Algorithmic work per launch and achieved rates. A step's work of a kernel
@@ -259,12 +267,26 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
     # R = P W_n^T (dense then pool); the W GEMM then has K = d_in + m, resp. d_in.
     split = [L.dataflow == "dense_then_pool" for L in layers]
     width = [L.d_out if sp else L.m for L, sp in zip(layers, split)]
+    fused = [fused_layer(L, wl.T) for L in layers]
     if "pool" in kernels:
         k = kernels["pool"]
         k["algo_bytes_per_launch"] = per_launch(
-            "pool", sum(live_entries * w * esz + idx_bytes + N * w * esz for w in width))
+            "pool", sum(live_entries * w * esz + idx_bytes + N * w * esz
+                        for w, fu in zip(width, fused) if not fu))
         k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
         k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
+    if "pool_w" in kernels:
+        # Gathered rows, the neighbourhood table, the self rows and the output;
+        # the W_s product's flops beside them.
+        k = kernels["pool_w"]
+        k["algo_bytes_per_launch"] = per_launch(
+            "pool_w", sum(live_entries * L.d_out * esz + idx_bytes + N * L.d_in * esz
+                          + N * L.d_out * esz for L, fu in zip(layers, fused) if fu))
+        k["achieved_GBs"] = k["algo_bytes_per_launch"] / (k["avg_ms"] * 1e-3) / 1e9
+        k["frac_hbm"] = k["achieved_GBs"] / HBM_PEAK_GBS
+        k["algo_flops_per_launch"] = per_launch(
+            "pool_w", sum(2.0 * N * L.d_in * L.d_out for L, fu in zip(layers, fused) if fu))
+        k["achieved_TFLOPs"] = k["algo_flops_per_launch"] / (k["avg_ms"] * 1e-3) / 1e12
     chained = [chained_layer(L) for L in layers]
     for name, fl in (("gemm_q", sum(2.0 * n_transform * L.d_in * L.m
                                     for L, ch in zip(layers, chained) if not ch)),
@@ -273,7 +295,7 @@ def add_rooflines(kernels, wl, layers, N, n_transform, live_entries, weights_sto
                      ("gemm_qr", sum(2.0 * n_transform * (L.d_in * L.m + L.m * L.d_out)
                                      for L, ch in zip(layers, chained) if ch)),
                      ("gemm_w", sum(2.0 * N * (L.d_in + (0 if sp else L.m)) * L.d_out
-                                    for L, sp in zip(layers, split)))):
+                                    for L, sp, fu in zip(layers, split, fused) if not fu))):
         if name in kernels:
             k = kernels[name]
             k["algo_flops_per_launch"] = per_launch(name, fl)
@@ -328,7 +350,7 @@ def roofline_of(kernels, wl):
         return {"kernel": dominant, "bound": "mfma", "achieved": kd["achieved_TFLOPs"],
                 "peak": MFMA_PEAK_TFLOPS[wl.dtype], "unit": "TFLOP/s", "frac": kd["frac_mfma"],
                 "traffic": None}
-    src_file = {"pool": "pool.hip", "walk_topt": "walk.hip",
+    src_file = {"pool": "pool.hip", "pool_w": "poolw.hip", "walk_topt": "walk.hip",
                 "hard_neg": "hardneg.hip"}.get(dominant, "")
     tr = load_traffic(src_file, wl.name) if src_file else None
     frac = (kd["achieved_GBs"] / HBM_PEAK_GBS) if "achieved_GBs" in kd else None
@@ -415,7 +437,7 @@ def bench_embed_all(args, wl, inp):
                   walk_steps, args.steps)
     value = N * args.steps / elapsed
     layer_ms = sum(v["ms_per_step"] for k, v in kernels.items()
-                   if k in ("gemm_q", "gemm_r", "gemm_qr", "pool", "gemm_w"))
+                   if k in ("gemm_q", "gemm_r", "gemm_qr", "pool", "pool_w", "gemm_w"))
     extra = {"walk_steps_per_s": kernels.get("walk_topt", {}).get("edge_steps_per_s"),
              # N over the layer kernels' time alone (walks excluded), hipEvents;
              # only in the in-order schedule (overlapped launches share the chip).

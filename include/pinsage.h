@@ -454,7 +454,9 @@ enum {
   PINSAGE_KERNEL_GEMM_QR = 10,  /* Q transform chained into the neighbour half of
                                    W (DENSE_THEN_POOL, bf16, d_in = d_out = 256) */
   PINSAGE_KERNEL_WALK_TABLE = 11, /* the walk table of pinsage_embed_all's walks */
-  PINSAGE_KERNEL_COUNT = 12
+  PINSAGE_KERNEL_POOL_W = 12, /* pool and W fused (DENSE_THEN_POOL, bf16,
+                                 d_in = d_out = 256, top_t <= 64) */
+  PINSAGE_KERNEL_COUNT = 13
 };
 int pinsage_profile_enable(int on);
 int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);

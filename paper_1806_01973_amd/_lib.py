@@ -23,7 +23,8 @@ POOLS = {"importance": 0, "mean": 1, "max": 2}
 (KERNEL_WALK, KERNEL_GEMM_Q, KERNEL_POOL, KERNEL_GEMM_W, KERNEL_MINIBATCH, KERNEL_LOSS,
  KERNEL_GEMM_R, KERNEL_MLP) = range(8)
 KERNEL_NAMES = ["walk_topt", "gemm_q", "pool", "gemm_w", "minibatch", "loss", "gemm_r", "mlp",
-                "hard_neg", "graph_nbr", "gemm_qr", "walk_table"]
+                "hard_neg", "graph_nbr", "gemm_qr", "walk_table",
+                "pool_w"]
 
 EXPORTED = [
     "pinsage_version", "pinsage_status_string", "pinsage_last_error",

@@ -198,10 +198,13 @@ int check_nbr(const pinsage_neighborhoods_t* n, int64_t rows, const char* what) 
 //                    P chunk is replaced by two copies of the reordered W_n'
 //                    [d_out][m] (one per stream of the overlapped schedule);
 //                    P never exists.
+//   DENSE_THEN_POOL, bf16, d_in = d_out = 256: + W_s as product fragments for
+//                    the fused pool and W kernel (used when top_t <= 64; the
+//                    pooled chunk then stays unused).
 struct LayerWs {
-  size_t table = 0, pchunk = 0, pooled = 0;
+  size_t table = 0, pchunk = 0, pooled = 0, wsp = 0;
   bool chained = false;
-  size_t total() const { return table + pchunk + pooled; }
+  size_t total() const { return table + pchunk + pooled + wsp; }
 };
 
 bool chained_layer(const pinsage_layer_t* L) {
@@ -220,6 +223,8 @@ LayerWs layer_ws(const pinsage_layer_t* L, int64_t n_transform, int64_t n_out) {
     w.pchunk = w.chained ? 2 * align_up((size_t)L->d_out * L->m * es)
                          : align_up((size_t)tr_chunk * L->m * es);
     w.pooled = align_up((size_t)out_chunk * L->d_out * es);
+    if (pool_w_supported(L->d_in, L->d_out, L->dtype == PINSAGE_BF16, 1))
+      w.wsp = align_up(pool_w_ws_bytes());
   } else {
     w.table = align_up((size_t)n_transform * L->m * es);
     w.pooled = align_up((size_t)out_chunk * L->m * es);
@@ -351,6 +356,32 @@ int run_pool_dense(const pinsage_layer_t* L, const void* h_in, int64_t n_in,
   unsigned char* nbuf = table + lw.table + lw.pchunk;
   const int pool_width = split ? L->d_out : L->m;
   hipError_t e;
+  if (lw.wsp && pool_w_supported(L->d_in, L->d_out, bf16, nbr->top_t)) {
+    // Pool and W in one kernel over all rows: no pooled chunk, no separate GEMM.
+    unsigned char* wsp = nbuf + lw.pooled;
+    e = launch_permute_ws(L->W, (int64_t)L->d_in + L->m, wsp, s);
+    if (e != hipSuccess) return hip_fail(e, "W_s permute launch");
+    PoolWLaunch pw{};
+    pw.R = table;
+    pw.n_transform = n_transform;
+    pw.idx = nbr->idx;
+    pw.counts = nbr->counts;
+    pw.weights = nbr->weights;
+    pw.T = nbr->top_t;
+    pw.mode = (int)L->pool;
+    pw.H = h_in;
+    pw.self_rows = self_rows;
+    pw.h_row0 = 0;
+    pw.rows_h = n_in;
+    pw.ldh = L->d_in;
+    pw.Wsp = wsp;
+    pw.bias = L->w;
+    pw.out = h_out;
+    pw.rows = n_out;
+    e = launch_pool_w(pw, s);
+    if (e != hipSuccess) return hip_fail(e, "pool and W launch");
+    return PINSAGE_OK;
+  }
   for (int64_t r0 = 0; r0 < n_out; r0 += kChunkRows) {
     const int64_t rows = (n_out - r0) < kChunkRows ? (n_out - r0) : kChunkRows;
     const int T = nbr->top_t;

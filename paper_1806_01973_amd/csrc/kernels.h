@@ -10,7 +10,7 @@ namespace pinsage {
 // Kernel classes for per-launch timing; values match PINSAGE_KERNEL_*.
 enum KernelClass { kKWalk = 0, kKGemmQ = 1, kKPool = 2, kKGemmW = 3, kKMinibatch = 4, kKLoss = 5,
                    kKGemmR = 6, kKMlp = 7, kKHardNeg = 8, kKGraphNbr = 9, kKGemmQR = 10,
-                   kKWalkTable = 11, kKCount = 12 };
+                   kKWalkTable = 11, kKPoolW = 12, kKCount = 13 };
 
 // Records a start/stop hipEvent pair around a launch when timing is enabled.
 class ProfileScope {
@@ -125,6 +125,32 @@ struct PoolLaunch {
   int mode;  // PoolMode
 };
 hipError_t launch_pool(const PoolLaunch& a, hipStream_t s);
+
+// Pool and W fused (poolw.hip): out[r] = L2norm(ReLU(W_s h[self(r)] + pool(R, N(r))
+// + bias)) for bf16, d_in = d_out = 256, T <= 64. W_s arrives as fragments
+// from launch_permute_ws (pool_w_ws_bytes() of workspace).
+struct PoolWLaunch {
+  const void* R;           // [n_transform][256] rows to pool
+  int64_t n_transform;
+  const int32_t* idx;
+  const uint16_t* counts;
+  const float* weights;    // nullable: derived from counts
+  int T;
+  int mode;                // PoolMode
+  const void* H;           // self rows
+  const int32_t* self_rows;  // nullable: row r reads H row h_row0 + r
+  int64_t h_row0;
+  int64_t rows_h;
+  int64_t ldh;
+  const void* Wsp;
+  const float* bias;       // [256]
+  void* out;               // [rows][256]
+  int64_t rows;
+};
+bool pool_w_supported(int d_in, int d_out, bool bf16, int T);
+size_t pool_w_ws_bytes();
+hipError_t launch_permute_ws(const void* W, int64_t ldw, void* Wsp, hipStream_t s);
+hipError_t launch_pool_w(const PoolWLaunch& a, hipStream_t s);
 
 // C[r][c] = epilogue(sum_k A[r][k] * B[c][k] + bias[c] + addend[r][c]) where
 // the A row is the concatenation of A0[rowmap ? rowmap[r] : r][0:K0] and
