@@ -59,7 +59,7 @@ METRIC = "node embeddings/sec (K=2 layerwise, all nodes) + walk steps/sec, 1 MI3
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 2, "hardneg": 20,
+DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard": 5, "hardneg": 20,
                  "bipartite": 20}
 DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1, "hardneg": 3,
                   "bipartite": 3}
