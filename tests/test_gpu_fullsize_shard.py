@@ -5,12 +5,13 @@ configuration of the all-node job (inputs drawn on the GPU by
 synth.device_gen):
 
 * neighbourhood rows (ids and counts) bit-exact against the oracle for every
-  row of the last 4,194,304-row chunk of the layer driver, the 1,000 boards
-  of highest degree, and 1M random sources;
+  row of the last 4,194,304-row range (the last row chunk of the two-kernel
+  layer order), the 1,000 boards of highest degree, and 1M random sources;
 * the embeddings of 1,032 targets through the oracle's Algorithm 2 with
-  neighbourhoods walked on demand: 42 from each of the 24 row chunks of the
-  layer driver (including each chunk's first and last row) and the nodes 0
-  and N - 1, for both layer dataflows.
+  neighbourhoods walked on demand: 42 from each of the 24 ranges of
+  4,194,304 rows (including each range's first and last row) and the nodes 0
+  and N - 1, for both layer dataflows (the dense-then-pool order runs the
+  chained transform and the fused pool and W kernel).
 The whole table (24-29B edge steps) is beyond the oracle's time here, hence
 the samples; the other workloads are compared in full.
 """
@@ -26,7 +27,7 @@ from helpers import check_embeddings, to_f64
 
 pytestmark = pytest.mark.gpu
 
-CHUNK_ROWS = 1 << 22  # rows per pool + W pass of the layer driver
+CHUNK_ROWS = 1 << 22  # rows per pool + W pass of the two-kernel layer order
 
 
 def _log(m):
