@@ -372,15 +372,54 @@ constexpr int kGBins = 4096;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 
 __device__ __forceinline__ void table_add(uint32_t* keys, uint32_t* cnt, uint32_t mask,
-                                          int lg_cap, uint32_t v) {
+                                          int lg_cap, uint32_t v, uint32_t n = 1u) {
   uint32_t h = (v * 2654435761u) >> (32 - lg_cap);
   while (true) {
     const uint32_t k = atomicCAS(&keys[h], kNoKey, v);
     if (k == kNoKey || k == v) {
-      atomicAdd(&cnt[h], 1u);
+      atomicAdd(&cnt[h], n);
       return;
     }
     h = (h + 1) & mask;
+  }
+}
+
+// Visits first go to a small LDS table (kLCache slots, kLProbe probes): the
+// pins a query's walks land on most often are met early and stay there, so
+// their visits cost an LDS atomic instead of two in L2. A pin that finds no
+// slot goes to the global table; the LDS counts are added to it after the
+// walks, so every pin's total is exact whichever table held its visits.
+constexpr int kLgLCache = 12;
+constexpr int kLCache = 1 << kLgLCache;
+constexpr int kLProbe = 4;
+__device__ __forceinline__ void visit_add(uint32_t* lkeys, uint32_t* lcnt, uint32_t* keys,
+                                          uint32_t* cnt, uint32_t mask, int lg_cap, uint32_t v) {
+  uint32_t h = (v * 2654435761u) >> (32 - kLgLCache);
+#pragma unroll
+  for (int p = 0; p < kLProbe; ++p) {
+    const uint32_t k = atomicCAS(&lkeys[h], kNoKey, v);
+    if (k == kNoKey || k == v) {
+      atomicAdd(&lcnt[h], 1u);
+      return;
+    }
+    h = (h + 1) & (kLCache - 1);
+  }
+  table_add(keys, cnt, mask, lg_cap, v);
+}
+
+// hist[bin] += 1 for every lane with `on`: one LDS atomic per distinct bin of
+// the wave (the lanes sharing the lowest pending lane's bin are added at once).
+// Count histograms put most pins in a few bins, where per-lane atomics would
+// serialise. Called by whole waves.
+__device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t bin, bool on) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint64_t pending = __ballot(on);
+  while (pending) {
+    const int leader = __builtin_ctzll(pending);
+    const uint32_t b = __shfl(bin, leader);
+    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == b) & pending;
+    if (lane == leader) atomicAdd(&hist[b], (uint32_t)__builtin_popcountll(same));
+    pending &= ~same;
   }
 }
 
@@ -464,6 +503,13 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
       keys[i] = kNoKey;
       cnt[i] = 0u;
     }
+    // The LDS visit table lives in `top` until the ranking needs it.
+    uint32_t* lkeys = reinterpret_cast<uint32_t*>(top);
+    uint32_t* lcnt = lkeys + kLCache;
+    for (int i = tid; i < kLCache; i += kThreads) {
+      lkeys[i] = kNoKey;
+      lcnt[i] = 0u;
+    }
     if (tid < 8) sh_i32[tid] = 0;
     __syncthreads();
 
@@ -498,7 +544,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
           for (int i = 0; i < kWalkers; ++i) {
             uint32_t v;
             if (W[i].advance(nx[i], a.num_pins, a.num_nodes, a.hops, &v) && v != kEmpty)
-              table_add(keys, cnt, mask, lg_cap, v);
+              visit_add(lkeys, lcnt, keys, cnt, mask, lg_cap, v);
             any = any || W[i].active;
           }
         }
@@ -506,6 +552,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         for (int i = 0; i < kWalkers; ++i) my_steps += (uint32_t)W[i].s;
       }
     }
+    __syncthreads();
+    for (int i = tid; i < kLCache; i += kThreads)
+      if (lkeys[i] != kNoKey) table_add(keys, cnt, mask, lg_cap, lkeys[i], lcnt[i]);
     __syncthreads();
     // The table was updated by atomics in L2: drop this CU's cached copies.
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -515,11 +564,11 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     __syncthreads();
     {
       int nd = 0;
-      for (uint32_t i = tid; i < cap; i += kThreads) {
-        if (keys[i] == kNoKey) continue;
-        ++nd;
+      for (uint32_t i = tid; i < cap; i += kThreads) {  // cap is a multiple of kThreads
+        const bool on = keys[i] != kNoKey;
+        nd += on ? 1 : 0;
         const uint32_t c = cnt[i];
-        atomicAdd(&hist[(c >> 12) < kGBins ? (c >> 12) : kGBins - 1], 1u);
+        wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
       }
       atomicAdd(&sh_i32[0], nd);
     }
@@ -541,9 +590,8 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
       for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
       __syncthreads();
       for (uint32_t i = tid; i < cap; i += kThreads) {
-        if (keys[i] == kNoKey) continue;
         const uint32_t c = cnt[i];
-        if ((c >> 12) == b1) atomicAdd(&hist[c & (kGBins - 1)], 1u);
+        wave_hist_add(hist, c & (kGBins - 1), keys[i] != kNoKey && (c >> 12) == b1);
       }
       __syncthreads();
       if (tid == 0) {
