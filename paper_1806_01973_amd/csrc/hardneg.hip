@@ -350,14 +350,20 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
 }
 
 // ---------------------------------------------------------------------------
-// Walk budgets above the LDS slots (walks * hops > 16384): the visits of a
-// query are counted in a global open-addressing table (capacity a power of
-// two >= 2 walks * hops, so it is at most half full; Fibonacci hashing,
-// linear probing, claimed by atomicCAS, counted by atomicAdd at device scope:
-// the final (pin, count) multiset does not depend on the order of the walks).
-// One 1024-thread workgroup per query (grid-stride; each workgroup reuses its
-// own table). Only the first rank_hi ranks matter, so the ranking is a
-// selection, not a full sort:
+// Walk budgets above the LDS slots (walks * hops > 16384). One 1024-thread
+// workgroup per query (grid-stride; each workgroup reuses its own workspace):
+//   W. the walks write their landings to a buffer at slot walk * hops + hop,
+//      as the on-chip kernel does in LDS (empty marker for the query itself
+//      and for slots a walk did not reach): no atomics on the walks' path;
+//   C. the buffer is counted one hash partition of the pins at a time in an
+//      LDS table (12,288 slots; a partition holds about 8,192 landings, so at
+//      most two thirds of the slots when every landing is a distinct pin), and
+//      each partition's (pin, count) pairs are appended to a compact list; a
+//      pin that finds no slot within 64 linear probes marks its partition as
+//      overflowing, which is then split in two by a second hash and counted
+//      again (and so on: a part with fewer than 64 pins cannot overflow), so
+//      every count is exact;
+// then, as only the first rank_hi ranks matter, a selection over the list:
 //   1. count histogram (12-bit digits, two passes) -> the count c* of rank
 //      rank_hi - 1, the number n_above of pins counted more than c*;
 //   2. the pins counted more than c* (fewer than rank_hi) sorted by count
@@ -365,46 +371,37 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
 //   3. the rank_hi - n_above smallest ids counted exactly c*: radix select on
 //      the id (11 + 10 + 10 bits), gathered and sorted ascending;
 //   4. the draws as in the on-chip kernel.
-// With at most rank_hi distinct pins, all of them take step 2.
+// With at most rank_hi distinct pins, all of them take step 2. The list's
+// order depends on the atomics' order, the selection's results do not.
 // ---------------------------------------------------------------------------
 constexpr int kGMaxRank = 8192;  // rank_hi limit of this path
 constexpr int kGBins = 4096;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+constexpr int kCSlots = 12288;   // LDS counting table: keys then counts (96 KB)
+constexpr int kCPerPart = 8192;  // landings per hash partition
+constexpr int kCProbes = 64;     // linear probes before a partition counts as overflowing
+static_assert(kCSlots % kThreads == 0, "whole waves sweep the table");
+static_assert(2 * kCSlots * 4 >= kGMaxRank * 8 + kGMaxRank * 4, "top and cls fit the table");
 
-__device__ __forceinline__ void table_add(uint32_t* keys, uint32_t* cnt, uint32_t mask,
-                                          int lg_cap, uint32_t v, uint32_t n = 1u) {
-  uint32_t h = (v * 2654435761u) >> (32 - lg_cap);
-  while (true) {
-    const uint32_t k = atomicCAS(&keys[h], kNoKey, v);
-    if (k == kNoKey || k == v) {
-      atomicAdd(&cnt[h], n);
-      return;
-    }
-    h = (h + 1) & mask;
-  }
+// MurmurHash3's 32-bit finaliser (a bijection with good avalanche).
+__device__ __forceinline__ uint32_t fmix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x85ebca6bu;
+  x ^= x >> 13;
+  x *= 0xc2b2ae35u;
+  x ^= x >> 16;
+  return x;
 }
-
-// Visits first go to a small LDS table (kLCache slots, kLProbe probes): the
-// pins a query's walks land on most often are met early and stay there, so
-// their visits cost an LDS atomic instead of two in L2. A pin that finds no
-// slot goes to the global table; the LDS counts are added to it after the
-// walks, so every pin's total is exact whichever table held its visits.
-constexpr int kLgLCache = 12;
-constexpr int kLCache = 1 << kLgLCache;
-constexpr int kLProbe = 4;
-__device__ __forceinline__ void visit_add(uint32_t* lkeys, uint32_t* lcnt, uint32_t* keys,
-                                          uint32_t* cnt, uint32_t mask, int lg_cap, uint32_t v) {
-  uint32_t h = (v * 2654435761u) >> (32 - kLgLCache);
-#pragma unroll
-  for (int p = 0; p < kLProbe; ++p) {
-    const uint32_t k = atomicCAS(&lkeys[h], kNoKey, v);
-    if (k == kNoKey || k == v) {
-      atomicAdd(&lcnt[h], 1u);
-      return;
-    }
-    h = (h + 1) & (kLCache - 1);
-  }
-  table_add(keys, cnt, mask, lg_cap, v);
+// Partition of a pin among `parts`, its half in a split of `split` (a power of
+// two) and its home slot in the LDS table: three unrelated hashes of the id.
+__device__ __forceinline__ uint32_t part_of(uint32_t v, uint32_t parts) {
+  return (uint32_t)(((uint64_t)fmix32(v) * parts) >> 32);
+}
+__device__ __forceinline__ uint32_t split_of(uint32_t v, uint32_t split) {
+  return fmix32(v ^ 0x9e3779b9u) & (split - 1);
+}
+__device__ __forceinline__ uint32_t home_of(uint32_t v) {
+  return (uint32_t)(((uint64_t)fmix32(v + 0x7f4a7c15u) * kCSlots) >> 32);
 }
 
 // hist[bin] += 1 for every lane with `on`: one LDS atomic per distinct bin of
@@ -478,49 +475,43 @@ __device__ __forceinline__ void low_bin(const uint32_t* hist, int nbins, int64_t
 
 template <typename OffT>
 __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegLaunch a,
-                                                                        uint32_t* table,
-                                                                        int lg_cap) {
+                                                                        uint32_t* ws,
+                                                                        int64_t ws_words) {
   __shared__ uint32_t hist[kGBins];
-  __shared__ uint64_t top[kGMaxRank];  // pins counted more than c*: (~count << 32) | id
-  __shared__ uint32_t cls[kGMaxRank];  // the smallest ids counted exactly c*
+  // The counting table during step C; then top (pins counted more than c*:
+  // (~count << 32) | id) and cls (the smallest ids counted exactly c*).
+  __shared__ __attribute__((aligned(16))) uint32_t pool[2 * kCSlots];
   __shared__ int64_t sh_i64[4];
   __shared__ int sh_i32[8];
-  const uint32_t cap = 1u << lg_cap, mask = cap - 1;
-  uint32_t* keys = table + (size_t)blockIdx.x * 2 * cap;
-  uint32_t* cnt = keys + cap;
+  uint32_t* lkeys = pool;
+  uint32_t* lcnt = pool + kCSlots;
+  uint64_t* top = reinterpret_cast<uint64_t*>(pool);
+  uint32_t* cls = pool + 2 * kGMaxRank;
+  const int64_t L = (int64_t)a.walks * a.hops;
+  uint32_t* buf = ws + (int64_t)blockIdx.x * ws_words;  // L landings
+  uint32_t* list = buf + L;                             // up to L (pin, count) pairs
   const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
   const int32_t* __restrict__ col = a.col;
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
   const int tid = threadIdx.x;
   const int R = a.rank_hi;
+  const uint32_t parts = (uint32_t)((L + kCPerPart - 1) / kCPerPart);
   uint32_t my_steps = 0;
 
   for (int64_t qi = blockIdx.x; qi < a.num_queries; qi += gridDim.x) {
     const int64_t u = (int64_t)a.queries[qi];
     const bool live = u >= 0 && u < a.num_nodes;
-    for (uint32_t i = tid; i < cap; i += kThreads) {
-      keys[i] = kNoKey;
-      cnt[i] = 0u;
-    }
-    // The LDS visit table lives in `top` until the ranking needs it.
-    uint32_t* lkeys = reinterpret_cast<uint32_t*>(top);
-    uint32_t* lcnt = lkeys + kLCache;
-    for (int i = tid; i < kLCache; i += kThreads) {
-      lkeys[i] = kNoKey;
-      lcnt[i] = 0u;
-    }
     if (tid < 8) sh_i32[tid] = 0;
-    __syncthreads();
 
-    // ---- walks, visits counted in the table ------------------------------
+    // ---- W. walks, landings into the buffer ------------------------------
     if (live) {
       for (int w0 = tid; w0 < a.walks; w0 += kWalkers * kThreads) {
         Walker<OffT> W[kWalkers];
 #pragma unroll
         for (int i = 0; i < kWalkers; ++i) {
           const int w = w0 + i * kThreads;
-          W[i].start(u, w, nullptr, w < a.walks);
+          W[i].start(u, w, buf + (int64_t)w * a.hops, w < a.walks);
         }
         bool any = true;
         while (any) {
@@ -542,38 +533,100 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
           any = false;
 #pragma unroll
           for (int i = 0; i < kWalkers; ++i) {
-            uint32_t v;
-            if (W[i].advance(nx[i], a.num_pins, a.num_nodes, a.hops, &v) && v != kEmpty)
-              visit_add(lkeys, lcnt, keys, cnt, mask, lg_cap, v);
+            W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
             any = any || W[i].active;
           }
         }
 #pragma unroll
-        for (int i = 0; i < kWalkers; ++i) my_steps += (uint32_t)W[i].s;
+        for (int i = 0; i < kWalkers; ++i) my_steps += W[i].finish(a.hops);
       }
+    } else {
+      for (int64_t i = tid; i < L; i += kThreads) buf[i] = kEmpty;
     }
     __syncthreads();
-    for (int i = tid; i < kLCache; i += kThreads)
-      if (lkeys[i] != kNoKey) table_add(keys, cnt, mask, lg_cap, lkeys[i], lcnt[i]);
-    __syncthreads();
-    // The table was updated by atomics in L2: drop this CU's cached copies.
+    // The buffer was written through L2 by other waves: drop this CU's cached
+    // lines of it before reading.
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+    // ---- C. count by hash partition in LDS ----------------------------------
+    for (uint32_t p = 0; p < parts; ++p) {
+      const int list0 = sh_i32[0];
+      uint32_t split = 1;
+      for (uint32_t sp = 0; sp < split;) {
+        for (int i = tid; i < kCSlots; i += kThreads) {
+          lkeys[i] = kNoKey;
+          lcnt[i] = 0u;
+        }
+        if (tid == 0) sh_i32[1] = 0;
+        __syncthreads();
+        // Each thread keeps four 16-byte loads of the buffer in flight.
+        auto count = [&](uint32_t v) __attribute__((always_inline)) {
+          if (v == kEmpty || part_of(v, parts) != p || split_of(v, split) != sp) return;
+          uint32_t h = home_of(v);
+          for (int probe = 0; probe < kCProbes; ++probe) {
+            const uint32_t k = atomicCAS(&lkeys[h], kNoKey, v);
+            if (k == kNoKey || k == v) {
+              atomicAdd(&lcnt[h], 1u);
+              return;
+            }
+            h = h + 1 == (uint32_t)kCSlots ? 0u : h + 1;
+          }
+          sh_i32[1] = 1;  // overflow: split the partition
+        };
+        const int64_t L4 = L / 4;
+        const uint4* buf4 = reinterpret_cast<const uint4*>(buf);
+        for (int64_t i = tid; i < L4; i += 4 * kThreads) {
+          uint4 x[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t j = i + r * kThreads;
+            x[r] = j < L4 ? buf4[j] : make_uint4(kEmpty, kEmpty, kEmpty, kEmpty);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            count(x[r].x);
+            count(x[r].y);
+            count(x[r].z);
+            count(x[r].w);
+          }
+        }
+        for (int64_t i = 4 * L4 + tid; i < L; i += kThreads) count(buf[i]);
+        __syncthreads();
+        if (sh_i32[1]) {
+          // Too crowded: split further, count the partition again from its
+          // first part.
+          split *= 2;
+          sp = 0;
+          __syncthreads();
+          if (tid == 0) sh_i32[0] = list0;
+          __syncthreads();
+          continue;
+        }
+        for (int i = tid; i < kCSlots; i += kThreads) {
+          const uint32_t k = lkeys[i];
+          if (k != kNoKey) {
+            const int pos = atomicAdd(&sh_i32[0], 1);
+            list[2 * (int64_t)pos] = k;
+            list[2 * (int64_t)pos + 1] = lcnt[i];
+          }
+        }
+        __syncthreads();
+        ++sp;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const int D = sh_i32[0];
+    const int Dr = (D + kThreads - 1) / kThreads * kThreads;  // whole waves sweep the list
 
     // ---- 1. count threshold ----------------------------------------------
     for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
     __syncthreads();
-    {
-      int nd = 0;
-      for (uint32_t i = tid; i < cap; i += kThreads) {  // cap is a multiple of kThreads
-        const bool on = keys[i] != kNoKey;
-        nd += on ? 1 : 0;
-        const uint32_t c = cnt[i];
-        wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
-      }
-      atomicAdd(&sh_i32[0], nd);
+    for (int i = tid; i < Dr; i += kThreads) {
+      const bool on = i < D;
+      const uint32_t c = on ? list[2 * (int64_t)i + 1] : 0u;
+      wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
     }
     __syncthreads();
-    const int D = sh_i32[0];
     uint32_t cstar = 0;  // pins counted more than cstar are ranked by step 2
     int64_t n_above = D;
     if (D > R) {
@@ -589,9 +642,10 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
       const int64_t above1 = sh_i64[0];
       for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
       __syncthreads();
-      for (uint32_t i = tid; i < cap; i += kThreads) {
-        const uint32_t c = cnt[i];
-        wave_hist_add(hist, c & (kGBins - 1), keys[i] != kNoKey && (c >> 12) == b1);
+      for (int i = tid; i < Dr; i += kThreads) {
+        const bool in = i < D;
+        const uint32_t c = in ? list[2 * (int64_t)i + 1] : 0u;
+        wave_hist_add(hist, c & (kGBins - 1), in && (c >> 12) == b1);
       }
       __syncthreads();
       if (tid == 0) {
@@ -607,13 +661,11 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     }
 
     // ---- 2. pins counted more than c*, by count desc, id asc ---------------
-    for (uint32_t i = tid; i < cap; i += kThreads) {
-      const uint32_t k = keys[i];
-      if (k == kNoKey) continue;
-      const uint32_t c = cnt[i];
+    for (int i = tid; i < D; i += kThreads) {
+      const uint32_t c = list[2 * (int64_t)i + 1];
       if (c > cstar) {
         const int slot = atomicAdd(&sh_i32[3], 1);
-        top[slot] = ((uint64_t)(~c) << 32) | k;
+        top[slot] = ((uint64_t)(~c) << 32) | list[2 * (int64_t)i];
       }
     }
     __syncthreads();
@@ -638,9 +690,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         const uint32_t hi_mask = pass == 0 ? 0u : (0xFFFFFFFFu << (sft + widths[pass]));
         for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
         __syncthreads();
-        for (uint32_t i = tid; i < cap; i += kThreads) {
-          const uint32_t k = keys[i];
-          if (k == kNoKey || cnt[i] != cstar || (k & hi_mask) != prefix) continue;
+        for (int i = tid; i < D; i += kThreads) {
+          const uint32_t k = list[2 * (int64_t)i];
+          if (list[2 * (int64_t)i + 1] != cstar || (k & hi_mask) != prefix) continue;
           atomicAdd(&hist[(k >> sft) & (nb - 1)], 1u);
         }
         __syncthreads();
@@ -657,9 +709,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         __syncthreads();
       }
       // prefix is the need-th smallest id of the class: gather ids <= prefix.
-      for (uint32_t i = tid; i < cap; i += kThreads) {
-        const uint32_t k = keys[i];
-        if (k == kNoKey || cnt[i] != cstar || k > prefix) continue;
+      for (int i = tid; i < D; i += kThreads) {
+        const uint32_t k = list[2 * (int64_t)i];
+        if (list[2 * (int64_t)i + 1] != cstar || k > prefix) continue;
         cls[atomicAdd(&sh_i32[5], 1)] = k;
       }
       __syncthreads();
@@ -682,14 +734,14 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
       }
       outq[j] = v;
     }
-    __syncthreads();  // the table and LDS are reused by the next query
+    __syncthreads();  // the buffer, the list and LDS are reused by the next query
   }
 
   if (a.total_steps) {
     const int wave = tid >> 6, lane = tid & (kWave - 1);
-    const int ws = wave_sum_i32((int)my_steps);
+    const int ws_sum = wave_sum_i32((int)my_steps);
     __shared__ int wave_tot[kWaves];
-    if (lane == 0) wave_tot[wave] = ws;
+    if (lane == 0) wave_tot[wave] = ws_sum;
     __syncthreads();
     if (tid == 0) {
       unsigned long long t = 0;
@@ -716,19 +768,19 @@ hipError_t launch_for_offsets(const HardNegLaunch& a, hipStream_t s) {
 
 }  // namespace
 
-int hard_negative_table_lg(int64_t landings) {
-  int lg = 1;
-  while ((1ll << lg) < 2 * landings) ++lg;
-  return lg;
-}
-
 int64_t hard_negative_blocks(int64_t num_queries) {
   return num_queries < kGMaxBlocks ? num_queries : kGMaxBlocks;
 }
 
+// Per resident workgroup: the landing buffer (L words) and the (pin, count)
+// list (2 L words), rounded to 256 bytes.
+static int64_t hard_negative_ws_words(int64_t landings) {
+  return (3 * landings + 63) / 64 * 64;
+}
+
 size_t hard_negative_workspace(int64_t landings, int64_t num_queries) {
   if (landings <= kMaxOnChipLandings || num_queries <= 0) return 0;
-  return (size_t)hard_negative_blocks(num_queries) * 2 * ((size_t)1 << hard_negative_table_lg(landings)) *
+  return (size_t)hard_negative_blocks(num_queries) * (size_t)hard_negative_ws_words(landings) *
          sizeof(uint32_t);
 }
 
@@ -738,13 +790,13 @@ hipError_t launch_hard_negatives(const HardNegLaunch& a, void* workspace, hipStr
   const int64_t landings = (int64_t)a.walks * a.hops;
   if (landings <= kMaxOnChipLandings)
     return a.offsets64 ? launch_for_offsets<int64_t>(a, s) : launch_for_offsets<int32_t>(a, s);
-  const int lg = hard_negative_table_lg(landings);
   const dim3 grid((unsigned)hard_negative_blocks(a.num_queries)), block(kThreads);
-  uint32_t* table = static_cast<uint32_t*>(workspace);
+  uint32_t* ws = static_cast<uint32_t*>(workspace);
+  const int64_t words = hard_negative_ws_words(landings);
   if (a.offsets64)
-    hipLaunchKernelGGL(hard_negative_global_kernel<int64_t>, grid, block, 0, s, a, table, lg);
+    hipLaunchKernelGGL(hard_negative_global_kernel<int64_t>, grid, block, 0, s, a, ws, words);
   else
-    hipLaunchKernelGGL(hard_negative_global_kernel<int32_t>, grid, block, 0, s, a, table, lg);
+    hipLaunchKernelGGL(hard_negative_global_kernel<int32_t>, grid, block, 0, s, a, ws, words);
   return hipGetLastError();
 }
 

@@ -73,9 +73,10 @@ struct HardNegLaunch {
   int32_t* out;
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
 };
-// Walk budgets above kMaxOnChipLandings count visits in a global table of the
-// workspace (hard_negative_workspace bytes; one table per resident workgroup)
-// and need rank_hi <= kMaxGlobalRank.
+// Walk budgets above kMaxOnChipLandings buffer a query's landings in the
+// workspace and count them in LDS by hash partition (hard_negative_workspace
+// bytes: landing buffer and (pin, count) list per resident workgroup), and
+// need rank_hi <= kMaxGlobalRank.
 constexpr int64_t kMaxOnChipLandings = 16384;
 constexpr int64_t kMaxLandings = 1ll << 22;
 constexpr int kMaxGlobalRank = 8192;

@@ -166,3 +166,35 @@ def test_global_table_int64_offsets(orc, tiny):
                   offsets64=True)
     np.testing.assert_array_equal(got, orc.hard_negatives(off, col, wl.num_pins, 8, 9000, 3, q,
                                                           50, 700, 4))
+
+
+def _fmix32(x):
+    # MurmurHash3's 32-bit finaliser, as the kernel partitions pins by it.
+    x ^= x >> 16
+    x = (x * 0x85EBCA6B) & 0xFFFFFFFF
+    x ^= x >> 13
+    x = (x * 0xC2B2AE35) & 0xFFFFFFFF
+    x ^= x >> 16
+    return x
+
+
+def test_global_table_partition_split(orc):
+    # One board joined to 30,000 pins that all fall in the first of the three
+    # hash partitions of 4096 walks x 5 landings: about 15,000 distinct pins in
+    # one partition, more than the 12,288 LDS slots, so the kernel splits it by
+    # its second hash and counts each part again. The ranking must still equal
+    # the oracle's.
+    walks, hops = 4096, 5
+    parts = (walks * hops + 8191) // 8192
+    chosen = [v for v in range(1, 400_000) if (_fmix32(v) * parts) >> 32 == 0][:30_000]
+    P = chosen[-1] + 1
+    edges = [(0, 0)] + [(v, 0) for v in chosen]
+    off, col = synth.csr_from_edges(P, 1, edges)
+    q = np.array([0, chosen[7], chosen[123]], np.int32)
+    lo, hi, k = 100, 8000, 16
+    print(f"[case] hard negatives, partition split P={P} pins={len(chosen)}", flush=True)
+    got, steps = _gpu(off, col, P, 1, q, k, 21, walks, hops, lo, hi)
+    np.testing.assert_array_equal(got, orc.hard_negatives(off, col, P, 21, walks, hops, q,
+                                                          lo, hi, k))
+    visits = orc.walk_visits(off, col, P, 21, 0, walks, hops)[0]
+    assert len(np.unique(visits[(visits >= 0) & (visits != 0)])) > 12_288
