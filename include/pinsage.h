@@ -208,9 +208,9 @@ typedef struct {
 
 /* Workspace bytes pinsage_hard_negatives needs for these parameters and
  * query count: 0 for walks * hops <= 16384 (the visits of a query are counted
- * on chip); above that, per resident workgroup (at most 256), a buffer of the
- * query's landings and a list of its (pin, count) pairs: 12 bytes per landing,
- * rounded up to 256 bytes. Errors as for pinsage_hard_negatives' parameters. */
+ * on chip); above that, per resident workgroup (at most 256), the query's
+ * landings twice (by walk, then by hash partition) and a list of its
+ * (pin, count) pairs: 16 bytes per landing, rounded up to 256 bytes. Errors as for pinsage_hard_negatives' parameters. */
 int pinsage_hard_negatives_workspace_size(const pinsage_hard_negative_params_t* params,
                                           int64_t num_queries, size_t* bytes);
 

@@ -355,10 +355,13 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
 //   W. the walks write their landings to a buffer at slot walk * hops + hop,
 //      as the on-chip kernel does in LDS (empty marker for the query itself
 //      and for slots a walk did not reach): no atomics on the walks' path;
-//   C. the buffer is counted one hash partition of the pins at a time in an
-//      LDS table (12,288 slots; a partition holds about 8,192 landings, so at
-//      most two thirds of the slots when every landing is a distinct pin), and
-//      each partition's (pin, count) pairs are appended to a compact list; a
+//   B. the landings are bucketed by hash partition of the pin (a histogram
+//      sweep and a scatter sweep of the buffer, one LDS atomic per distinct
+//      partition of a wave);
+//   C. each bucket is counted in an LDS table (12,288 slots; a partition holds
+//      about 8,192 landings, so at most two thirds of the slots when every
+//      landing is a distinct pin), and each partition's (pin, count) pairs
+//      are appended to a compact list; a
 //      pin that finds no slot within 64 linear probes marks its partition as
 //      overflowing, which is then split in two by a second hash and counted
 //      again (and so on: a part with fewer than 64 pins cannot overflow), so
@@ -380,6 +383,7 @@ constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 constexpr int kCSlots = 12288;   // LDS counting table: keys then counts (96 KB)
 constexpr int kCPerPart = 8192;  // landings per hash partition
 constexpr int kCProbes = 64;     // linear probes before a partition counts as overflowing
+constexpr int kMaxParts = 512;   // partitions of the largest budget (2^22 landings)
 static_assert(kCSlots % kThreads == 0, "whole waves sweep the table");
 static_assert(2 * kCSlots * 4 >= kGMaxRank * 8 + kGMaxRank * 4, "top and cls fit the table");
 
@@ -418,6 +422,27 @@ __device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t bin, bool
     if (lane == leader) atomicAdd(&hist[b], (uint32_t)__builtin_popcountll(same));
     pending &= ~same;
   }
+}
+
+// Slot in bucket `bin` (cursor[bin] counts the bucket's entries so far) for
+// every lane with `on`: one LDS atomic per distinct bin of the wave, the lanes
+// of a bin taking consecutive slots in lane order. Called by whole waves.
+__device__ __forceinline__ uint32_t wave_bucket_slot(uint32_t* cursor, uint32_t bin, bool on) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint64_t pending = __ballot(on);
+  uint32_t slot = 0;
+  while (pending) {
+    const int leader = __builtin_ctzll(pending);
+    const uint32_t b = __shfl(bin, leader);
+    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == b) & pending;
+    uint32_t base = 0;
+    if (lane == leader) base = atomicAdd(&cursor[b], (uint32_t)__builtin_popcountll(same));
+    base = __shfl(base, leader);
+    if ((same >> lane) & 1ull)
+      slot = base + (uint32_t)__builtin_popcountll(same & ((1ull << lane) - 1ull));
+    pending &= ~same;
+  }
+  return slot;
 }
 
 // Ascending bitonic sort of v[0, n), n a power of two <= 2 * 1024 * 4.
@@ -488,15 +513,17 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
   uint64_t* top = reinterpret_cast<uint64_t*>(pool);
   uint32_t* cls = pool + 2 * kGMaxRank;
   const int64_t L = (int64_t)a.walks * a.hops;
-  uint32_t* buf = ws + (int64_t)blockIdx.x * ws_words;  // L landings
-  uint32_t* list = buf + L;                             // up to L (pin, count) pairs
+  uint32_t* buf = ws + (int64_t)blockIdx.x * ws_words;  // L landings, by (walk, hop)
+  uint32_t* sorted = buf + L;                           // the landings, by partition
+  uint32_t* list = sorted + L;                          // up to L (pin, count) pairs
   const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
   const int32_t* __restrict__ col = a.col;
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
   const int tid = threadIdx.x;
   const int R = a.rank_hi;
-  const uint32_t parts = (uint32_t)((L + kCPerPart - 1) / kCPerPart);
+  const uint32_t parts = (uint32_t)((L + kCPerPart - 1) / kCPerPart);  // <= kMaxParts
+  __shared__ uint32_t pstart[kMaxParts + 1];
   uint32_t my_steps = 0;
 
   for (int64_t qi = blockIdx.x; qi < a.num_queries; qi += gridDim.x) {
@@ -548,9 +575,51 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     // lines of it before reading.
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-    // ---- C. count by hash partition in LDS ----------------------------------
+    // ---- B. bucket the landings by partition --------------------------------
+    // Whole waves sweep the buffer in 16-byte vectors (L4 rounded up to whole
+    // blocks; the tail of L past the last full vector is swept as scalars).
+    const int64_t L4 = L / 4;
+    const int64_t L4r = (L4 + kThreads - 1) / kThreads * kThreads;
+    const uint4* buf4 = reinterpret_cast<const uint4*>(buf);
+    auto sweep = [&](auto&& visit) __attribute__((always_inline)) {
+      for (int64_t i = tid; i < L4r; i += kThreads) {
+        const uint4 x = i < L4 ? buf4[i] : make_uint4(kEmpty, kEmpty, kEmpty, kEmpty);
+        visit(x.x);
+        visit(x.y);
+        visit(x.z);
+        visit(x.w);
+      }
+      for (int64_t i = 4 * L4 + tid; i < 4 * L4 + kThreads; i += kThreads)
+        visit(i < L ? buf[i] : kEmpty);
+    };
+    for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+    __syncthreads();
+    sweep([&](uint32_t v) {
+      wave_hist_add(hist, v == kEmpty ? 0u : part_of(v, parts), v != kEmpty);
+    });
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t run = 0;
+      for (uint32_t p = 0; p < parts; ++p) {
+        pstart[p] = run;
+        run += hist[p];
+        hist[p] = pstart[p];  // the bucket's cursor
+      }
+      pstart[parts] = run;
+    }
+    __syncthreads();
+    sweep([&](uint32_t v) {
+      const uint32_t b = v == kEmpty ? 0u : part_of(v, parts);
+      const uint32_t slot = wave_bucket_slot(hist, b, v != kEmpty);
+      if (v != kEmpty) sorted[slot] = v;
+    });
+    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+    // ---- C. count each partition's bucket in LDS ----------------------------
     for (uint32_t p = 0; p < parts; ++p) {
       const int list0 = sh_i32[0];
+      const int64_t b0 = pstart[p], b1 = pstart[p + 1];
       uint32_t split = 1;
       for (uint32_t sp = 0; sp < split;) {
         for (int i = tid; i < kCSlots; i += kThreads) {
@@ -559,38 +628,22 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         }
         if (tid == 0) sh_i32[1] = 0;
         __syncthreads();
-        // Each thread keeps four 16-byte loads of the buffer in flight.
-        auto count = [&](uint32_t v) __attribute__((always_inline)) {
-          if (v == kEmpty || part_of(v, parts) != p || split_of(v, split) != sp) return;
+        for (int64_t i = b0 + tid; i < b1; i += kThreads) {
+          const uint32_t v = sorted[i];
+          if (split_of(v, split) != sp) continue;
           uint32_t h = home_of(v);
+          bool placed = false;
           for (int probe = 0; probe < kCProbes; ++probe) {
             const uint32_t k = atomicCAS(&lkeys[h], kNoKey, v);
             if (k == kNoKey || k == v) {
               atomicAdd(&lcnt[h], 1u);
-              return;
+              placed = true;
+              break;
             }
             h = h + 1 == (uint32_t)kCSlots ? 0u : h + 1;
           }
-          sh_i32[1] = 1;  // overflow: split the partition
-        };
-        const int64_t L4 = L / 4;
-        const uint4* buf4 = reinterpret_cast<const uint4*>(buf);
-        for (int64_t i = tid; i < L4; i += 4 * kThreads) {
-          uint4 x[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int64_t j = i + r * kThreads;
-            x[r] = j < L4 ? buf4[j] : make_uint4(kEmpty, kEmpty, kEmpty, kEmpty);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            count(x[r].x);
-            count(x[r].y);
-            count(x[r].z);
-            count(x[r].w);
-          }
+          if (!placed) sh_i32[1] = 1;  // overflow: split the partition
         }
-        for (int64_t i = 4 * L4 + tid; i < L; i += kThreads) count(buf[i]);
         __syncthreads();
         if (sh_i32[1]) {
           // Too crowded: split further, count the partition again from its
@@ -772,10 +825,11 @@ int64_t hard_negative_blocks(int64_t num_queries) {
   return num_queries < kGMaxBlocks ? num_queries : kGMaxBlocks;
 }
 
-// Per resident workgroup: the landing buffer (L words) and the (pin, count)
-// list (2 L words), rounded to 256 bytes.
+// Per resident workgroup: the landing buffer (L words), the landings by
+// partition (L words) and the (pin, count) list (2 L words), rounded to 256
+// bytes.
 static int64_t hard_negative_ws_words(int64_t landings) {
-  return (3 * landings + 63) / 64 * 64;
+  return (4 * landings + 63) / 64 * 64;
 }
 
 size_t hard_negative_workspace(int64_t landings, int64_t num_queries) {

@@ -74,8 +74,9 @@ struct HardNegLaunch {
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
 };
 // Walk budgets above kMaxOnChipLandings buffer a query's landings in the
-// workspace and count them in LDS by hash partition (hard_negative_workspace
-// bytes: landing buffer and (pin, count) list per resident workgroup), and
+// workspace, bucket them by hash partition and count each bucket in LDS
+// (hard_negative_workspace bytes: the landings twice and a (pin, count) list
+// per resident workgroup), and
 // need rank_hi <= kMaxGlobalRank.
 constexpr int64_t kMaxOnChipLandings = 16384;
 constexpr int64_t kMaxLandings = 1ll << 22;
