@@ -64,8 +64,10 @@ DEFAULT_STEPS = {"tiny": 20, "medium": 20, "minibatch": 20, "large": 4, "shard":
 DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1, "hardneg": 3,
                   "bipartite": 3}
 # Hard negative workload: queries per step, walks and landings per query, the
-# rank window [lo, hi) (ranks 2000-5000 counted from 1).
-HN_QUERIES, HN_WALKS, HN_HOPS, HN_LO, HN_HI = 2048, 4096, 4, 1999, 5000
+# rank window [lo, hi) (ranks 2000-5000 counted from 1). At 32,768 x 4
+# landings the window is decided by visit counts (at 4,096 x 4, the LDS
+# kernel's budget, it falls among pins visited once).
+HN_QUERIES, HN_WALKS, HN_HOPS, HN_LO, HN_HI = 2048, 32768, 4, 1999, 5000
 DEVICE_GENERATED = ("large", "shard")
 
 
