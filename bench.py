@@ -27,11 +27,12 @@ Other workloads (measurement of the other rows; not the headline):
                                     2 layers over all nodes, featureless boards
   --workload hardneg                one step = hard negative items (Sec. 3.3)
                                     for 2,048 query pins of the 1.2M-node
-                                    graph: 4096 walks x 4 landings each
-                                    (--hn-walks, --hn-hops; budgets above
-                                    16,384 landings count visits in a global
-                                    table), ranks 2000-5000, --hard-neg draws
-                                    per query
+                                    graph: 32768 walks x 4 landings each
+                                    (--hn-walks, --hn-hops; budgets up to
+                                    16,384 landings count visits in LDS,
+                                    larger ones buffer the landings and count
+                                    them by hash partition), ranks 2000-5000,
+                                    --hard-neg draws per query
 
 Prints one JSON line: throughput of the whole step, walk steps/s, per-kernel
 times from hipEvents recorded around every launch in the timed region, the
@@ -68,6 +69,8 @@ DEFAULT_WARMUP = {"tiny": 3, "medium": 3, "minibatch": 3, "large": 1, "shard": 1
 # landings the window is decided by visit counts (at 4,096 x 4, the LDS
 # kernel's budget, it falls among pins visited once).
 HN_QUERIES, HN_WALKS, HN_HOPS, HN_LO, HN_HI = 2048, 32768, 4, 1999, 5000
+# Hard negatives mined inside the minibatch step (--hard-neg): walks per pair.
+MB_HN_WALKS = 4096
 DEVICE_GENERATED = ("large", "shard")
 
 
@@ -587,7 +590,7 @@ def bench_minibatch(args, wl, inp):
     def run(i):
         q, p, n = dev[i]
         if k:  # Sec. 3.3: the queries' hard negatives join their negative sets
-            ps.hard_negatives(inp["g"], q, k, wl.seed + 1, HN_WALKS, HN_HOPS, HN_LO, HN_HI,
+            ps.hard_negatives(inp["g"], q, k, wl.seed + 1, MB_HN_WALKS, HN_HOPS, HN_LO, HN_HI,
                               out=hard, stream=stream)
         mb.run(inp["x"], q, p, n, 0.1, want_z=False, hard=hard, stream=stream)
         sizes.append(mb.sizes())
@@ -630,7 +633,7 @@ def cpu_baseline_minibatch(inp, wl, threads, k=0):
     hard = valid = None
     if k:
         hard = oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins,
-                                     wl.seed + 1, HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k,
+                                     wl.seed + 1, MB_HN_WALKS, HN_HOPS, q, HN_LO, HN_HI, k,
                                      nthreads=threads)
         valid = hard >= 0
     t_hard = time.perf_counter() - t_hard
@@ -691,12 +694,13 @@ def bench_hard_negatives(args, wl, inp):
 
 
 def cpu_baseline_hard_negatives(inp, wl, threads, k, walks=HN_WALKS, hops=HN_HOPS):
-    """The oracle's hard negatives for a sample of query pins (16,384, i.e. eight
-    steps' worth, at the default budget; proportionally fewer at larger ones)."""
+    """The oracle's hard negatives for a sample of query pins (16,384 at 4,096 x 4
+    landings per query; proportionally fewer at larger budgets: 2,048, one
+    step's worth, at the default 32,768 x 4)."""
     import numpy as np
     import oracle
     rng = np.random.default_rng(10_000)
-    nq = max(256, 16_384 * HN_WALKS * HN_HOPS // (walks * hops))
+    nq = max(256, 16_384 * 4096 * 4 // (walks * hops))
     q = rng.integers(0, wl.num_pins, nq).astype(np.int32)
     t0 = time.perf_counter()
     oracle.hard_negatives(inp["host"]["offsets"], inp["host"]["col"], wl.num_pins, wl.seed + 1,
