@@ -253,3 +253,41 @@ def test_output_mlp(orc, dtype, dims, n):
     torch.cuda.synchronize()
     ref = orc.output_mlp(h, P["G1"], P["g"], P["G2"])
     check_embeddings(to_f64(z), ref, dtype, f"mlp {dtype} {dims}")
+
+
+@pytest.mark.parametrize("T,n_out", [(1, 31), (64, 33), (64, 1_000), (65, 97), (50, 32)])
+@pytest.mark.parametrize("stored", [True, False])
+def test_fused_pool_w_edges(orc, T, n_out, stored):
+    # The fused pool and W kernel (bf16, d_in = d_out = 256, dense then pool)
+    # at its limits: one slot, the full 64 slots (T = 65 falls back to the
+    # two-kernel order), row groups of 32 with a ragged last group, rows whose
+    # slots are all empty, weights stored or derived from counts.
+    import paper_1806_01973_amd as ps
+    rng = np.random.default_rng(T * 1000 + n_out)
+    d_in, m, d_out = 256, 512, 256
+    n_transform = 700
+    n_in = n_transform + n_out + 57  # the first n_transform rows are the pins
+    print(f"[case] fused pool and W T={T} n_out={n_out} stored={stored}", flush=True)
+    h = synth.bf16_round(rng.standard_normal((n_in, d_in)).astype(np.float32))
+    wl = synth.Workload("layer", 1, 1, "uniform8", 0, 8, None, d_in, m, d_out, 1, 1, 1, T,
+                        "bf16", 5)
+    layer = synth.make_layers(wl)[0]
+    idx, counts, weights = synth.random_neighborhoods(n_out, n_transform, T, seed=T + n_out)
+    idx[::7] = -1  # every seventh row has no neighbour at all
+    self_rows = rng.integers(0, n_in, size=n_out).astype(np.int32)
+    dev = ps.DeviceLayer(layer["Q"], layer["q"], layer["W"], layer["w"], dtype=torch.bfloat16,
+                         dataflow="dense_then_pool")
+    nb = ps.Neighborhoods(torch.as_tensor(idx).cuda(), torch.as_tensor(counts).cuda(),
+                          torch.as_tensor(weights).cuda() if stored else None)
+    out = ps.convolve_layer(dev, torch.as_tensor(h).to(device="cuda", dtype=torch.bfloat16),
+                            n_transform, nb, self_rows=torch.as_tensor(self_rows).cuda())
+    torch.cuda.synchronize()
+    if stored:
+        w_ref = weights
+    else:  # alpha = count / (sum of the row's counts), every slot counted
+        s = counts.astype(np.float64).sum(axis=1, keepdims=True)
+        w_ref = np.where(s > 0, counts / np.maximum(s, 1), 0.0).astype(np.float32)
+        w_ref = np.where(idx >= 0, w_ref, 0.0).astype(np.float32)
+    ref = orc.convolve_layer(h, n_transform, layer["Q"], layer["q"], layer["W"], layer["w"], idx,
+                             w_ref, self_rows=self_rows)
+    check_embeddings(to_f64(out), ref, "bf16", f"fused T={T} n={n_out} stored={stored}")
