@@ -121,6 +121,31 @@ def copy_calibration(gib: float = 1.0, reps: int = 5) -> None:
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
 
 
+def host_cpu() -> dict:
+    """The host CPU the oracle ran on: model, logical CPUs, physical cores."""
+    model, phys = None, set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            pid = core = None
+            for line in f:
+                key, _, val = line.partition(":")
+                key, val = key.strip(), val.strip()
+                if key == "model name" and model is None:
+                    model = val
+                elif key == "physical id":
+                    pid = val
+                elif key == "core id":
+                    core = val
+                elif not key and pid is not None and core is not None:
+                    phys.add((pid, core))
+                    pid = core = None
+            if pid is not None and core is not None:
+                phys.add((pid, core))
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count(), "physical_cores": len(phys) or None}
+
+
 def random_read_calibration(table_gib: int = 16, steps: int = 32, reps: int = 3) -> None:
     """Dependent random reads per second (the library's calibration kernel):
     4-, 8- and 16-byte elements from a table_gib table, and 16-byte elements
@@ -919,6 +944,7 @@ def main() -> int:
                                                             args.hard_neg or 0)
         else:
             result["cpu_baseline"] = cpu_baseline_embed(inp, wl, threads)
+        result["cpu_baseline"]["host"] = host_cpu()
     print(json.dumps(result), flush=True)
     return 0
 
