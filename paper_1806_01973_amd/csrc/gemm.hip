@@ -408,6 +408,19 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
     }
   };
 
+  // bf16 L2 tiles too large to stage whole (512 columns): one row band at a
+  // time through the free stage ring, so the addend arrives and the output
+  // leaves as whole 16-byte row pieces (consecutive lanes, consecutive
+  // pieces of a row) instead of 8-byte pieces of 32 rows per instruction.
+  // Band i is row band i of every wave: tile rows WM wm' + 32 i + (0..31) for
+  // each wm'; band row b <-> tile row WM (b / 32) + 32 i + b % 32.
+  constexpr bool kBandLds = C::kBf16 && C::L2 && !kStaged;
+  constexpr int BROWS = 32 * C::WAVES_M;
+  static_assert(!kBandLds || BROWS * TROW <= STAGES * C::STAGE_BYTES, "a band fits the ring");
+  auto band_row = [&](int i, int b) __attribute__((always_inline)) {
+    return (b >> 5) * C::WM + 32 * i + (b & 31);
+  };
+
   if constexpr (!C::L2) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -415,6 +428,78 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(GemmLaunch a) {
       store_band(i, 1.0f);
     }
     flush_tile();
+  } else if constexpr (kBandLds) {
+    const int b_lane = wm * 32 + row_in_blk;  // this lane's row within a band
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      // The band's addend rows into LDS (rows past M read as zeros).
+      if (a.addend) {
+#pragma unroll 4
+        for (int e = tid; e < BROWS * PER_ROW; e += THREADS) {
+          const int b = e / PER_ROW, ck = e % PER_ROW;
+          const int64_t r = m0 + band_row(i, b);
+          const int c = n0 + 8 * ck;
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (r < a.M && c < a.N)
+            v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.addend) + r * a.N + c);
+          *reinterpret_cast<uint4*>(smem + b * TROW + 16 * ck) = v;
+        }
+      }
+      __syncthreads();
+      // + bias + addend, ReLU, and the row's partial sum of squares.
+      float s = 0.0f;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float4 bv = *reinterpret_cast<const float4*>(bias_s + c0(j, g));
+          float x[4] = {acc[i][j][4 * g + 0] + bv.x, acc[i][j][4 * g + 1] + bv.y,
+                        acc[i][j][4 * g + 2] + bv.z, acc[i][j][4 * g + 3] + bv.w};
+          if (a.addend) {
+            const uint2 v = *reinterpret_cast<const uint2*>(smem + b_lane * TROW + c0(j, g) * 2);
+            x[0] += __uint_as_float(v.x << 16);
+            x[1] += __uint_as_float(v.x & 0xFFFF0000u);
+            x[2] += __uint_as_float(v.y << 16);
+            x[3] += __uint_as_float(v.y & 0xFFFF0000u);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[i][j][4 * g + e] = fmaxf(x[e], 0.0f);
+        }
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s = fmaf(acc[i][j][e], acc[i][j][e], s);
+      s += __shfl_xor(s, 32);
+      if (half == 0) red[wn * BM + a_base_row + i * 32 + row_in_blk] = s;
+      __syncthreads();  // partial sums visible; every addend read of the band done
+      {
+        const int r = a_base_row + i * 32 + row_in_blk;
+        float ss = 0.0f;
+#pragma unroll
+        for (int w = 0; w < C::WAVES_N; ++w) ss += red[w * BM + r];
+        const float scale = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float v0 = acc[i][j][4 * g] * scale, v1 = acc[i][j][4 * g + 1] * scale;
+            const float v2 = acc[i][j][4 * g + 2] * scale, v3 = acc[i][j][4 * g + 3] * scale;
+            *reinterpret_cast<uint2*>(smem + b_lane * TROW + c0(j, g) * 2) =
+                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          }
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int e = tid; e < BROWS * PER_ROW; e += THREADS) {
+        const int b = e / PER_ROW, ck = e % PER_ROW;
+        const int64_t r = m0 + band_row(i, b);
+        const int c = n0 + 8 * ck;
+        if (r < a.M && c < a.N)
+          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(a.C) + r * a.N + c) =
+              *reinterpret_cast<const uint4*>(smem + b * TROW + 16 * ck);
+      }
+      __syncthreads();  // the staged band is read before the next band's addend lands
+    }
   } else {
     // Sum of squares of each row: over the lane's columns, then its partner
     // half-wave (lane ^ 32), then the WAVES_N waves of the row band in a
