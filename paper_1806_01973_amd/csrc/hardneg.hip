@@ -615,6 +615,11 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     });
     __syncthreads();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    // From here hist[c] counts the listed pins of count c < kGBins and
+    // sh_i32[6] those of larger counts, filled as the pairs are emitted.
+    for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+    if (tid == 0) sh_i32[6] = 0;
+    __syncthreads();
 
     // ---- C. count each partition's bucket in LDS ----------------------------
     for (uint32_t p = 0; p < parts; ++p) {
@@ -647,9 +652,16 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         __syncthreads();
         if (sh_i32[1]) {
           // Too crowded: split further, count the partition again from its
-          // first part.
+          // first part, and take the parts listed so far back out of the
+          // count histogram (rare).
           split *= 2;
           sp = 0;
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          for (int i = list0 + tid; i < sh_i32[0]; i += kThreads) {
+            const uint32_t c = list[2 * (int64_t)i + 1];
+            if (c < (uint32_t)kGBins) atomicSub(&hist[c], 1u);
+            else atomicSub(&sh_i32[6], 1);
+          }
           __syncthreads();
           if (tid == 0) sh_i32[0] = list0;
           __syncthreads();
@@ -657,11 +669,14 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         }
         for (int i = tid; i < kCSlots; i += kThreads) {
           const uint32_t k = lkeys[i];
+          const uint32_t c = lcnt[i];
           if (k != kNoKey) {
             const int pos = atomicAdd(&sh_i32[0], 1);
             list[2 * (int64_t)pos] = k;
-            list[2 * (int64_t)pos + 1] = lcnt[i];
+            list[2 * (int64_t)pos + 1] = c;
+            if (c >= (uint32_t)kGBins) atomicAdd(&sh_i32[6], 1);
           }
+          wave_hist_add(hist, c < (uint32_t)kGBins ? c : 0u, k != kNoKey && c < (uint32_t)kGBins);
         }
         __syncthreads();
         ++sp;
@@ -672,17 +687,34 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     const int Dr = (D + kThreads - 1) / kThreads * kThreads;  // whole waves sweep the list
 
     // ---- 1. count threshold ----------------------------------------------
-    for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
-    __syncthreads();
-    for (int i = tid; i < Dr; i += kThreads) {
-      const bool on = i < D;
-      const uint32_t c = on ? list[2 * (int64_t)i + 1] : 0u;
-      wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
-    }
-    __syncthreads();
+    // Usually rank rank_hi - 1 falls among counts below kGBins, whose
+    // histogram the listing filled: c* and n_above come from it directly.
+    // Otherwise (at least rank_hi pins counted kGBins or more) two passes over
+    // the list histogram the count's high and low 12 bits.
     uint32_t cstar = 0;  // pins counted more than cstar are ranked by step 2
     int64_t n_above = D;
-    if (D > R) {
+    const int n_big = sh_i32[6];
+    if (D > R && n_big < R) {
+      if (tid == 0) {
+        int b;
+        int64_t above;
+        top_bin(hist, R - 1 - n_big, &b, &above);
+        sh_i32[1] = b;
+        sh_i64[0] = n_big + above;
+      }
+      __syncthreads();
+      cstar = (uint32_t)sh_i32[1];
+      n_above = sh_i64[0];
+    } else if (D > R) {
+      __syncthreads();  // every wave has read n_big before hist is cleared
+      for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
+      __syncthreads();
+      for (int i = tid; i < Dr; i += kThreads) {
+        const bool on = i < D;
+        const uint32_t c = on ? list[2 * (int64_t)i + 1] : 0u;
+        wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
+      }
+      __syncthreads();
       if (tid == 0) {
         int b1;
         int64_t above;
