@@ -67,7 +67,8 @@ def test_embed_all_full(orc, wl, dataflow):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("dims", [(64, 64, 64), (256, 512, 256), (128, 96, 512), (48, 2048, 128)])
+@pytest.mark.parametrize("dims", [(64, 64, 64), (256, 512, 256), (128, 96, 512), (48, 2048, 128),
+                                  (64, 80, 400), (96, 160, 272)])
 @pytest.mark.parametrize("dataflow", DATAFLOWS)
 def test_convolve_layer_self_rows(orc, dtype, dims, dataflow):
     import paper_1806_01973_amd as ps
