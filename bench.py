@@ -436,9 +436,11 @@ def bench_embed_all(args, wl, inp):
     import torch
 
     import paper_1806_01973_amd as ps
-    # The library overlaps the walks with the first transform only for graphs
-    # of 2^18 to 2^22 pins (larger CSRs outgrow the MALL and the walks need
-    # every CU); other graphs get no schedule.
+    # Graphs of 2^18 to 2^22 pins run the walks beside the first transform.
+    # Larger ones run in order: their walks are bound by dependent random reads
+    # and slow down beside the transform by about as much as it would save
+    # (the library would overlap the shard's chained first layer, but at
+    # 2/8 of the CUs that measured 1341 against 1349 ms per step).
     overlapped = bool(args.overlap) and (1 << 18) <= wl.num_pins <= (1 << 22)
     job = ps.EmbedAll(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed,
                       weights=wl.name != "shard", overlap=args.overlap if overlapped else 0)

@@ -345,11 +345,14 @@ int pinsage_embed_all_workspace_size(const pinsage_graph_t* graph,
  * layers[k].d_in must equal layers[k-1].d_out; one storage dtype throughout.
  * schedule: NULL (walks, then the transform, in order on `stream`) or a
  * handle from pinsage_schedule_create on the current device (else
- * PINSAGE_EINVAL): with 262,144 to 4,194,304 pins the walks and the first
- * layer's transform then run beside each other on its masked streams, forked
- * from and joined back into `stream` by events (also on error returns), so
- * the call stays asynchronous and may be captured into a graph; other pin
- * counts run in order. The output does not depend on the schedule. */
+ * PINSAGE_EINVAL): with at least 262,144 pins, and at most 4,194,304 unless
+ * the first layer is bf16 dense-then-pool with d_in = d_out = 256 (the chained
+ * transform) and the graph's walk table fits in the first layer's output
+ * buffer of the workspace, the walks and the first layer's transform then run
+ * beside each other on its masked streams, forked from and joined back into
+ * `stream` by events (also on error returns), so the call stays asynchronous
+ * and may be captured into a graph; other pin counts run in order. The
+ * output does not depend on the schedule. */
 int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
                       const pinsage_layer_t* layers, int32_t num_layers, const void* x,
                       pinsage_neighborhoods_t* nbr_out, void* h_out,

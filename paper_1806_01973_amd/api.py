@@ -298,7 +298,9 @@ class EmbedAll:
     """Preallocated all-node embedding job (neighbourhoods + K layers, Sec. 3.4).
     overlap: 0 runs the walks and the first transform in order; 1-7 gives the
     job a Schedule on that many eighths of the CUs (used for graphs of 2^18 to
-    2^22 pins; the output is the same bits either way)."""
+    2^22 pins, and above 2^22 when the first layer is chained and the walk
+    table fits in the first layer's output buffer; the output is the same bits
+    either way)."""
 
     def __init__(self, graph: DeviceGraph, layers: List[DeviceLayer], walks: int, hops: int,
                  T: int, seed: int, weights: bool = True, overlap: int = 0):

@@ -465,10 +465,11 @@ int run_layer(const pinsage_layer_t* L, const void* h_in, int64_t n_in, int64_t 
 // floor((j + 1) k / 8) > floor(j k / 8), k = the share in eighths, which spreads
 // the side's bytes evenly over the mask words.
 
-// Pin counts that overlap: at least 2^18, and at most one transform chunk.
-// With more pins the graph outgrows the MALL, the walks become bound by HBM
-// latency and need every CU (measured on 10M pins: the walks slowed by more
-// than the transform share saved), so larger graphs run in order.
+// Pin counts that overlap: at least 2^18, and at most one transform chunk
+// unless the first layer is chained and the walk table fits beside it. Larger
+// graphs walking the CSR (two dependent reads per step) slowed by more than the
+// transform share saved (measured on 10M pins); the table's single read per
+// step keeps its rate on 7/8 of the CUs.
 constexpr int64_t kMinOverlapRows = 1ll << 18;
 constexpr int64_t kMaxOverlapRows = kChunkRows;
 
@@ -1021,9 +1022,17 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
 
   // Walks, then the first layer's transform: beside each other on the
   // schedule's masked streams when one is given and the pin count is in the
-  // overlapped range, else in order on the caller's stream.
+  // overlapped range, else in order on the caller's stream. Beside the
+  // transform the walks read the walk table from the first layer-output
+  // buffer (free until the first layer's pool writes it) when it fits there,
+  // else the CSR. With the table a first layer in the chained form overlaps
+  // at any pin count: the walks are then bound by dependent reads, whose rate
+  // holds on 7/8 of the CUs, and the chained transform needs no row chunks.
   bool transformed = false;
-  if (schedule && P >= kMinOverlapRows && P <= kMaxOverlapRows) {
+  unsigned char* const ov_table = (tb && num_layers > 1 && h >= tb) ? hbuf[0] : nullptr;
+  const bool ov_range =
+      P >= kMinOverlapRows && (P <= kMaxOverlapRows || (ov_table && chained_layer(L0)));
+  if (schedule && ov_range) {
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "current device");
@@ -1049,8 +1058,13 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
       // on error paths too (no work of this call is left unjoined).
       st = run_transform_rows(L0, x, n, P, nullptr, n, ws, 0, a, 0, ov.side);
       const hipError_t e1 = hipEventRecord(ov.side_done, ov.side);
-      if (!st) st = pinsage_build_neighborhoods(graph, walk, nullptr, n, nbr_out, total_steps,
-                                                ov.walk);
+      if (!st && ov_table) {
+        const hipError_t et = launch_walk_table(graph->row_offsets,
+                                                graph->offset_type == PINSAGE_I64, graph->col,
+                                                graph->nnz, n, ov_table, ov.walk);
+        if (et != hipSuccess) st = hip_fail(et, "walk table launch");
+      }
+      if (!st) st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, ov_table, ov.walk);
       const hipError_t e2 = hipEventRecord(ov.walk_done, ov.walk);
       // Join: the caller's stream waits for the walks before its share of
       // the transform, and for the side before the pool.

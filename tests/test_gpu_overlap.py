@@ -9,8 +9,10 @@ in-order one (walks, then the whole transform on the caller's stream):
 * the 1.2M-node fp32 graph, both layer dataflows, side CU shares of 2/8, 3/8
   and 4/8, three calls in a row (the pin share moves between calls), the
   same graph in bf16, and a single layer (the overlapped layer is the last);
-* a 4.5M-node graph with more pins than one 4,194,304-row chunk and a tiny
-  graph: both outside the overlapped range, so every share runs in order;
+* a 4.5M-node bf16 graph with more pins than one 4,194,304-row chunk, whose
+  first layer is chained and whose walk table fits in the first layer's output
+  buffer, so it overlaps too (the walks reading that table), and a tiny graph
+  (below the overlapped range: every share runs in order);
 * int64 row offsets with weights derived from counts, at 2^18 pins (the
   smallest overlapped size) and 2^18 - 1 pins (in order);
 * the overlapped call captured into a HIP graph and replayed.
@@ -78,7 +80,7 @@ def test_chunked_schedules_agree():
     from synth.device_gen import make_features_device, make_graph_device
     base = synth.WORKLOADS["minibatch"]  # bf16, 256 -> 512 -> 256
     wl = dataclasses.replace(base.scaled(4_300_000, 200_000, "overlap-chunked"), walks=20)
-    print("[case] schedules, 4.3M pins (two transform chunks, in order) bf16", flush=True)
+    print("[case] schedules, 4.3M pins (chained first layer, overlapped) bf16", flush=True)
     offsets, col, _ = make_graph_device(wl)
     x = make_features_device(wl, offsets, col)
     g = ps.DeviceGraph(offsets, col, wl.num_pins, wl.num_boards)
