@@ -610,6 +610,9 @@ def bench_minibatch(args, wl, inp):
     sets = [synth.minibatch_pairs(wl, inp["host"]["offsets"], inp["host"]["col"], B, n_neg,
                                   seed=i) for i in range(total)]
     dev = [[torch.as_tensor(a).cuda() for a in s] for s in sets]
+    # The graph's walk table, built once (as a caller would when the graph is
+    # loaded): the frontier walks and the hard negatives' walks read it.
+    inp["g"].build_walk_table()
     mb = ps.Minibatch(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed, B, n_neg,
                       mlp=inp.get("mlp"), num_hard=k)
     hard = torch.empty((B, k), dtype=torch.int32, device="cuda") if k else None
@@ -637,10 +640,11 @@ def bench_minibatch(args, wl, inp):
         edge_steps += int(mb.steps.item())
     edge_steps /= args.steps
     kd = kernels["walk_topt"]
-    walk_rates(kd, edge_steps / (kd["launches"] / args.steps), wl.offsets64)
+    walk_rates(kd, edge_steps / (kd["launches"] / args.steps), wl.offsets64, table=True)
+    inp["g"].drop_walk_table()
     extra = {"walk_steps_per_s": edge_steps / (kd["ms_per_step"] * 1e-3),
              "config_extra": {"pairs": B, "negatives": n_neg, "margin": 0.1,
-                              "hard_negatives_per_pair": k,
+                              "hard_negatives_per_pair": k, "walk_table": True,
                               "mean_frontier_sizes": mean_sizes,
                               "loss_last": float(mb.loss.item())}}
     metric = ("minibatch forward (Algorithm 2) + max-margin loss, training pairs/sec, 1 MI355X"
@@ -702,6 +706,9 @@ def bench_hard_negatives(args, wl, inp):
           for _ in range(total)]
     out = torch.empty((HN_QUERIES, k), dtype=torch.int32, device="cuda")
     steps_dev = []
+    # The graph's walk table, built once (as a caller would when the graph is
+    # loaded): every walk step is one dependent read.
+    inp["g"].build_walk_table()
 
     def run(i):
         _, st = ps.hard_negatives(inp["g"], qs[i], k, wl.seed + 1, args.hn_walks, args.hn_hops, HN_LO,
@@ -712,11 +719,12 @@ def bench_hard_negatives(args, wl, inp):
     kernels = kernel_table(prof, args.steps)
     edge_steps = sum(int(t.item()) for t in steps_dev[args.warmup:]) / args.steps
     kd = kernels["hard_neg"]
-    walk_rates(kd, edge_steps, wl.offsets64)
+    walk_rates(kd, edge_steps, wl.offsets64, table=True)
+    inp["g"].drop_walk_table()
     value = HN_QUERIES * args.steps / elapsed
     extra = {"walk_steps_per_s": edge_steps * args.steps / elapsed,
              "config_extra": {"queries": HN_QUERIES, "walks": args.hn_walks, "hops": args.hn_hops,
-                              "rank_window": [HN_LO, HN_HI], "per_query": k,
+                              "rank_window": [HN_LO, HN_HI], "per_query": k, "walk_table": True,
                               "empty_rows_last": int((out[:, 0] < 0).sum().item())}}
     metric = "hard negative items (Sec. 3.3, PPR rank window), queries/sec, 1 MI355X"
     return value, "queries/s", metric, elapsed, kernels, extra

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 10
+#define PINSAGE_ABI_VERSION 11
 
 enum {
   PINSAGE_OK = 0,
@@ -56,7 +56,13 @@ typedef enum { PINSAGE_F32 = 0, PINSAGE_BF16 = 1 } pinsage_dtype_t;
 
 /* Bipartite pin-board graph (Sec. 3.1). row_offsets: device, num_nodes + 1
  * entries of offset_type, row_offsets[0] = 0, non-decreasing, last = nnz.
- * col: device, nnz int32 node ids. I32 offsets require nnz < 2^31. */
+ * col: device, nnz int32 node ids. I32 offsets require nnz < 2^31.
+ * walk_table: NULL, or device memory filled by pinsage_build_walk_table for
+ * this graph (same row_offsets and col, unmodified since; 16-byte aligned,
+ * nnz < 2^31). When set, every random walk of the library (neighbourhoods,
+ * minibatch frontiers, hard negatives, the all-node job) reads it: one
+ * dependent read per edge step instead of the node's offsets and then a
+ * neighbour id. The walks, and so every result, are the same bits. */
 typedef struct {
   int64_t num_pins;
   int64_t num_boards;
@@ -64,6 +70,7 @@ typedef struct {
   pinsage_index_t offset_type;
   const void* row_offsets;
   const int32_t* col;
+  const void* walk_table;
 } pinsage_graph_t;
 
 /* Random-walk parameters (Sec. 3.2). Each of `walks_per_node` walks from a
@@ -162,6 +169,25 @@ typedef struct {
   const float* g;
   const void* G2;
 } pinsage_mlp_t;
+
+/* Walk table of a graph (a layout of its CSR for the random walks of
+ * Sec. 3.2): 16 bytes per CSR position e, {col[e], degree of col[e], row
+ * start of col[e] (low, high 32 bits)}, degree 0 for a node whose row is
+ * empty or malformed, so that an edge step reads one entry at a uniform
+ * position of the current node's row.
+ *   pinsage_walk_table_size   *bytes = 16 nnz. PINSAGE_EUNSUPPORTED when
+ *                             nnz >= 2^31 (*bytes = 0), PINSAGE_EINVAL for a
+ *                             malformed graph or NULL bytes.
+ *   pinsage_build_walk_table  fills `table` (device, 16-byte aligned, at
+ *                             least the size above; caller-owned) on
+ *                             `stream`, asynchronously; set graph.walk_table
+ *                             to it for later calls. PINSAGE_EWORKSPACE when
+ *                             table_bytes is too small, PINSAGE_EINVAL for
+ *                             NULL or misaligned table. Rebuild it after
+ *                             changing the CSR. */
+int pinsage_walk_table_size(const pinsage_graph_t* graph, size_t* bytes);
+int pinsage_build_walk_table(const pinsage_graph_t* graph, void* table, size_t table_bytes,
+                             void* stream);
 
 /* Version of this ABI (PINSAGE_ABI_VERSION). */
 int pinsage_version(void);

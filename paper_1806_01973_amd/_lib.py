@@ -38,13 +38,15 @@ EXPORTED = [
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
     "pinsage_profile_enable", "pinsage_profile_read", "pinsage_profile_random_reads",
+    "pinsage_walk_table_size", "pinsage_build_walk_table",
 ]
 
 
 class Graph(ctypes.Structure):
     _fields_ = [("num_pins", ctypes.c_int64), ("num_boards", ctypes.c_int64),
                 ("nnz", ctypes.c_int64), ("offset_type", ctypes.c_int),
-                ("row_offsets", ctypes.c_void_p), ("col", ctypes.c_void_p)]
+                ("row_offsets", ctypes.c_void_p), ("col", ctypes.c_void_p),
+                ("walk_table", ctypes.c_void_p)]
 
 
 class WalkParams(ctypes.Structure):
@@ -155,6 +157,8 @@ def lib():
     L.pinsage_profile_random_reads.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
                                                ctypes.c_void_p]
+    L.pinsage_walk_table_size.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(ctypes.c_size_t)]
+    L.pinsage_build_walk_table.argtypes = [ctypes.POINTER(Graph), P, ctypes.c_size_t, P]
     for name in EXPORTED:
         fn = getattr(L, name)
         if fn.restype is None or fn.restype is ctypes.c_int:

@@ -61,6 +61,7 @@ class DeviceGraph:
         odt = torch.int64 if self.offsets64 else torch.int32
         self.offsets = offsets.to(device=device, dtype=odt).contiguous()
         self.col = col.to(device=device, dtype=torch.int32).contiguous()
+        self.walk_table: Optional[torch.Tensor] = None
         if self.offsets.numel() != self.num_nodes + 1:
             raise ValueError("offsets must have num_nodes + 1 entries")
 
@@ -68,10 +69,28 @@ class DeviceGraph:
     def num_nodes(self) -> int:
         return self.num_pins + self.num_boards
 
+    def build_walk_table(self, stream=None) -> "DeviceGraph":
+        """Builds the graph's walk table (16 bytes per CSR position); every later
+        walk on this graph reads it (same results, one read per edge step)."""
+        n = ctypes.c_size_t(0)
+        self.walk_table = None
+        L.check(L.lib().pinsage_walk_table_size(ctypes.byref(self.struct()), ctypes.byref(n)),
+                "pinsage_walk_table_size")
+        table = torch.empty(max(1, n.value), dtype=torch.uint8, device=self.col.device)
+        L.check(L.lib().pinsage_build_walk_table(ctypes.byref(self.struct()), table.data_ptr(),
+                                                 table.numel(), _stream(stream)),
+                "pinsage_build_walk_table")
+        self.walk_table = table
+        return self
+
+    def drop_walk_table(self) -> None:
+        self.walk_table = None
+
     def struct(self) -> L.Graph:
         return L.Graph(self.num_pins, self.num_boards, self.nnz,
                        L.PINSAGE_I64 if self.offsets64 else L.PINSAGE_I32,
-                       self.offsets.data_ptr(), self.col.data_ptr())
+                       self.offsets.data_ptr(), self.col.data_ptr(),
+                       self.walk_table.data_ptr() if self.walk_table is not None else None)
 
 
 @dataclass
@@ -321,6 +340,7 @@ class EmbedAll:
     def run(self, x: torch.Tensor, stream=None) -> torch.Tensor:
         x = _dev(x, "x", self.layers[0].dtype)
         sched = self.schedule.handle if self.schedule is not None else None
+        self._g = self.graph.struct()  # picks up a walk table built since
         st = L.lib().pinsage_embed_all(ctypes.byref(self._g), ctypes.byref(self.walk),
                                        self._layers, len(self.layers), _ptr(x),
                                        ctypes.byref(self._nbr), _ptr(self.out), _ptr(self.steps),
@@ -465,6 +485,7 @@ class Minibatch:
             hp = _dev(hard, "hard", torch.int32).data_ptr()
         pairs = L.Pairs(self.B, self.n_neg, q.data_ptr(), p.data_ptr(), ng.data_ptr(), margin,
                         self.k_hard, hp)
+        self._g = self.graph.struct()  # picks up a walk table built since
         st = L.lib().pinsage_minibatch_forward(ctypes.byref(self._g), ctypes.byref(self.walk),
                                                self._layers, len(self.layers), self._mlp_ref(),
                                                _ptr(x),

@@ -72,6 +72,12 @@ int check_graph(const pinsage_graph_t* g) {
     return fail(PINSAGE_EUNSUPPORTED, "nnz %lld needs int64 row offsets", (long long)g->nnz);
   if (!g->row_offsets) return fail(PINSAGE_EINVAL, "row_offsets is NULL");
   if (!g->col && g->nnz > 0) return fail(PINSAGE_EINVAL, "col is NULL");
+  if (g->walk_table) {
+    if (g->nnz > kWalkTableMaxNnz)
+      return fail(PINSAGE_EUNSUPPORTED, "nnz %lld too large for a walk table", (long long)g->nnz);
+    if (reinterpret_cast<uintptr_t>(g->walk_table) % 16)
+      return fail(PINSAGE_EINVAL, "walk_table is not 16-byte aligned");
+  }
   return PINSAGE_OK;
 }
 
@@ -638,8 +644,41 @@ int pinsage_build_neighborhoods(const pinsage_graph_t* graph, const pinsage_walk
   if ((st = check_nbr(out, num_sources, "build_neighborhoods"))) return st;
   if (out->top_t != walk->top_t)
     return fail(PINSAGE_EINVAL, "out->top_t %d != walk->top_t %d", out->top_t, walk->top_t);
-  return run_walks(graph, walk, sources, num_sources, out, total_steps, nullptr,
+  return run_walks(graph, walk, sources, num_sources, out, total_steps, graph->walk_table,
                    static_cast<hipStream_t>(stream));
+}
+
+int pinsage_walk_table_size(const pinsage_graph_t* graph, size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(PINSAGE_EINVAL, "bytes is NULL");
+  *bytes = 0;
+  const int st = check_graph(graph);
+  if (st) return st;
+  if (graph->nnz > kWalkTableMaxNnz)
+    return fail(PINSAGE_EUNSUPPORTED, "nnz %lld too large for a walk table",
+                (long long)graph->nnz);
+  *bytes = (size_t)graph->nnz * 16;
+  return PINSAGE_OK;
+}
+
+int pinsage_build_walk_table(const pinsage_graph_t* graph, void* table, size_t table_bytes,
+                             void* stream) {
+  g_last_error.clear();
+  size_t need = 0;
+  const int st = pinsage_walk_table_size(graph, &need);
+  if (st) return st;
+  if (!table && need > 0) return fail(PINSAGE_EINVAL, "table is NULL");
+  if (table_bytes < need)
+    return fail(PINSAGE_EWORKSPACE, "table %zu bytes < required %zu", table_bytes, need);
+  if (reinterpret_cast<uintptr_t>(table) % 16)
+    return fail(PINSAGE_EINVAL, "table is not 16-byte aligned");
+  if (need == 0) return PINSAGE_OK;
+  const hipError_t e =
+      launch_walk_table(graph->row_offsets, graph->offset_type == PINSAGE_I64, graph->col,
+                        graph->nnz, graph->num_pins + graph->num_boards, table,
+                        static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "walk table launch");
+  return PINSAGE_OK;
 }
 
 int check_hard_negative_params(const pinsage_hard_negative_params_t* params, int64_t num_queries) {
@@ -712,6 +751,7 @@ int pinsage_hard_negatives(const pinsage_graph_t* graph,
   a.k = h.num_per_query;
   a.out = out;
   a.total_steps = total_steps;
+  a.table = graph->walk_table;
   hipError_t e = launch_hard_negatives(a, workspace, s);
   if (e != hipSuccess) return hip_fail(e, "hard negative launch");
   return PINSAGE_OK;
@@ -1029,9 +1069,10 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   // at any pin count: the walks are then bound by dependent reads, whose rate
   // holds on 7/8 of the CUs, and the chained transform needs no row chunks.
   bool transformed = false;
-  unsigned char* const ov_table = (tb && num_layers > 1 && h >= tb) ? hbuf[0] : nullptr;
-  const bool ov_range =
-      P >= kMinOverlapRows && (P <= kMaxOverlapRows || (ov_table && chained_layer(L0)));
+  const void* const gtab = graph->walk_table;  // the caller's table, when given
+  unsigned char* const ov_table = (!gtab && tb && num_layers > 1 && h >= tb) ? hbuf[0] : nullptr;
+  const bool ov_range = P >= kMinOverlapRows &&
+                        (P <= kMaxOverlapRows || ((gtab || ov_table) && chained_layer(L0)));
   if (schedule && ov_range) {
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
@@ -1064,7 +1105,9 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
                                                 graph->nnz, n, ov_table, ov.walk);
         if (et != hipSuccess) st = hip_fail(et, "walk table launch");
       }
-      if (!st) st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, ov_table, ov.walk);
+      if (!st)
+        st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, gtab ? gtab : ov_table,
+                       ov.walk);
       const hipError_t e2 = hipEventRecord(ov.walk_done, ov.walk);
       // Join: the caller's stream waits for the walks before its share of
       // the transform, and for the side before the pool.
@@ -1085,13 +1128,13 @@ int pinsage_embed_all(const pinsage_graph_t* graph, const pinsage_walk_params_t*
   if (!transformed) {
     // In order: the walks read the graph's walk table, built in the layers'
     // region of the workspace (one read per edge step instead of two).
-    if (tb) {
+    if (tb && !gtab) {
       const hipError_t e = launch_walk_table(graph->row_offsets, graph->offset_type == PINSAGE_I64,
                                              graph->col, graph->nnz, n, ws, s);
       if (e != hipSuccess) return hip_fail(e, "walk table launch");
     }
-    if ((st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, tb ? ws : nullptr, s)))
-      return st;
+    const void* tab = gtab ? gtab : (tb ? ws : nullptr);
+    if ((st = run_walks(graph, walk, nullptr, n, nbr_out, total_steps, tab, s))) return st;
     if ((st = run_transform(L0, x, n, P, nullptr, n, ws, s))) return st;
   }
 
@@ -1458,6 +1501,7 @@ int pinsage_minibatch_forward(const pinsage_graph_t* graph, const pinsage_walk_p
     a.counts = reinterpret_cast<uint16_t*>(ws + p.ncnt[k]);
     a.weights = reinterpret_cast<float*>(ws + p.nw[k]);
     a.total_steps = total_steps;  // accumulated over the levels
+    a.table = graph->walk_table;
     PINSAGE_TRY(launch_walk_topt(a, s), "walk launch");
     return PINSAGE_OK;
   };

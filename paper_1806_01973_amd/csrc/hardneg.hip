@@ -168,14 +168,89 @@ __device__ __forceinline__ int block_exclusive_sum(int v, int wave, int lane, in
   return before + incl - v;
 }
 
-template <typename OffT, int E>
+// The walks of query u (Sec. 3.2, as the neighbourhood walks): kWalkers walks
+// per thread in lockstep (w0, w0 + 1024, ...), so their dependent reads
+// overlap; walk w's pin landings go to slots[w * hops ..]. TABLE: each edge
+// step reads one 16-byte walk-table entry (the neighbour's id, degree and row
+// start) instead of the current node's offsets and then a neighbour id; the
+// source's row comes from its offsets, validated as pick() validates a row.
+// Returns this thread's edge steps.
+template <typename OffT, bool TABLE>
+__device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u, int tid,
+                                               uint32_t* slots, uint32_t k0, uint32_t k1) {
+  const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
+  const int32_t* __restrict__ col = a.col;
+  const uint4* __restrict__ tab = static_cast<const uint4*>(a.table);
+  int64_t ulo = 0;
+  int32_t udeg = 0;
+  if constexpr (TABLE) {
+    const int64_t lo = (int64_t)off[u], hi = (int64_t)off[u + 1];
+    if (!(hi - lo <= 0 || lo < 0 || hi > a.nnz)) {
+      ulo = lo;
+      udeg = (int32_t)(hi - lo);
+    }
+  }
+  uint32_t steps = 0;
+  for (int w0 = tid; w0 < a.walks; w0 += kWalkers * kThreads) {
+    Walker<OffT> W[kWalkers];
+#pragma unroll
+    for (int i = 0; i < kWalkers; ++i) {
+      const int w = w0 + i * kThreads;
+      W[i].start(u, w, slots + (int64_t)w * a.hops, w < a.walks);
+      W[i].lo = ulo;
+      W[i].deg = udeg;
+    }
+    bool any = true;
+    while (any) {
+      if constexpr (TABLE) {
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) W[i].pick_carried(k0, k1);
+        uint4 e[kWalkers];
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i)
+          e[i] = W[i].active ? tab[W[i].next_at] : make_uint4(0u, 0u, 0u, 0u);
+        any = false;
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) {
+          W[i].land_entry(e[i], a.num_pins, a.num_nodes, a.hops);
+          any = any || W[i].active;
+        }
+      } else {
+        int64_t lo[kWalkers], hi[kWalkers];
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) {
+          lo[i] = 0;
+          hi[i] = 0;
+          if (W[i].active) {
+            lo[i] = (int64_t)off[W[i].cur];
+            hi[i] = (int64_t)off[W[i].cur + 1];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) W[i].pick(lo[i], hi[i], a.nnz, k0, k1);
+        int32_t nx[kWalkers];
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) nx[i] = W[i].active ? col[W[i].next_at] : 0;
+        any = false;
+#pragma unroll
+        for (int i = 0; i < kWalkers; ++i) {
+          W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
+          any = any || W[i].active;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kWalkers; ++i) steps += W[i].finish(a.hops);
+  }
+  return steps;
+}
+
+template <typename OffT, int E, bool TABLE>
 __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a) {
   constexpr int N = kThreads * E;
   __shared__ uint32_t keys[N + N / E];  // visits (sorted, padded), then head positions, rank keys
   __shared__ uint32_t ids[N];           // pins in rank order (repeated pins by number p)
   __shared__ int wave_tot[kWaves];
-  const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
-  const int32_t* __restrict__ col = a.col;
   const int WH = a.walks * a.hops;
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
@@ -198,44 +273,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
       const int slot = e * kThreads + tid;
       if (slot >= WH || !live) keys[slot] = kEmpty;
     }
-    if (live) {
-      // kWalkers walks per thread in lockstep (w0, w0 + 1024, ...): their
-      // dependent offset -> neighbour reads overlap.
-      for (int w0 = tid; w0 < a.walks; w0 += kWalkers * kThreads) {
-        Walker<OffT> W[kWalkers];
-#pragma unroll
-        for (int i = 0; i < kWalkers; ++i) {
-          const int w = w0 + i * kThreads;
-          W[i].start(u, w, keys + w * a.hops, w < a.walks);
-        }
-        bool any = true;
-        while (any) {
-          int64_t lo[kWalkers], hi[kWalkers];
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) {
-            lo[i] = 0;
-            hi[i] = 0;
-            if (W[i].active) {
-              lo[i] = (int64_t)off[W[i].cur];
-              hi[i] = (int64_t)off[W[i].cur + 1];
-            }
-          }
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) W[i].pick(lo[i], hi[i], a.nnz, k0, k1);
-          int32_t nx[kWalkers];
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) nx[i] = W[i].active ? col[W[i].next_at] : 0;
-          any = false;
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) {
-            W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
-            any = any || W[i].active;
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < kWalkers; ++i) my_steps += W[i].finish(a.hops);
-      }
-    }
+    if (live) my_steps += walk_query<OffT, TABLE>(a, u, tid, keys, k0, k1);
     __syncthreads();
 
     // ---- 2. sort visits by id ---------------------------------------------
@@ -498,7 +536,7 @@ __device__ __forceinline__ void low_bin(const uint32_t* hist, int nbins, int64_t
   *below = cum;
 }
 
-template <typename OffT>
+template <typename OffT, bool TABLE>
 __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegLaunch a,
                                                                         uint32_t* ws,
                                                                         int64_t ws_words) {
@@ -516,8 +554,6 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
   uint32_t* buf = ws + (int64_t)blockIdx.x * ws_words;  // L landings, by (walk, hop)
   uint32_t* sorted = buf + L;                           // the landings, by partition
   uint32_t* list = sorted + L;                          // up to L (pin, count) pairs
-  const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
-  const int32_t* __restrict__ col = a.col;
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
   const int tid = threadIdx.x;
@@ -533,40 +569,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
 
     // ---- W. walks, landings into the buffer ------------------------------
     if (live) {
-      for (int w0 = tid; w0 < a.walks; w0 += kWalkers * kThreads) {
-        Walker<OffT> W[kWalkers];
-#pragma unroll
-        for (int i = 0; i < kWalkers; ++i) {
-          const int w = w0 + i * kThreads;
-          W[i].start(u, w, buf + (int64_t)w * a.hops, w < a.walks);
-        }
-        bool any = true;
-        while (any) {
-          int64_t lo[kWalkers], hi[kWalkers];
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) {
-            lo[i] = 0;
-            hi[i] = 0;
-            if (W[i].active) {
-              lo[i] = (int64_t)off[W[i].cur];
-              hi[i] = (int64_t)off[W[i].cur + 1];
-            }
-          }
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) W[i].pick(lo[i], hi[i], a.nnz, k0, k1);
-          int32_t nx[kWalkers];
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) nx[i] = W[i].active ? col[W[i].next_at] : 0;
-          any = false;
-#pragma unroll
-          for (int i = 0; i < kWalkers; ++i) {
-            W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
-            any = any || W[i].active;
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < kWalkers; ++i) my_steps += W[i].finish(a.hops);
-      }
+      my_steps += walk_query<OffT, TABLE>(a, u, tid, buf, k0, k1);
     } else {
       for (int64_t i = tid; i < L; i += kThreads) buf[i] = kEmpty;
     }
@@ -836,19 +839,26 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
   }
 }
 
-template <typename OffT>
+template <typename OffT, bool TABLE>
 hipError_t launch_for_offsets(const HardNegLaunch& a, hipStream_t s) {
   const int wh = a.walks * a.hops;
   const int64_t cap = 1ll << 13;
   const dim3 grid((unsigned)(a.num_queries < cap ? a.num_queries : cap));
   const dim3 block(kThreads);
-  if (wh <= 1 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 1>), grid, block, 0, s, a);
-  else if (wh <= 2 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 2>), grid, block, 0, s, a);
-  else if (wh <= 4 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 4>), grid, block, 0, s, a);
-  else if (wh <= 8 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 8>), grid, block, 0, s, a);
-  else if (wh <= 16 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 16>), grid, block, 0, s, a);
+  if (wh <= 1 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 1, TABLE>), grid, block, 0, s, a);
+  else if (wh <= 2 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 2, TABLE>), grid, block, 0, s, a);
+  else if (wh <= 4 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 4, TABLE>), grid, block, 0, s, a);
+  else if (wh <= 8 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 8, TABLE>), grid, block, 0, s, a);
+  else if (wh <= 16 * kThreads) hipLaunchKernelGGL((hard_negative_kernel<OffT, 16, TABLE>), grid, block, 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+template <typename OffT, bool TABLE>
+void launch_global(const HardNegLaunch& a, uint32_t* ws, int64_t words, hipStream_t s) {
+  const int64_t blocks = a.num_queries < kGMaxBlocks ? a.num_queries : kGMaxBlocks;
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  hipLaunchKernelGGL((hard_negative_global_kernel<OffT, TABLE>), grid, block, 0, s, a, ws, words);
 }
 
 }  // namespace
@@ -874,15 +884,21 @@ hipError_t launch_hard_negatives(const HardNegLaunch& a, void* workspace, hipStr
   if (a.num_queries <= 0) return hipSuccess;
   ProfileScope prof(kKHardNeg, s);
   const int64_t landings = (int64_t)a.walks * a.hops;
-  if (landings <= kMaxOnChipLandings)
-    return a.offsets64 ? launch_for_offsets<int64_t>(a, s) : launch_for_offsets<int32_t>(a, s);
-  const dim3 grid((unsigned)hard_negative_blocks(a.num_queries)), block(kThreads);
+  const bool table = a.table != nullptr;
+  if (landings <= kMaxOnChipLandings) {
+    if (a.offsets64)
+      return table ? launch_for_offsets<int64_t, true>(a, s) : launch_for_offsets<int64_t, false>(a, s);
+    return table ? launch_for_offsets<int32_t, true>(a, s) : launch_for_offsets<int32_t, false>(a, s);
+  }
   uint32_t* ws = static_cast<uint32_t*>(workspace);
   const int64_t words = hard_negative_ws_words(landings);
-  if (a.offsets64)
-    hipLaunchKernelGGL(hard_negative_global_kernel<int64_t>, grid, block, 0, s, a, ws, words);
-  else
-    hipLaunchKernelGGL(hard_negative_global_kernel<int32_t>, grid, block, 0, s, a, ws, words);
+  if (a.offsets64) {
+    if (table) launch_global<int64_t, true>(a, ws, words, s);
+    else launch_global<int64_t, false>(a, ws, words, s);
+  } else {
+    if (table) launch_global<int32_t, true>(a, ws, words, s);
+    else launch_global<int32_t, false>(a, ws, words, s);
+  }
   return hipGetLastError();
 }
 

@@ -72,6 +72,7 @@ struct HardNegLaunch {
   int k;
   int32_t* out;
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
+  const void* table;                // nullable: the graph's walk table
 };
 // Walk budgets above kMaxOnChipLandings buffer a query's landings in the
 // workspace, bucket them by hash partition and count each bucket in LDS

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 10
+    assert lib.pinsage_version() == 11
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -83,6 +83,33 @@ def test_build_neighborhoods_validation(L):
         L.PINSAGE_EINVAL  # row mismatch
     assert call(_graph(L), walk, None, 15, L.Neighborhoods(15, 8, None, FAKE, None)) == \
         L.PINSAGE_EINVAL
+
+
+def test_walk_table_validation(L):
+    lib = L.lib()
+    n = ctypes.c_size_t(7)
+    assert lib.pinsage_walk_table_size(ctypes.byref(_graph(L)), ctypes.byref(n)) == L.PINSAGE_OK
+    assert n.value == 40 * 16
+    assert lib.pinsage_walk_table_size(ctypes.byref(_graph(L)), None) == L.PINSAGE_EINVAL
+    g64 = _graph(L, nnz=2**31, offset_type=L.PINSAGE_I64)
+    assert lib.pinsage_walk_table_size(ctypes.byref(g64), ctypes.byref(n)) == L.PINSAGE_EUNSUPPORTED
+    assert n.value == 0
+    assert lib.pinsage_walk_table_size(ctypes.byref(_graph(L, num_pins=-1)),
+                                       ctypes.byref(n)) == L.PINSAGE_EINVAL
+    build = lambda g, t, b: lib.pinsage_build_walk_table(ctypes.byref(g), t, b, None)
+    assert build(_graph(L), FAKE, 40 * 16 - 1) == L.PINSAGE_EWORKSPACE
+    assert build(_graph(L), None, 40 * 16) == L.PINSAGE_EINVAL
+    assert build(_graph(L), FAKE + 8, 40 * 16) == L.PINSAGE_EINVAL  # alignment
+    assert build(g64, FAKE, 2**36) == L.PINSAGE_EUNSUPPORTED
+    # A graph carrying a walk table: checked wherever the graph is.
+    walk = L.WalkParams(1, 10, 2, 8)
+    nb = L.Neighborhoods(15, 8, FAKE, FAKE, None)
+    for g, want in ((_graph(L, walk_table=FAKE + 4), L.PINSAGE_EINVAL),
+                    (_graph(L, nnz=2**31, offset_type=L.PINSAGE_I64, walk_table=FAKE),
+                     L.PINSAGE_EUNSUPPORTED)):
+        assert lib.pinsage_build_neighborhoods(ctypes.byref(g), ctypes.byref(walk), None, 15,
+                                               ctypes.byref(nb), None, None) == want
+        assert b"walk" in lib.pinsage_last_error() or b"nnz" in lib.pinsage_last_error()
 
 
 def test_hard_negatives_validation(L):
