@@ -592,13 +592,13 @@ const char* pinsage_status_string(int status) {
 const char* pinsage_last_error(void) { return g_last_error.c_str(); }
 
 // Bytes of a graph's walk table (0 when nnz is too large for one).
-size_t walk_table_bytes(const pinsage_graph_t* g) {
+static size_t walk_table_bytes(const pinsage_graph_t* g) {
   return g->nnz > 0 && g->nnz <= kWalkTableMaxNnz ? align_up((size_t)g->nnz * 16) : 0;
 }
 
 // The walks and top-T of validated arguments; `table` is the graph's walk
 // table or NULL (read the CSR).
-int run_walks(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
+static int run_walks(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
               const int32_t* sources, int64_t num_sources, pinsage_neighborhoods_t* out,
               unsigned long long* total_steps, const void* table, hipStream_t s) {
   if (total_steps) {
@@ -681,7 +681,8 @@ int pinsage_build_walk_table(const pinsage_graph_t* graph, void* table, size_t t
   return PINSAGE_OK;
 }
 
-int check_hard_negative_params(const pinsage_hard_negative_params_t* params, int64_t num_queries) {
+static int check_hard_negative_params(const pinsage_hard_negative_params_t* params,
+                                      int64_t num_queries) {
   if (!params) return fail(PINSAGE_EINVAL, "hard negative params are NULL");
   const pinsage_hard_negative_params_t& h = *params;
   if (h.walks < 1 || h.hops < 1)
