@@ -599,8 +599,8 @@ static size_t walk_table_bytes(const pinsage_graph_t* g) {
 // The walks and top-T of validated arguments; `table` is the graph's walk
 // table or NULL (read the CSR).
 static int run_walks(const pinsage_graph_t* graph, const pinsage_walk_params_t* walk,
-              const int32_t* sources, int64_t num_sources, pinsage_neighborhoods_t* out,
-              unsigned long long* total_steps, const void* table, hipStream_t s) {
+                     const int32_t* sources, int64_t num_sources, pinsage_neighborhoods_t* out,
+                     unsigned long long* total_steps, const void* table, hipStream_t s) {
   if (total_steps) {
     hipError_t e = launch_zero_u64(total_steps, 1, s);
     if (e != hipSuccess) return hip_fail(e, "step counter reset");
