@@ -253,8 +253,7 @@ __global__ __launch_bounds__(256) void pool_narrow_kernel(PoolLaunch a) {
 // per batch (one batch when the row has at most RG * NB slots), slot ids and
 // alphas passed to the groups by lane permutes. Group g sums slots g, g + RG,
 // ... in rank order and the groups are combined by the same butterfly as in
-// pool_narrow_kernel (and, for RG = 1, the same order as pool_kernel), so the
-// result is the same bits. Measured on random 512-byte rows from a 41 GB
+// pool_narrow_kernel, so the result is the same bits. Measured on random 512-byte rows from a 41 GB
 // table: as fast as a gather with no header reads at all (+16% over the
 // batched kernel).
 template <bool BF16, int MODE, int RG, int NB>
@@ -366,15 +365,17 @@ hipError_t launch_mode(const PoolLaunch& a, hipStream_t s) {
   const dim3 grid((unsigned)(blocks_needed < cap ? blocks_needed : cap));
   const dim3 block(256);
   const int vec_per_row = a.m / VN;
-  if (a.T <= kWave) {
+  // The header-in-registers kernel for rows narrower than a wave slab (it gathers
+  // 1 KB per load instruction from two or four rows at once). Rows of a full
+  // slab measured as fast or faster in the batched kernel (1.2M- and 12M-node
+  // graphs: 6.49 against 6.61 ms, 25.1 against 25.3 ms), and much faster on
+  // short neighbourhoods (graph neighbourhoods of about 3 pins: 0.84 against
+  // 1.58 ms), where the header's round trip is most of a row's work.
+  if (a.T <= kWave && vec_per_row <= kWave / 2) {
     if (vec_per_row <= kWave / 4)
       hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 4, 16>), grid, block, 0, s, a);
-    else if (vec_per_row <= kWave / 2)
-      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 2, 32>), grid, block, 0, s, a);
-    else if (slabs <= 1)
-      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 1, 32>), grid, block, 0, s, a);
     else
-      return launch_batched<BF16, MODE>(a, grid, block, slabs, vec_per_row, s);
+      hipLaunchKernelGGL((pool_head_kernel<BF16, MODE, 2, 32>), grid, block, 0, s, a);
     return hipGetLastError();
   }
   return launch_batched<BF16, MODE>(a, grid, block, slabs, vec_per_row, s);
