@@ -26,10 +26,13 @@
 //      16-column group reordered to match (permute_wn_kernel), so the product
 //      is the same sum over the same 32 columns.
 // Q chunks (16 KB for d_in = 256, with the chunk's 32 bias values behind the
-// padded rows) and W_n' chunks (16 KB for d_out = 256) travel global -> LDS by
-// DMA (global_load_lds_dwordx4) into two rings of two slots each (74 KB per
-// block), one barrier per chunk; rows are padded by 16 bytes so fragment reads
-// of 16 rows fall on distinct banks. The first product of chunk j + 1 and the
+// rows) and W_n' chunks (16 KB for d_out = 256) travel global -> LDS by DMA
+// (global_load_lds_dwordx4) into two rings of two slots each (65 KB per
+// block), one barrier per chunk. Rows are unpadded; their 16-byte vectors are
+// XOR-swizzled so that the 16 lanes of a fragment read fall on distinct banks
+// (padding the rows instead, as measured, costs 7%: a fifth more W_n' DMA bytes
+// into the LDS, whose bandwidth bounds this kernel, and per-DMA offset
+// arithmetic). The first product of chunk j + 1 and the
 // second of chunk j run interleaved, step by step, so the matrix pipe never
 // waits for the bias/ReLU/rounding of a chunk. R is accumulated in fp32 over
 // the chunks in order and rounded once to bf16.
@@ -78,25 +81,25 @@ __device__ __forceinline__ void wait_all_and_barrier() {
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" : : : "memory");
 }
 
-// KS = d_in / 16 k-steps of the first product (d_in a multiple of 128, so a
-// Q row has a multiple of 16 vectors), NB = d_out / 32 output blocks.
+// KS = d_in / 16 k-steps of the first product (16: d_in = 256), NB = d_out / 32
+// output blocks.
 template <int KS, int NB>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void chain_kernel(ChainLaunch a) {
-  // LDS rows are padded by 16 bytes: 16 consecutive rows read at the same
-  // column then start 4 banks apart (528 = 64 x 8 + 16 bytes, 80 = 64 + 16),
-  // so fragment reads are conflict-free and their addresses are one base
-  // register plus immediate offsets.
-  constexpr int QROW = KS * 32 + 16;  // bytes of a padded Q row (d_in bf16)
-  constexpr int WROW = 64 + 16;       // bytes of a padded W_n' row (32 bf16)
-  constexpr int QDATA = kMC * QROW;   // the chunk's bias floats follow the rows
-  constexpr int QDMA = (QDATA + kMC * 4 + 1023) / 1024;  // 1 KB DMA blocks per Q slot
-  constexpr int WDMA = (NB * 32 * WROW + 1023) / 1024;
-  constexpr int QBYTES = QDMA * 1024;
-  constexpr int WBYTES = WDMA * 1024;
-  constexpr int WRING = 2 * QBYTES;   // the W_n' ring follows the Q ring
+  // Unpadded LDS rows with XOR-swizzled 16-byte vectors: vector v of Q row r
+  // sits in slot v ^ (r & 15), vector v of W_n' row n in slot v ^ ((n >> 2) & 3),
+  // so the 16 lanes of a fragment read fall on distinct banks, and each DMA
+  // lane's source offset is one per-lane value plus a wave-uniform base.
+  constexpr int QROWB = KS * 32;           // bytes of a Q row (d_in bf16)
+  constexpr int QDATA = kMC * QROWB;       // the chunk's bias floats follow the rows
+  constexpr int QBYTES = QDATA + 256;
+  constexpr int WROWB = kMC * 2;           // bytes of a W_n' row chunk
+  constexpr int WBYTES = NB * 32 * WROWB;
+  constexpr int WRING = 2 * QBYTES;        // the W_n' ring follows the Q ring
+  constexpr int QDMA = QDATA / 1024;       // 1 KB DMA blocks: two Q rows ...
+  constexpr int WDMA = WBYTES / 1024;      // ... or 16 W_n' rows
   static_assert(KS == 2 * NB, "the two products interleave step for step");
-  static_assert(QDATA % 16 == 0, "bias vectors aligned");
+  static_assert(KS == 16 && QDMA % kWaves == 0 && WDMA % kWaves == 0, "DMA split");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * QBYTES + 2 * WBYTES];
   const uint32_t smem_base =
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
@@ -109,46 +112,36 @@ void chain_kernel(ChainLaunch a) {
   const int nc = m / kMC;
   const int64_t row0w = (int64_t)blockIdx.x * kTileRows + 32 * wave + r32;
 
-  // DMA: 1 KB block blk of a Q slot holds padded Q rows then the bias; wave w
-  // issues blocks w, w + 4, ... Lane i of a block fills byte 16 i of it: the
-  // row's vector there, or (pad and tail bytes, never read) a copy of the
-  // chunk's first vector; lanes over the bias bytes stay off, and the last
-  // wave fills them from q. Offsets are recomputed per issue (a few integer
-  // ops) rather than held in registers, which the two products' operands and
-  // accumulators fill.
+  // DMA block blk = wave + 4 d. Q: lane i fills row 2 blk + (i >> 5), slot
+  // i & 31, whose vector is (i & 31) ^ ((2 blk + (i >> 5)) & 15)
+  // = (i & 31) ^ x ^ 8 (d & 1) with x = (2 wave + (i >> 5)) & 15 < 8.
+  // W_n': lane i fills row 16 blk + (i >> 2), slot i & 3, vector
+  // (i & 3) ^ ((i >> 4) & 3).
   const unsigned char* const qbase = static_cast<const unsigned char*>(a.Q);
   const unsigned char* const wbase = static_cast<const unsigned char*>(a.Wp);
   const unsigned char* const bbase = reinterpret_cast<const unsigned char*>(a.q);
+  const uint32_t qlane =
+      (uint32_t)((lane >> 5) * QROWB + 16 * ((lane & 31) ^ ((2 * wave + (lane >> 5)) & 15)));
+  const uint32_t wlane =
+      (uint32_t)((lane >> 2) * m * 2 + 16 * ((lane & 3) ^ ((lane >> 4) & 3)));
   auto issue_q = [&](int j) __attribute__((always_inline)) {
     const int slot = j & 1;
-    const unsigned char* qb = qbase + (int64_t)j * kMC * a.d_in * 2;
 #pragma unroll
-    for (int d = 0; d < (QDMA + kWaves - 1) / kWaves; ++d) {
+    for (int d = 0; d < QDMA / kWaves; ++d) {
       const int blk = wave + kWaves * d;
-      if (blk >= QDMA) break;  // wave-uniform
-      const int p = blk * 1024 + 16 * lane;
-      const int r = p / QROW, c = p % QROW;
-      uint32_t off = 0;
-      if (r < kMC && c < KS * 32) off = (uint32_t)((r * a.d_in) * 2 + c);
-      if (p < QDATA || p >= QDATA + kMC * 4)
-        dma16(qb, off, __builtin_amdgcn_readfirstlane(smem_base + slot * QBYTES + blk * 1024));
+      dma16(qbase + (int64_t)j * QDATA + blk * 1024, (d & 1) ? (qlane ^ 128u) : qlane,
+            __builtin_amdgcn_readfirstlane(smem_base + slot * QBYTES + blk * 1024));
     }
     if (wave == kWaves - 1 && lane < kMC / 4)
-      dma16(bbase, (uint32_t)(j * kMC * 4 + 16 * lane),
+      dma16(bbase + j * kMC * 4, (uint32_t)(16 * lane),
             __builtin_amdgcn_readfirstlane(smem_base + slot * QBYTES + QDATA));
   };
   auto issue_w = [&](int j) __attribute__((always_inline)) {
     const int slot = j & 1;
-    const unsigned char* wb = wbase + (int64_t)j * kMC * 2;
 #pragma unroll
-    for (int d = 0; d < (WDMA + kWaves - 1) / kWaves; ++d) {
+    for (int d = 0; d < WDMA / kWaves; ++d) {
       const int blk = wave + kWaves * d;
-      if (blk >= WDMA) break;  // wave-uniform
-      const int p = blk * 1024 + 16 * lane;
-      const int n = p / WROW, c = p % WROW;
-      uint32_t off = 0;
-      if (n < NB * 32 && c < 64) off = (uint32_t)(n * m * 2 + c);
-      dma16(wb, off,
+      dma16(wbase + j * WROWB + (int64_t)blk * 16 * m * 2, wlane,
             __builtin_amdgcn_readfirstlane(smem_base + WRING + slot * WBYTES + blk * 1024));
     }
   };
@@ -173,15 +166,18 @@ void chain_kernel(ChainLaunch a) {
   f32x16 acc1;
   u32x4 pa[2];
 
-  const int qoff = r32 * QROW + 16 * h;
-  const int woff = WRING + r32 * WROW + 16 * h;
+  // Q fragment of k-step ks: row r32, vector 2 ks + h, i.e. byte
+  // r32 * QROWB + 16 ((2 ks + h) ^ (r32 & 15)) = qa ^ 32 ks.
+  const int qa = r32 * QROWB + 16 * (h ^ (r32 & 15));
+  // W_n' fragment of step t: row 32 (t >> 1) + r32, vector 2 (t & 1) + h.
+  const int wb0 = WRING + r32 * WROWB + 16 * (h ^ ((r32 >> 2) & 3));
+  const int wb1 = WRING + r32 * WROWB + 16 * ((2 + h) ^ ((r32 >> 2) & 3));
   auto read_q = [&](int slot, int ks) __attribute__((always_inline)) {
-    return *reinterpret_cast<const u32x4*>(smem + slot * QBYTES + qoff + 32 * ks);
+    return *reinterpret_cast<const u32x4*>(smem + slot * QBYTES + (qa ^ (32 * ks)));
   };
-  // Step t of the second product: output block t / 2, k-step t % 2.
   auto read_w = [&](int slot, int t) __attribute__((always_inline)) {
-    return *reinterpret_cast<const u32x4*>(smem + slot * WBYTES + woff +
-                                           32 * (t >> 1) * WROW + 32 * (t & 1));
+    return *reinterpret_cast<const u32x4*>(smem + slot * WBYTES + ((t & 1) ? wb1 : wb0) +
+                                           32 * WROWB * (t >> 1));
   };
   auto zero_acc1 = [&]() __attribute__((always_inline)) {
 #pragma unroll
