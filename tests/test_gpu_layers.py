@@ -67,8 +67,11 @@ def test_embed_all_full(orc, wl, dataflow):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+# (256, m, 256) in bf16, dense then pool, runs the chained transform: m = 32
+# (one chunk), 96 (an odd chunk count), 512 and 2048 (the largest m it takes).
 @pytest.mark.parametrize("dims", [(64, 64, 64), (256, 512, 256), (128, 96, 512), (48, 2048, 128),
-                                  (64, 80, 400), (96, 160, 272)])
+                                  (64, 80, 400), (96, 160, 272), (256, 32, 256), (256, 96, 256),
+                                  (256, 2048, 256)])
 @pytest.mark.parametrize("dataflow", DATAFLOWS)
 def test_convolve_layer_self_rows(orc, dtype, dims, dataflow):
     import paper_1806_01973_amd as ps
