@@ -32,10 +32,10 @@
 // XOR-swizzled so that the 16 lanes of a fragment read fall on distinct banks
 // (padding the rows instead, as measured, costs 7%: a fifth more W_n' DMA bytes
 // into the LDS, whose bandwidth bounds this kernel, and per-DMA offset
-// arithmetic). The first product of chunk j + 1 and the
-// second of chunk j run interleaved, step by step, so the matrix pipe never
-// waits for the bias/ReLU/rounding of a chunk. R is accumulated in fp32 over
-// the chunks in order and rounded once to bf16.
+// arithmetic). The first product of chunk j + 1 and the second of chunk j run
+// interleaved, step by step, so the matrix pipe never waits for the
+// bias/ReLU/rounding of a chunk. R is accumulated in fp32 over the chunks in
+// order and rounded once to bf16.
 #include "device_util.h"
 #include "kernels.h"
 
