@@ -440,7 +440,8 @@ def bench_embed_all(args, wl, inp):
     # Larger ones run in order: their walks are bound by dependent random reads
     # and slow down beside the transform by about as much as it would save
     # (the library would overlap the shard's chained first layer, but at
-    # 2/8 of the CUs that measured 1341 against 1349 ms per step).
+    # 2/8 of the CUs that measured 1345 ms per step against 1341-1351 in order
+    # on the same box, within the spread of runs).
     overlapped = bool(args.overlap) and (1 << 18) <= wl.num_pins <= (1 << 22)
     job = ps.EmbedAll(inp["g"], inp["layers"], wl.walks, wl.hops, wl.T, wl.seed,
                       weights=wl.name != "shard", overlap=args.overlap if overlapped else 0)
