@@ -177,6 +177,40 @@ def random_read_calibration(table_gib: int = 16, steps: int = 32, reps: int = 3)
     print(json.dumps(out), flush=True)
 
 
+def random_gather_calibration(targets: int = 8_000_000, reps: int = 3) -> None:
+    """Random row gathers per second in the importance pool's access pattern
+    (the library's calibration kernel): 512-byte rows from tables of 1, 4 and
+    16 GiB and from one the size of the 100M-node shard's R table (80M rows),
+    50 rows per target, and 1 KB rows from a table of the same size, 32 rows per
+    target."""
+    import torch
+    from paper_1806_01973_amd import _lib
+    L = _lib.lib()
+    shard_r = 80_000_000 * 512
+    table = torch.empty(shard_r, dtype=torch.uint8, device="cuda")  # never written
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {"targets": targets, "reps": reps}
+    for name, nbytes, rb, per in (("512B_1GiB", 1 << 30, 512, 50), ("512B_4GiB", 4 << 30, 512, 50),
+                                  ("512B_16GiB", 16 << 30, 512, 50),
+                                  ("512B_shardR", shard_r, 512, 50), ("1KB_shardR", shard_r, 1024, 32)):
+        def launch():
+            _lib.check(L.pinsage_profile_random_gathers(table.data_ptr(), nbytes, rb, targets, per,
+                                                        1, sink.data_ptr(), stream.cuda_stream),
+                       "random gathers")
+        launch()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            launch()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[f"gather_GBs_{name}"] = targets * per * rb / (ms * 1e-3) / 1e9
+        out[f"ms_{name}"] = ms
+    print(json.dumps(out), flush=True)
+
+
 def load_inputs(wl, dataflow="pool_then_dense", pool="importance"):
     """Inputs on the GPU plus host views the CPU baseline needs."""
     import numpy as np
@@ -858,6 +892,9 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--random-read-calibration", action="store_true",
                     help="dependent random reads/s from a 16 GiB table (the walks' ceiling)")
+    ap.add_argument("--gather-calibration", action="store_true",
+                    help="random 512-byte and 1 KB row gathers/s in the pool's pattern (the "
+                         "pool's ceiling)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -872,6 +909,9 @@ def main() -> int:
         return 0
     if args.random_read_calibration:
         random_read_calibration()
+        return 0
+    if args.gather_calibration:
+        random_gather_calibration()
         return 0
     if args.layer:
         return layer_probe(args)

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define PINSAGE_ABI_VERSION 11
+#define PINSAGE_ABI_VERSION 12
 
 enum {
   PINSAGE_OK = 0,
@@ -507,6 +507,28 @@ int pinsage_profile_read(int kernel, int64_t* launches, double* total_ms);
  * or 16, a table smaller than one element, or steps or chains below 1. */
 int pinsage_profile_random_reads(const void* table, size_t table_bytes, int32_t elem_bytes,
                                  int32_t steps, uint32_t* sink, int64_t chains, void* stream);
+
+/* Random row gathers (bench support, not part of the method): the rate at
+ * which whole rows are gathered from uniformly random positions of a table,
+ * in the access pattern of the importance pool (Sec. 3.2, Algorithm 1 line 1:
+ * a target's neighbour rows, gathered at unrelated positions). Target t
+ * (t < targets) gathers per_target rows; slot s takes row
+ * (h * rows) >> 32, h the high 32 bits of the SplitMix64 finaliser of
+ * seed + 64 t + s, rows = table_bytes / row_bytes. A wave takes one target at
+ * a time and issues all of its loads (two 512-byte rows or one 1 KB row per
+ * instruction) before it consumes any.
+ * table: device, 16-byte aligned, table_bytes bytes, contents arbitrary
+ *   (never written); row_bytes: 512 or 1024; targets >= 1;
+ *   1 <= per_target <= 64 (512-byte rows) or 32 (1 KB rows);
+ * sink: device uint32, the caller's value plus every gathered 32-bit word
+ *   (mod 2^32); the caller zeroes it. Asynchronous on `stream`; time it with
+ *   events on that stream.
+ * Errors: PINSAGE_EINVAL for a NULL pointer, a misaligned table, another row
+ * size, a table smaller than one row or counts out of range;
+ * PINSAGE_EUNSUPPORTED for 2^32 rows or more. */
+int pinsage_profile_random_gathers(const void* table, size_t table_bytes, int32_t row_bytes,
+                                   int64_t targets, int32_t per_target, uint64_t seed,
+                                   uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,7 @@ EXPORTED = [
     "pinsage_output_mlp", "pinsage_max_margin_loss",
     "pinsage_minibatch_workspace_size", "pinsage_minibatch_forward",
     "pinsage_profile_enable", "pinsage_profile_read", "pinsage_profile_random_reads",
-    "pinsage_walk_table_size", "pinsage_build_walk_table",
+    "pinsage_profile_random_gathers", "pinsage_walk_table_size", "pinsage_build_walk_table",
 ]
 
 
@@ -157,6 +157,9 @@ def lib():
     L.pinsage_profile_random_reads.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
                                                ctypes.c_void_p]
+    L.pinsage_profile_random_gathers.argtypes = [ctypes.c_void_p, ctypes.c_size_t,
+                                                 ctypes.c_int32, ctypes.c_int64, ctypes.c_int32,
+                                                 ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
     L.pinsage_walk_table_size.argtypes = [ctypes.POINTER(Graph), ctypes.POINTER(ctypes.c_size_t)]
     L.pinsage_build_walk_table.argtypes = [ctypes.POINTER(Graph), P, ctypes.c_size_t, P]
     for name in EXPORTED:

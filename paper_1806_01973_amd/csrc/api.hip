@@ -1252,6 +1252,29 @@ int pinsage_profile_random_reads(const void* table, size_t table_bytes, int32_t 
   return PINSAGE_OK;
 }
 
+int pinsage_profile_random_gathers(const void* table, size_t table_bytes, int32_t row_bytes,
+                                   int64_t targets, int32_t per_target, uint64_t seed,
+                                   uint32_t* sink, void* stream) {
+  g_last_error.clear();
+  if (!table || !sink) return fail(PINSAGE_EINVAL, "NULL table or sink");
+  if (row_bytes != 512 && row_bytes != 1024)
+    return fail(PINSAGE_EINVAL, "row size %d (512 or 1024)", row_bytes);
+  if (reinterpret_cast<uintptr_t>(table) % 16 != 0)
+    return fail(PINSAGE_EINVAL, "table not 16-byte aligned");
+  const uint64_t rows = table_bytes / (size_t)row_bytes;
+  if (rows < 1) return fail(PINSAGE_EINVAL, "table smaller than one row");
+  if (rows >= (1ull << 32)) return fail(PINSAGE_EUNSUPPORTED, "%llu rows (< 2^32)",
+                                        (unsigned long long)rows);
+  const int max_per = row_bytes == 512 ? 64 : 32;
+  if (targets < 1 || per_target < 1 || per_target > max_per)
+    return fail(PINSAGE_EINVAL, "targets %lld, rows per target %d (1..%d)", (long long)targets,
+                per_target, max_per);
+  hipError_t e = launch_random_gathers(table, rows, row_bytes, targets, per_target, seed, sink,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "random gather launch");
+  return PINSAGE_OK;
+}
+
 int pinsage_output_mlp_workspace_size(const pinsage_mlp_t* mlp, int64_t n, size_t* bytes) {
   g_last_error.clear();
   int st = check_mlp(mlp);

@@ -217,6 +217,11 @@ hipError_t launch_chain(const ChainLaunch& a, hipStream_t s);
 // `elements` (a power of two) elements of elem_bytes (4, 8 or 16) bytes.
 hipError_t launch_random_reads(const void* table, uint64_t elements, int elem_bytes, int steps,
                                uint32_t* sink, int64_t chains, hipStream_t s);
+// Random row gathers (bench support): targets x per rows of row_bytes (512 or
+// 1024) from `rows` rows at hashed positions; every word is added into *sink.
+hipError_t launch_random_gathers(const void* table, uint64_t rows, int row_bytes,
+                                 int64_t targets, int per, uint64_t seed, uint32_t* sink,
+                                 hipStream_t s);
 
 // Max-margin loss (Eq. 1): per_pair[b] = mean over the shared negatives and
 // pair b's present hard negatives of max(0, zq.zn - zq.zpos + margin),

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 def test_version_and_status_strings(L):
     lib = L.lib()
-    assert lib.pinsage_version() == 11
+    assert lib.pinsage_version() == 12
     for code in (0, -1, -2, -3, -4):
         assert lib.pinsage_status_string(code)
     assert lib.pinsage_status_string(-99) == b"unknown status"
@@ -263,6 +263,24 @@ def test_random_read_calibration_validation(L):
     assert f(FAKE, 1 << 20, 16, 8, FAKE, 0, None) == E
     assert f(FAKE, 1 << 20, 12, 8, FAKE, 256, None) == E
     assert b"element size 12" in lib.pinsage_last_error()
+
+
+def test_random_gather_calibration_validation(L):
+    lib = L.lib()
+    E = L.PINSAGE_EINVAL
+    f = lib.pinsage_profile_random_gathers
+    assert f(None, 1 << 20, 512, 8, 50, 1, FAKE, None) == E
+    assert f(FAKE, 1 << 20, 512, 8, 50, 1, None, None) == E
+    for rb in (0, 256, 768, 2048):
+        assert f(FAKE, 1 << 20, rb, 8, 50, 1, FAKE, None) == E
+    assert b"row size 2048" in lib.pinsage_last_error()
+    assert f(FAKE + 8, 1 << 20, 512, 8, 50, 1, FAKE, None) == E  # misaligned
+    assert f(FAKE, 511, 512, 8, 50, 1, FAKE, None) == E  # smaller than one row
+    assert f(FAKE, 1 << 20, 512, 0, 50, 1, FAKE, None) == E
+    assert f(FAKE, 1 << 20, 512, 8, 0, 1, FAKE, None) == E
+    assert f(FAKE, 1 << 20, 512, 8, 65, 1, FAKE, None) == E
+    assert f(FAKE, 1 << 20, 1024, 8, 33, 1, FAKE, None) == E
+    assert f(FAKE, 512 << 32, 512, 8, 8, 1, FAKE, None) == L.PINSAGE_EUNSUPPORTED  # 2^32 rows
 
 
 def test_minibatch_validation_and_workspace(L):

@@ -1,7 +1,11 @@
-"""GPU: the random-read calibration kernel (bench support) follows the chains
-it documents -- every lane's reads land where a host replay of the same
-hash chain says, for 4-, 8- and 16-byte elements, and it validates its
-arguments on the device path too."""
+"""GPU: the calibration kernels (bench support) read what they document.
+
+* Random reads: every lane's reads land where a host replay of the same hash
+  chain says, for 4-, 8- and 16-byte elements.
+* Random row gathers: the sum of every gathered word equals a host replay of
+  the documented row positions, for 512-byte and 1 KB rows, with targets
+  spanning several rounds of the grid.
+"""
 
 import ctypes
 
@@ -59,3 +63,38 @@ def test_chains_match_host_replay(eb):
         elements *= 2
     ref = _replay(words, eb, chains, steps, elements)
     np.testing.assert_array_equal(sink.cpu().numpy().view(np.uint32), ref)
+
+
+def _mix64_np(x):
+    x = x ^ (x >> np.uint64(30))
+    x = x * np.uint64(0xbf58476d1ce4e5b9)
+    x = x ^ (x >> np.uint64(27))
+    x = x * np.uint64(0x94d049bb133111eb)
+    return x ^ (x >> np.uint64(31))
+
+
+@pytest.mark.parametrize("row_bytes,rows,targets,per", [(512, 1000, 3001, 50), (512, 777, 40000, 64),
+                                                        (1024, 1000, 3001, 32), (1024, 513, 40000, 7)])
+def test_gathers_match_host_replay(row_bytes, rows, targets, per):
+    from paper_1806_01973_amd import _lib
+    L = _lib.lib()
+    rng = np.random.default_rng(row_bytes + per)
+    wpr = row_bytes // 4
+    words = rng.integers(0, 2**32, size=rows * wpr + 5, dtype=np.uint32)  # 20 bytes past the rows
+    table = torch.from_numpy(words.view(np.int32)).cuda()
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    seed = 0x1234_5678_9ABC
+    print(f"[case] random-gather calibration {row_bytes} B rows, {rows} rows, {targets} x {per}",
+          flush=True)
+    st = L.pinsage_profile_random_gathers(table.data_ptr(), words.nbytes, row_bytes, targets, per,
+                                          seed, sink.data_ptr(), None)
+    assert st == 0, L.pinsage_last_error()
+    torch.cuda.synchronize()
+    with np.errstate(over="ignore"):
+        keys = (np.uint64(seed) + np.uint64(64) * np.arange(targets, dtype=np.uint64)[:, None]
+                + np.arange(per, dtype=np.uint64)[None, :])
+        h = _mix64_np(keys) >> np.uint64(32)
+        idx = (h * np.uint64(rows)) >> np.uint64(32)
+    row_sums = words[:rows * wpr].reshape(rows, wpr).astype(np.uint64).sum(axis=1)
+    ref = int(row_sums[idx.ravel()].sum()) & 0xFFFFFFFF
+    assert int(sink.cpu().numpy().view(np.uint32)[0]) == ref
