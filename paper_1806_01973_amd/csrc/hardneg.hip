@@ -168,16 +168,33 @@ __device__ __forceinline__ int block_exclusive_sum(int v, int wave, int lane, in
   return before + incl - v;
 }
 
+// MurmurHash3's 32-bit finaliser (a bijection with good avalanche).
+__device__ __forceinline__ uint32_t fmix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x85ebca6bu;
+  x ^= x >> 13;
+  x *= 0xc2b2ae35u;
+  x ^= x >> 16;
+  return x;
+}
+// Partition of a pin among `parts` (the global path's buckets).
+__device__ __forceinline__ uint32_t part_of(uint32_t v, uint32_t parts) {
+  return (uint32_t)(((uint64_t)fmix32(v) * parts) >> 32);
+}
+
 // The walks of query u (Sec. 3.2, as the neighbourhood walks): kWalkers walks
 // per thread in lockstep (w0, w0 + 1024, ...), so their dependent reads
 // overlap; walk w's pin landings go to slots[w * hops ..]. TABLE: each edge
 // step reads one 16-byte walk-table entry (the neighbour's id, degree and row
 // start) instead of the current node's offsets and then a neighbour id; the
 // source's row comes from its offsets, validated as pick() validates a row.
-// Returns this thread's edge steps.
-template <typename OffT, bool TABLE>
+// HIST: every recorded landing (a pin other than u) also adds one to
+// part_hist[part_of(pin, parts)] in LDS. Returns this thread's edge steps.
+template <typename OffT, bool TABLE, bool HIST = false>
 __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u, int tid,
-                                               uint32_t* slots, uint32_t k0, uint32_t k1) {
+                                               uint32_t* slots, uint32_t k0, uint32_t k1,
+                                               uint32_t* part_hist = nullptr,
+                                               uint32_t parts = 0) {
   const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
   const int32_t* __restrict__ col = a.col;
   const uint4* __restrict__ tab = static_cast<const uint4*>(a.table);
@@ -212,7 +229,11 @@ __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u
         any = false;
 #pragma unroll
         for (int i = 0; i < kWalkers; ++i) {
+          const int before = W[i].landed;
           W[i].land_entry(e[i], a.num_pins, a.num_nodes, a.hops);
+          if constexpr (HIST)
+            if (W[i].landed > before && W[i].cur != W[i].u)
+              atomicAdd(&part_hist[part_of((uint32_t)W[i].cur, parts)], 1u);
           any = any || W[i].active;
         }
       } else {
@@ -234,7 +255,11 @@ __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u
         any = false;
 #pragma unroll
         for (int i = 0; i < kWalkers; ++i) {
+          const int before = W[i].landed;
           W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
+          if constexpr (HIST)
+            if (W[i].landed > before && W[i].cur != W[i].u)
+              atomicAdd(&part_hist[part_of((uint32_t)W[i].cur, parts)], 1u);
           any = any || W[i].active;
         }
       }
@@ -392,10 +417,11 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
 // workgroup per query (grid-stride; each workgroup reuses its own workspace):
 //   W. the walks write their landings to a buffer at slot walk * hops + hop,
 //      as the on-chip kernel does in LDS (empty marker for the query itself
-//      and for slots a walk did not reach): no atomics on the walks' path;
-//   B. the landings are bucketed by hash partition of the pin (a histogram
-//      sweep and a scatter sweep of the buffer, one LDS atomic per distinct
-//      partition of a wave);
+//      and for slots a walk did not reach), and add each recorded landing to
+//      its hash partition's count in LDS (the walks wait on memory, the LDS
+//      atomics cost them nothing measurable);
+//   B. the landings are bucketed by partition (a scatter sweep of the buffer,
+//      one LDS atomic per distinct partition of a wave);
 //   C. each bucket is counted in an LDS table (12,288 slots; a partition holds
 //      about 8,192 landings, so at most two thirds of the slots when every
 //      landing is a distinct pin), and each partition's (pin, count) pairs
@@ -425,20 +451,8 @@ constexpr int kMaxParts = 512;   // partitions of the largest budget (2^22 landi
 static_assert(kCSlots % kThreads == 0, "whole waves sweep the table");
 static_assert(2 * kCSlots * 4 >= kGMaxRank * 8 + kGMaxRank * 4, "top and cls fit the table");
 
-// MurmurHash3's 32-bit finaliser (a bijection with good avalanche).
-__device__ __forceinline__ uint32_t fmix32(uint32_t x) {
-  x ^= x >> 16;
-  x *= 0x85ebca6bu;
-  x ^= x >> 13;
-  x *= 0xc2b2ae35u;
-  x ^= x >> 16;
-  return x;
-}
-// Partition of a pin among `parts`, its half in a split of `split` (a power of
-// two) and its home slot in the LDS table: three unrelated hashes of the id.
-__device__ __forceinline__ uint32_t part_of(uint32_t v, uint32_t parts) {
-  return (uint32_t)(((uint64_t)fmix32(v) * parts) >> 32);
-}
+// Its half in a split of `split` (a power of two) and its home slot in the
+// LDS table: two more hashes of the id, unrelated to part_of's.
 __device__ __forceinline__ uint32_t split_of(uint32_t v, uint32_t split) {
   return fmix32(v ^ 0x9e3779b9u) & (split - 1);
 }
@@ -566,10 +580,12 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     const int64_t u = (int64_t)a.queries[qi];
     const bool live = u >= 0 && u < a.num_nodes;
     if (tid < 8) sh_i32[tid] = 0;
+    for (uint32_t b = tid; b < parts; b += kThreads) hist[b] = 0u;
+    __syncthreads();
 
-    // ---- W. walks, landings into the buffer ------------------------------
+    // ---- W. walks, landings into the buffer, partition histogram in LDS ----
     if (live) {
-      my_steps += walk_query<OffT, TABLE>(a, u, tid, buf, k0, k1);
+      my_steps += walk_query<OffT, TABLE, true>(a, u, tid, buf, k0, k1, hist, parts);
     } else {
       for (int64_t i = tid; i < L; i += kThreads) buf[i] = kEmpty;
     }
@@ -595,12 +611,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
       for (int64_t i = 4 * L4 + tid; i < 4 * L4 + kThreads; i += kThreads)
         visit(i < L ? buf[i] : kEmpty);
     };
-    for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
-    __syncthreads();
-    sweep([&](uint32_t v) {
-      wave_hist_add(hist, v == kEmpty ? 0u : part_of(v, parts), v != kEmpty);
-    });
-    __syncthreads();
+    // hist[p] holds partition p's landings, counted as the walks recorded them.
     if (tid == 0) {
       uint32_t run = 0;
       for (uint32_t p = 0; p < parts; ++p) {
