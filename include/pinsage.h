@@ -234,9 +234,12 @@ typedef struct {
 
 /* Workspace bytes pinsage_hard_negatives needs for these parameters and
  * query count: 0 for walks * hops <= 16384 (the visits of a query are counted
- * on chip); above that, per resident workgroup (at most 256), the query's
- * landings twice (by walk, then by hash partition) and a list of its
- * (pin, count) pairs: 16 bytes per landing, rounded up to 256 bytes. Errors as for pinsage_hard_negatives' parameters. */
+ * on chip); above that, per resident workgroup (at most 256), L = walks * hops
+ * landings of a query: a bucket of 12,288 landings for each of its
+ * ceil(L / 8192) hash partitions, an overflow list of up to L landings and its
+ * copy by partition, and a list of up to L (pin, count) pairs:
+ * 4 (12288 ceil(L / 8192) + 4 L) bytes, rounded up to 256 bytes. Errors as for
+ * pinsage_hard_negatives' parameters. */
 int pinsage_hard_negatives_workspace_size(const pinsage_hard_negative_params_t* params,
                                           int64_t num_queries, size_t* bytes);
 

@@ -182,19 +182,38 @@ __device__ __forceinline__ uint32_t part_of(uint32_t v, uint32_t parts) {
   return (uint32_t)(((uint64_t)fmix32(v) * parts) >> 32);
 }
 
+constexpr int kCPerPart = 8192;  // landings per hash partition (on average at most)
+constexpr int kCCap = 12288;     // bucket capacity of a partition in the workspace
+
 // The walks of query u (Sec. 3.2, as the neighbourhood walks): kWalkers walks
 // per thread in lockstep (w0, w0 + 1024, ...), so their dependent reads
 // overlap; walk w's pin landings go to slots[w * hops ..]. TABLE: each edge
 // step reads one 16-byte walk-table entry (the neighbour's id, degree and row
 // start) instead of the current node's offsets and then a neighbour id; the
 // source's row comes from its offsets, validated as pick() validates a row.
-// HIST: every recorded landing (a pin other than u) also adds one to
-// part_hist[part_of(pin, parts)] in LDS. Returns this thread's edge steps.
-template <typename OffT, bool TABLE, bool HIST = false>
+// Returns this thread's edge steps.
+// BUCKET (the global path): a landing is not written to slots; a recorded one
+// (a pin p other than u) goes straight to its hash partition's bucket,
+// bk.buckets[part * kCCap + n] with n from that partition's LDS cursor, or,
+// once the bucket holds kCCap, to the overflow list (its own LDS cursor).
+struct Buckets {
+  uint32_t* cursor;   // LDS [parts], zeroed
+  uint32_t parts;
+  uint32_t* buckets;  // [parts][kCCap]
+  uint32_t* ovf;      // >= walks * hops words
+  int* ovf_n;         // LDS, zeroed
+};
+__device__ __forceinline__ void bucket_append(const Buckets& bk, uint32_t v) {
+  if (v == kEmpty) return;  // the query itself
+  const uint32_t p = part_of(v, bk.parts);
+  const uint32_t n = atomicAdd(&bk.cursor[p], 1u);
+  if (n < (uint32_t)kCCap) bk.buckets[(int64_t)p * kCCap + n] = v;
+  else bk.ovf[atomicAdd(bk.ovf_n, 1)] = v;
+}
+template <typename OffT, bool TABLE, bool BUCKET = false>
 __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u, int tid,
                                                uint32_t* slots, uint32_t k0, uint32_t k1,
-                                               uint32_t* part_hist = nullptr,
-                                               uint32_t parts = 0) {
+                                               const Buckets& bk = Buckets{}) {
   const OffT* __restrict__ off = static_cast<const OffT*>(a.row_offsets);
   const int32_t* __restrict__ col = a.col;
   const uint4* __restrict__ tab = static_cast<const uint4*>(a.table);
@@ -229,11 +248,16 @@ __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u
         any = false;
 #pragma unroll
         for (int i = 0; i < kWalkers; ++i) {
-          const int before = W[i].landed;
-          W[i].land_entry(e[i], a.num_pins, a.num_nodes, a.hops);
-          if constexpr (HIST)
-            if (W[i].landed > before && W[i].cur != W[i].u)
-              atomicAdd(&part_hist[part_of((uint32_t)W[i].cur, parts)], 1u);
+          if constexpr (BUCKET) {
+            // land_entry without the slot write.
+            uint32_t v;
+            if (W[i].advance((int32_t)e[i].x, a.num_pins, a.num_nodes, a.hops, &v))
+              bucket_append(bk, v);
+            W[i].deg = (int32_t)e[i].y;
+            W[i].lo = (int64_t)(((uint64_t)e[i].w << 32) | (uint64_t)e[i].z);
+          } else {
+            W[i].land_entry(e[i], a.num_pins, a.num_nodes, a.hops);
+          }
           any = any || W[i].active;
         }
       } else {
@@ -255,17 +279,21 @@ __device__ __forceinline__ uint32_t walk_query(const HardNegLaunch& a, int64_t u
         any = false;
 #pragma unroll
         for (int i = 0; i < kWalkers; ++i) {
-          const int before = W[i].landed;
-          W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
-          if constexpr (HIST)
-            if (W[i].landed > before && W[i].cur != W[i].u)
-              atomicAdd(&part_hist[part_of((uint32_t)W[i].cur, parts)], 1u);
+          if constexpr (BUCKET) {
+            uint32_t v;
+            if (W[i].advance(nx[i], a.num_pins, a.num_nodes, a.hops, &v)) bucket_append(bk, v);
+          } else {
+            W[i].land(nx[i], a.num_pins, a.num_nodes, a.hops);
+          }
           any = any || W[i].active;
         }
       }
     }
 #pragma unroll
-    for (int i = 0; i < kWalkers; ++i) steps += W[i].finish(a.hops);
+    for (int i = 0; i < kWalkers; ++i) {
+      if constexpr (BUCKET) steps += W[i].exists ? (uint32_t)W[i].s : 0u;  // no slots to pad
+      else steps += W[i].finish(a.hops);
+    }
   }
   return steps;
 }
@@ -415,16 +443,16 @@ __global__ __launch_bounds__(kThreads) void hard_negative_kernel(HardNegLaunch a
 // ---------------------------------------------------------------------------
 // Walk budgets above the LDS slots (walks * hops > 16384). One 1024-thread
 // workgroup per query (grid-stride; each workgroup reuses its own workspace):
-//   W. the walks write their landings to a buffer at slot walk * hops + hop,
-//      as the on-chip kernel does in LDS (empty marker for the query itself
-//      and for slots a walk did not reach), and add each recorded landing to
-//      its hash partition's count in LDS (the walks wait on memory, the LDS
-//      atomics cost them nothing measurable);
-//   B. the landings are bucketed by partition (a scatter sweep of the buffer,
-//      one LDS atomic per distinct partition of a wave);
-//   C. each bucket is counted in an LDS table (12,288 slots; a partition holds
-//      about 8,192 landings, so at most two thirds of the slots when every
-//      landing is a distinct pin), and each partition's (pin, count) pairs
+//   W. each recorded landing (a pin other than the query) goes straight to the
+//      bucket of its hash partition in the workspace, at the slot the
+//      partition's LDS cursor hands out (the walks wait on memory, the LDS
+//      atomics cost them nothing measurable); a partition holds about 8,192
+//      landings, and those past a full bucket (12,288) go to an overflow list;
+//   B. the overflow list, if any, is bucketed by partition (a histogram sweep
+//      and a scatter sweep, one LDS atomic per distinct partition of a wave);
+//   C. each partition (its bucket, then its overflow landings) is counted in
+//      an LDS table (12,288 slots: at most two thirds full at the average
+//      partition size when every landing is a distinct pin), and its (pin, count) pairs
 //      are appended to a compact list; a
 //      pin that finds no slot within 64 linear probes marks its partition as
 //      overflowing, which is then split in two by a second hash and counted
@@ -445,7 +473,6 @@ constexpr int kGMaxRank = 8192;  // rank_hi limit of this path
 constexpr int kGBins = 4096;
 constexpr uint32_t kNoKey = 0xFFFFFFFFu;
 constexpr int kCSlots = 12288;   // LDS counting table: keys then counts (96 KB)
-constexpr int kCPerPart = 8192;  // landings per hash partition
 constexpr int kCProbes = 64;     // linear probes before a partition counts as overflowing
 constexpr int kMaxParts = 512;   // partitions of the largest budget (2^22 landings)
 static_assert(kCSlots % kThreads == 0, "whole waves sweep the table");
@@ -565,15 +592,19 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
   uint64_t* top = reinterpret_cast<uint64_t*>(pool);
   uint32_t* cls = pool + 2 * kGMaxRank;
   const int64_t L = (int64_t)a.walks * a.hops;
-  uint32_t* buf = ws + (int64_t)blockIdx.x * ws_words;  // L landings, by (walk, hop)
-  uint32_t* sorted = buf + L;                           // the landings, by partition
-  uint32_t* list = sorted + L;                          // up to L (pin, count) pairs
   const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFull);
   const uint32_t k1 = (uint32_t)(a.seed >> 32);
   const int tid = threadIdx.x;
   const int R = a.rank_hi;
   const uint32_t parts = (uint32_t)((L + kCPerPart - 1) / kCPerPart);  // <= kMaxParts
-  __shared__ uint32_t pstart[kMaxParts + 1];
+  // This workgroup's workspace: the partitions' buckets, the overflow list,
+  // the overflow list by partition, and the (pin, count) list.
+  uint32_t* buckets = ws + (int64_t)blockIdx.x * ws_words;  // [parts][kCCap]
+  uint32_t* ovf = buckets + (int64_t)parts * kCCap;          // up to L landings
+  uint32_t* ovf_sorted = ovf + L;                           // the same, by partition
+  uint32_t* list = ovf_sorted + L;                          // up to L (pin, count) pairs
+  __shared__ uint32_t pstart[kMaxParts + 1];  // overflow landings by partition
+  __shared__ uint32_t pcount[kMaxParts];      // landings in each partition's bucket
   uint32_t my_steps = 0;
 
   for (int64_t qi = blockIdx.x; qi < a.num_queries; qi += gridDim.x) {
@@ -583,50 +614,52 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     for (uint32_t b = tid; b < parts; b += kThreads) hist[b] = 0u;
     __syncthreads();
 
-    // ---- W. walks, landings into the buffer, partition histogram in LDS ----
+    // ---- W. walks, landings into their partitions' buckets -----------------
     if (live) {
-      my_steps += walk_query<OffT, TABLE, true>(a, u, tid, buf, k0, k1, hist, parts);
-    } else {
-      for (int64_t i = tid; i < L; i += kThreads) buf[i] = kEmpty;
+      const Buckets bk{hist, parts, buckets, ovf, &sh_i32[7]};
+      // (The walkers' slots are never written in this mode.)
+      my_steps += walk_query<OffT, TABLE, true>(a, u, tid, ovf, k0, k1, bk);
     }
     __syncthreads();
-    // The buffer was written through L2 by other waves: drop this CU's cached
-    // lines of it before reading.
+    // The buckets were written through L2 by other waves: drop this CU's
+    // cached lines of them before reading.
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-
-    // ---- B. bucket the landings by partition --------------------------------
-    // Whole waves sweep the buffer in 16-byte vectors (L4 rounded up to whole
-    // blocks; the tail of L past the last full vector is swept as scalars).
-    const int64_t L4 = L / 4;
-    const int64_t L4r = (L4 + kThreads - 1) / kThreads * kThreads;
-    const uint4* buf4 = reinterpret_cast<const uint4*>(buf);
-    auto sweep = [&](auto&& visit) __attribute__((always_inline)) {
-      for (int64_t i = tid; i < L4r; i += kThreads) {
-        const uint4 x = i < L4 ? buf4[i] : make_uint4(kEmpty, kEmpty, kEmpty, kEmpty);
-        visit(x.x);
-        visit(x.y);
-        visit(x.z);
-        visit(x.w);
-      }
-      for (int64_t i = 4 * L4 + tid; i < 4 * L4 + kThreads; i += kThreads)
-        visit(i < L ? buf[i] : kEmpty);
-    };
-    // hist[p] holds partition p's landings, counted as the walks recorded them.
-    if (tid == 0) {
-      uint32_t run = 0;
-      for (uint32_t p = 0; p < parts; ++p) {
-        pstart[p] = run;
-        run += hist[p];
-        hist[p] = pstart[p];  // the bucket's cursor
-      }
-      pstart[parts] = run;
-    }
+    for (uint32_t p = tid; p < parts; p += kThreads)
+      pcount[p] = hist[p] < (uint32_t)kCCap ? hist[p] : (uint32_t)kCCap;
+    const int n_ovf = sh_i32[7];
     __syncthreads();
-    sweep([&](uint32_t v) {
-      const uint32_t b = v == kEmpty ? 0u : part_of(v, parts);
-      const uint32_t slot = wave_bucket_slot(hist, b, v != kEmpty);
-      if (v != kEmpty) sorted[slot] = v;
-    });
+
+    // ---- B. the overflow (landings past a full bucket) by partition --------
+    // Rare (a partition far above its average, as when a few pins take most
+    // landings): a histogram sweep and a scatter sweep of the list.
+    if (n_ovf > 0) {
+      const int64_t nr = ((int64_t)n_ovf + kThreads - 1) / kThreads * kThreads;
+      for (uint32_t b = tid; b < parts; b += kThreads) hist[b] = 0u;
+      __syncthreads();
+      for (int64_t i = tid; i < nr; i += kThreads) {
+        const uint32_t v = i < n_ovf ? ovf[i] : kEmpty;
+        wave_hist_add(hist, v == kEmpty ? 0u : part_of(v, parts), v != kEmpty);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t run = 0;
+        for (uint32_t p = 0; p < parts; ++p) {
+          pstart[p] = run;
+          run += hist[p];
+          hist[p] = pstart[p];  // the partition's cursor
+        }
+        pstart[parts] = run;
+      }
+      __syncthreads();
+      for (int64_t i = tid; i < nr; i += kThreads) {
+        const uint32_t v = i < n_ovf ? ovf[i] : kEmpty;
+        const uint32_t b = v == kEmpty ? 0u : part_of(v, parts);
+        const uint32_t slot = wave_bucket_slot(hist, b, v != kEmpty);
+        if (v != kEmpty) ovf_sorted[slot] = v;
+      }
+    } else {
+      for (uint32_t p = tid; p <= parts; p += kThreads) pstart[p] = 0u;
+    }
     __syncthreads();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     // From here hist[c] counts the listed pins of count c < kGBins and
@@ -635,10 +668,13 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     if (tid == 0) sh_i32[6] = 0;
     __syncthreads();
 
-    // ---- C. count each partition's bucket in LDS ----------------------------
+    // ---- C. count each partition's landings in LDS ---------------------------
+    // Partition p: its bucket, then its overflow landings.
     for (uint32_t p = 0; p < parts; ++p) {
       const int list0 = sh_i32[0];
-      const int64_t b0 = pstart[p], b1 = pstart[p + 1];
+      const uint32_t* bkt = buckets + (int64_t)p * kCCap;
+      const int64_t n1 = pcount[p];
+      const int64_t o0 = pstart[p], n = n1 + (pstart[p + 1] - o0);
       uint32_t split = 1;
       for (uint32_t sp = 0; sp < split;) {
         for (int i = tid; i < kCSlots; i += kThreads) {
@@ -647,8 +683,8 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         }
         if (tid == 0) sh_i32[1] = 0;
         __syncthreads();
-        for (int64_t i = b0 + tid; i < b1; i += kThreads) {
-          const uint32_t v = sorted[i];
+        for (int64_t i = tid; i < n; i += kThreads) {
+          const uint32_t v = i < n1 ? bkt[i] : ovf_sorted[o0 + (i - n1)];
           if (split_of(v, split) != sp) continue;
           uint32_t h = home_of(v);
           bool placed = false;
@@ -878,11 +914,12 @@ int64_t hard_negative_blocks(int64_t num_queries) {
   return num_queries < kGMaxBlocks ? num_queries : kGMaxBlocks;
 }
 
-// Per resident workgroup: the landing buffer (L words), the landings by
-// partition (L words) and the (pin, count) list (2 L words), rounded to 256
-// bytes.
+// Per resident workgroup: the partitions' buckets (kCCap words each), the
+// overflow list and its copy by partition (L words each) and the (pin, count)
+// list (2 L words), rounded to 256 bytes.
 static int64_t hard_negative_ws_words(int64_t landings) {
-  return (4 * landings + 63) / 64 * 64;
+  const int64_t parts = (landings + kCPerPart - 1) / kCPerPart;
+  return (parts * kCCap + 4 * landings + 63) / 64 * 64;
 }
 
 size_t hard_negative_workspace(int64_t landings, int64_t num_queries) {

@@ -129,12 +129,14 @@ def test_hard_negatives_validation(L):
     n = ctypes.c_size_t(1)
     assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(hp()), 4, ctypes.byref(n)) == 0
     assert n.value == 0  # 16384 landings: on chip
-    big = hp(hops=5)     # 20480 landings: landings twice + (pin, count) list, 16 B each
+    big = hp(hops=5)     # 20480 landings: 3 partitions' buckets of 12288, overflow
+    per = 4 * (3 * 12288 + 4 * 20480)  # list twice, (pin, count) list
+    assert per % 256 == 0
     assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(big), 4, ctypes.byref(n)) == 0
-    assert n.value == 4 * 16 * 20480
+    assert n.value == 4 * per
     assert lib.pinsage_hard_negatives_workspace_size(ctypes.byref(big), 10_000,
                                                      ctypes.byref(n)) == 0
-    assert n.value == 256 * 16 * 20480  # at most 256 resident workgroups
+    assert n.value == 256 * per  # at most 256 resident workgroups
     assert call(_graph(L), big, FAKE, 4, FAKE) == L.PINSAGE_EWORKSPACE
     assert call(_graph(L), big, FAKE, 4, FAKE, FAKE, 100) == L.PINSAGE_EWORKSPACE
     assert call(_graph(L), big, FAKE, 4, FAKE, FAKE + 8, 1 << 30) == L.PINSAGE_EINVAL

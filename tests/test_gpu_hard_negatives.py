@@ -182,8 +182,9 @@ def test_global_table_partition_split(orc):
     # One board joined to 30,000 pins that all fall in the first of the three
     # hash partitions of 4096 walks x 5 landings: about 15,000 distinct pins in
     # one partition, more than the 12,288 LDS slots, so the kernel splits it by
-    # its second hash and counts each part again. The ranking must still equal
-    # the oracle's.
+    # its second hash and counts each part again; its landings also overflow
+    # the partition's workspace bucket. The ranking must still equal the
+    # oracle's.
     walks, hops = 4096, 5
     parts = (walks * hops + 8191) // 8192
     chosen = [v for v in range(1, 400_000) if (_fmix32(v) * parts) >> 32 == 0][:30_000]
@@ -198,3 +199,6 @@ def test_global_table_partition_split(orc):
                                                           lo, hi, k))
     visits = orc.walk_visits(off, col, P, 21, 0, walks, hops)[0]
     assert len(np.unique(visits[(visits >= 0) & (visits != 0)])) > 12_288
+    # Every landing falls in that partition, more than its 12,288-landing
+    # workspace bucket holds: the rest takes the overflow list.
+    assert np.count_nonzero((visits >= 0) & (visits != 0)) > 12_288
