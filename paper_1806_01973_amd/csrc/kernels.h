@@ -74,11 +74,11 @@ struct HardNegLaunch {
   unsigned long long* total_steps;  // nullable; accumulated (caller zeroes)
   const void* table;                // nullable: the graph's walk table
 };
-// Walk budgets above kMaxOnChipLandings buffer a query's landings in the
-// workspace, bucket them by hash partition and count each bucket in LDS
-// (hard_negative_workspace bytes: the landings twice and a (pin, count) list
-// per resident workgroup), and
-// need rank_hi <= kMaxGlobalRank.
+// Walk budgets above kMaxOnChipLandings bucket a query's landings by hash
+// partition in the workspace as the walks record them and count each bucket
+// in LDS (hard_negative_workspace bytes per resident workgroup: the buckets,
+// an overflow list twice and a (pin, count) list), and need
+// rank_hi <= kMaxGlobalRank.
 constexpr int64_t kMaxOnChipLandings = 16384;
 constexpr int64_t kMaxLandings = 1ll << 22;
 constexpr int kMaxGlobalRank = 8192;
