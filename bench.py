@@ -418,10 +418,18 @@ def roofline_of(kernels, wl):
                 "hard_neg": "hardneg.hip"}.get(dominant, "")
     tr = load_traffic(src_file, wl.name) if src_file else None
     frac = (kd["achieved_GBs"] / HBM_PEAK_GBS) if "achieved_GBs" in kd else None
+    walk_like = "edge_steps_per_launch" in kd
     out = {"kernel": dominant, "bound": "hbm", "achieved": kd.get("achieved_GBs"),
            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": frac,
            "traffic": None if tr is None else tr["bytes_per_launch"],
-           "bytes": "algorithmic (every gathered row counted once per use)"}
+           "bytes": ("algorithmic (the edge steps' reads: one 16-byte walk-table entry, or "
+                     "an offset pair and a column id, per step)" if walk_like else
+                     "algorithmic (every gathered row counted once per use)")}
+    if walk_like:
+        # Walk kernels are bound by the rate of dependent random reads, not by
+        # HBM bytes: their time against that floor sits beside the HBM figures.
+        out["random_read_floor_ms"] = kd.get("random_read_floor_ms")
+        out["frac_of_random_read_floor"] = kd.get("frac_of_random_read_floor")
     if frac is not None and frac > 1.0:
         # More algorithmic bytes per second than HBM can deliver: the caches
         # (L2, MALL) serve part of the re-gathered rows, so this is not an HBM

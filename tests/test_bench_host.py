@@ -90,6 +90,19 @@ def test_dominant_kernel_roofline_and_traffic(monkeypatch, tmp_path):
     assert r["traffic"] is None
 
 
+def test_walk_bound_roofline():
+    # A walk-dominated line (the hard negative bench) labels its algorithmic
+    # bytes as the edge steps' reads and carries the random-read floor.
+    k = {"hard_neg": {"ms_per_step": 12.9, "avg_ms": 12.9}}
+    bench.walk_rates(k["hard_neg"], 536_870_912, False, table=True)
+    r = bench.roofline_of(k, synth.WORKLOADS["medium"])
+    assert r["kernel"] == "hard_neg" and r["bound"] == "hbm"
+    assert "walk-table entry" in r["bytes"]
+    assert r["achieved"] == pytest.approx(536_870_912 * 16 / (12.9e-3) / 1e9)
+    assert r["random_read_floor_ms"] == pytest.approx(536_870_912 / bench.RANDOM_READS_PER_S * 1e3)
+    assert r["frac_of_random_read_floor"] == pytest.approx(r["random_read_floor_ms"] / 12.9)
+
+
 def test_counter_summaries_match_current_sources():
     # Every committed counter summary was taken on the kernel source now in the
     # tree (else the bench reports no traffic for it, and the summary is stale).
