@@ -550,31 +550,75 @@ __device__ __forceinline__ int pow2_at_least(int n) {
   return p;
 }
 
-// Scans hist[0, kGBins) from the top: the bin holding the want-th largest
-// element (0-based) and the number of elements in the bins above it.
-__device__ __forceinline__ void top_bin(const uint32_t* hist, int64_t want, int* bin,
-                                        int64_t* above) {
-  int64_t cum = 0;
-  int b = kGBins - 1;
-  for (; b > 0; --b) {
-    if (cum + hist[b] > want) break;
-    cum += hist[b];
+// Scans hist[0, kGBins) from the top for the bin holding the want-th largest
+// element (0-based) and the number of elements in the bins above it; bin 0
+// (with every element above it) when no bin above 0 holds it. The whole block
+// calls it (it contains barriers): thread t takes bins kGBins - 1 - 4 t - j,
+// j < 4, a block scan gives the elements above each thread's four, and the
+// thread holding the bin where the running count passes `want` writes the
+// result to *bin and *above (shared).
+static_assert(kGBins == 4 * kThreads, "four count bins per thread");
+__device__ __forceinline__ void top_bin_block(const uint32_t* hist, int64_t want, int tid,
+                                              int* wave_tot, int* bin, int64_t* above) {
+  const int wave = tid >> 6, lane = tid & (kWave - 1);
+  int c[4], sum = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    c[j] = (int)hist[kGBins - 1 - 4 * tid - j];
+    sum += c[j];
   }
-  *bin = b;
-  *above = cum;
+  int total;
+  int64_t cum = block_exclusive_sum(sum, wave, lane, wave_tot, &total);
+  if (tid == 0) {
+    *bin = 0;
+    *above = (int64_t)total - (int64_t)hist[0];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int b = kGBins - 1 - 4 * tid - j;
+    if (b >= 1 && cum <= want && cum + c[j] > want) {
+      *bin = b;
+      *above = cum;
+    }
+    cum += c[j];
+  }
+  __syncthreads();
 }
 
-// From the bottom: the bin holding the want-th smallest (0-based).
-__device__ __forceinline__ void low_bin(const uint32_t* hist, int nbins, int64_t want, int* bin,
-                                        int64_t* below) {
-  int64_t cum = 0;
-  int b = 0;
-  for (; b < nbins - 1; ++b) {
-    if (cum + hist[b] > want) break;
-    cum += hist[b];
+// From the bottom: the bin of hist[0, nbins) holding the want-th smallest
+// element (0-based) and the number of elements below it; bin nbins - 1 (with
+// every element below it) when no lower bin holds it. The bins from nbins to
+// kGBins must be zero. The whole block calls it (it contains barriers):
+// thread t takes bins 4 t + j, j < 4, and the thread holding the bin where
+// the running count passes `want` writes the result (shared).
+__device__ __forceinline__ void low_bin_block(const uint32_t* hist, int nbins, int64_t want,
+                                              int tid, int* wave_tot, int* bin,
+                                              int64_t* below) {
+  const int wave = tid >> 6, lane = tid & (kWave - 1);
+  int c[4], sum = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    c[j] = (int)hist[4 * tid + j];
+    sum += c[j];
   }
-  *bin = b;
-  *below = cum;
+  int total;
+  int64_t cum = block_exclusive_sum(sum, wave, lane, wave_tot, &total);
+  if (tid == 0) {
+    *bin = nbins - 1;
+    *below = (int64_t)total - (int64_t)hist[nbins - 1];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int b = 4 * tid + j;
+    if (b < nbins - 1 && cum <= want && cum + c[j] > want) {
+      *bin = b;
+      *below = cum;
+    }
+    cum += c[j];
+  }
+  __syncthreads();
 }
 
 template <typename OffT, bool TABLE>
@@ -603,6 +647,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
   uint32_t* ovf = buckets + (int64_t)parts * kCCap;          // up to L landings
   uint32_t* ovf_sorted = ovf + L;                           // the same, by partition
   uint32_t* list = ovf_sorted + L;                          // up to L (pin, count) pairs
+  __shared__ int scan_tot[kWaves];            // top_bin_block's wave sums
   __shared__ uint32_t pstart[kMaxParts + 1];  // overflow landings by partition
   __shared__ uint32_t pcount[kMaxParts];      // landings in each partition's bucket
   uint32_t my_steps = 0;
@@ -745,16 +790,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
     int64_t n_above = D;
     const int n_big = sh_i32[6];
     if (D > R && n_big < R) {
-      if (tid == 0) {
-        int b;
-        int64_t above;
-        top_bin(hist, R - 1 - n_big, &b, &above);
-        sh_i32[1] = b;
-        sh_i64[0] = n_big + above;
-      }
-      __syncthreads();
+      top_bin_block(hist, R - 1 - n_big, tid, scan_tot, &sh_i32[1], &sh_i64[0]);
       cstar = (uint32_t)sh_i32[1];
-      n_above = sh_i64[0];
+      n_above = n_big + sh_i64[0];
     } else if (D > R) {
       __syncthreads();  // every wave has read n_big before hist is cleared
       for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
@@ -765,14 +803,7 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         wave_hist_add(hist, (c >> 12) < kGBins ? (c >> 12) : kGBins - 1, on);
       }
       __syncthreads();
-      if (tid == 0) {
-        int b1;
-        int64_t above;
-        top_bin(hist, R - 1, &b1, &above);
-        sh_i32[1] = b1;
-        sh_i64[0] = above;
-      }
-      __syncthreads();
+      top_bin_block(hist, R - 1, tid, scan_tot, &sh_i32[1], &sh_i64[0]);
       const uint32_t b1 = (uint32_t)sh_i32[1];
       const int64_t above1 = sh_i64[0];
       for (int b = tid; b < kGBins; b += kThreads) hist[b] = 0u;
@@ -783,16 +814,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
         wave_hist_add(hist, c & (kGBins - 1), in && (c >> 12) == b1);
       }
       __syncthreads();
-      if (tid == 0) {
-        int b2;
-        int64_t above2;
-        top_bin(hist, R - 1 - above1, &b2, &above2);
-        sh_i32[2] = b2;
-        sh_i64[1] = above1 + above2;
-      }
-      __syncthreads();
+      top_bin_block(hist, R - 1 - above1, tid, scan_tot, &sh_i32[2], &sh_i64[1]);
       cstar = (b1 << 12) | (uint32_t)sh_i32[2];
-      n_above = sh_i64[1];
+      n_above = above1 + sh_i64[1];
     }
 
     // ---- 2. pins counted more than c*, by count desc, id asc ---------------
@@ -831,16 +855,9 @@ __global__ __launch_bounds__(kThreads) void hard_negative_global_kernel(HardNegL
           atomicAdd(&hist[(k >> sft) & (nb - 1)], 1u);
         }
         __syncthreads();
-        if (tid == 0) {
-          int d;
-          int64_t below;
-          low_bin(hist, nb, want, &d, &below);
-          sh_i32[4] = d;
-          sh_i64[2] = want - below;
-        }
-        __syncthreads();
+        low_bin_block(hist, nb, want, tid, scan_tot, &sh_i32[4], &sh_i64[2]);
         prefix |= (uint32_t)sh_i32[4] << sft;
-        want = sh_i64[2];
+        want -= sh_i64[2];
         __syncthreads();
       }
       // prefix is the need-th smallest id of the class: gather ids <= prefix.
